@@ -1,0 +1,104 @@
+"""RRQ oracle: plain CPU implementations of construction and reconstruction.
+
+TEST INFRASTRUCTURE. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package. The product path
+(``paper_2608_04048_amd``) never imports it.
+
+Two independent writings of the same definition:
+* ``rrq_oracle.py`` (numpy, vectorised over groups): the readable definition;
+* ``rrq_oracle.c`` (plain scalar C, OpenMP over groups): the same steps for
+  inputs too large for numpy, and the timed CPU baseline.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+from . import rrq_oracle as np_oracle  # noqa: F401  (re-export)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "rrq_oracle.c")
+_LIB = os.path.join(_HERE, "librrq_oracle.so")
+
+CFLAGS = ["-O2", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-std=c11",
+          "-fPIC", "-shared", "-Wall", "-Wextra"]
+
+_lib = None
+
+
+def build_c_oracle(force: bool = True) -> str:
+    """Compile the C oracle into oracle/librrq_oracle.so with gcc."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", *CFLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build_c_oracle(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        lib.rrq_oracle_construct.argtypes = [P, ctypes.c_int64, ctypes.c_int32,
+                                             ctypes.c_int32, P, P, P]
+        lib.rrq_oracle_construct.restype = ctypes.c_int
+        lib.rrq_oracle_reconstruct.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32,
+                                               ctypes.c_int32, ctypes.c_int32,
+                                               ctypes.c_int32, P]
+        lib.rrq_oracle_reconstruct.restype = ctypes.c_int
+        lib.rrq_oracle_threads.argtypes = []
+        lib.rrq_oracle_threads.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    assert a.flags["C_CONTIGUOUS"]
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def c_construct(w_bits: np.ndarray, group_size: int, n_stages: int):
+    """C oracle construction of flat bfloat16 bits -> (codes, scales, zeros)."""
+    lib = _load()
+    w = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
+    n = w.size
+    codes = np.empty((n_stages, n // 16), dtype=np.uint32)
+    scales = np.empty((n_stages, n // group_size), dtype=np.float32)
+    zeros = np.empty((n_stages, n // group_size), dtype=np.float32)
+    rc = lib.rrq_oracle_construct(_ptr(w), n, group_size, n_stages,
+                                  _ptr(codes), _ptr(scales), _ptr(zeros))
+    if rc == 2:
+        raise ValueError("RRQ oracle: inputs must be finite")
+    if rc != 0:
+        raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
+    return codes, scales, zeros
+
+
+def c_reconstruct(codes: np.ndarray, scales: np.ndarray, zeros: np.ndarray,
+                  group_size: int, k_stages: int, out_dtype: str = "f32"):
+    """C oracle prefix-k reconstruction -> float32 or bfloat16 bits (uint16)."""
+    lib = _load()
+    codes = np.ascontiguousarray(codes, dtype=np.uint32)
+    scales = np.ascontiguousarray(scales, dtype=np.float32)
+    zeros = np.ascontiguousarray(zeros, dtype=np.float32)
+    S = codes.shape[0]
+    n = codes.shape[1] * 16
+    bf16 = out_dtype == "bf16"
+    out = np.empty(n, dtype=np.uint16 if bf16 else np.float32)
+    rc = lib.rrq_oracle_reconstruct(_ptr(codes), _ptr(scales), _ptr(zeros), n,
+                                    group_size, S, k_stages, int(bf16), _ptr(out))
+    if rc != 0:
+        raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
+    return out
+
+
+def c_threads() -> int:
+    """OpenMP threads the C oracle runs with."""
+    return int(_load().rrq_oracle_threads())

@@ -1,0 +1,177 @@
+/*
+ * Plain scalar CPU oracle for RRQ construction and prefix reconstruction.
+ *
+ * TEST INFRASTRUCTURE. Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load this library. It shares no source, header
+ * or table with the HIP library, and the HIP library never calls it.
+ *
+ * It computes, group by group and element by element, the same fixed reading
+ * of the paper as the numpy oracle (oracle/rrq_oracle.py), written a second
+ * time as straight C so that large inputs finish in seconds:
+ *   Eq. 1-3   per-group affine quantizer and its residual;
+ *   Eq. 4-7   base stage on the weights, each later stage on the residual;
+ *   Alg. 1    quantize / store / dequantize / subtract, no base checkpoint;
+ *   Eq. 8     prefix reconstruction, also Eq. 18-19;
+ *   Sec. 4.1  2-bit RTN stages, group size 128 (32 and 64 also accepted).
+ *
+ * Build: gcc -O2 -fopenmp -ffp-contract=off (no fast-math): every float
+ * operation below is one IEEE binary32 operation rounded to nearest-even,
+ * with no fused multiply-add.
+ */
+#include <math.h>
+#include <omp.h>
+#include <stdint.h>
+#include <string.h>
+
+#define ORACLE_OK 0
+#define ORACLE_ERR_ARGS 1
+#define ORACLE_ERR_NONFINITE 2
+
+static float bf16_to_f32(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+/* Nearest bfloat16, ties to even (finite inputs). */
+static uint16_t f32_to_bf16(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    uint32_t trunc = u >> 16;
+    uint32_t rest = u & 0xFFFFu;
+    if (rest > 0x8000u || (rest == 0x8000u && (trunc & 1u)))
+        trunc += 1u;
+    return (uint16_t)trunc;
+}
+
+/*
+ * One asymmetric min-max RTN stage of one group (Eq. 1-3) with 2^bits - 1
+ * steps: writes the codes Q[0..G), the scale and zero-point, and replaces
+ * r[j] by r[j] - rhat[j] when update_residual is set.
+ */
+static void rtn_stage_group(float *r, int G, int bits, int update_residual,
+                            uint8_t *Q, float *s_out, float *z_out)
+{
+    const int maxq = (1 << bits) - 1;
+    float lo = 0.0f, hi = 0.0f;           /* zero is always in the range */
+    for (int j = 0; j < G; ++j) {
+        if (r[j] < lo) lo = r[j];
+        if (r[j] > hi) hi = r[j];
+    }
+    float d = hi - lo;
+    float s = d / (float)maxq;
+    if (!(s >= 0x1p-126f)) {              /* zero or subnormal: degenerate */
+        for (int j = 0; j < G; ++j) Q[j] = 0;
+        *s_out = 0.0f;
+        *z_out = 0.0f;
+        return;                            /* residual unchanged */
+    }
+    float inv = 1.0f / s;
+    float z = rintf((0.0f - lo) * inv);    /* integer zero-point */
+    z = z + 0.0f;                          /* +0 for a zero zero-point */
+    for (int j = 0; j < G; ++j) {
+        float t = r[j] * inv;
+        /* t + z is exact in double at every place where its rounding to an
+         * integer is decided; rint rounds ties to even. */
+        double q = rint((double)t + (double)z);
+        if (q < 0.0) q = 0.0;
+        if (q > (double)maxq) q = (double)maxq;
+        Q[j] = (uint8_t)q;
+        if (update_residual) {
+            float qz = (float)Q[j] - z;    /* exact */
+            float rhat = qz * s;
+            r[j] = r[j] - rhat;
+        }
+    }
+    *s_out = s;
+    *z_out = z;
+}
+
+/*
+ * Construct the RRQ package of n binary32-widened bfloat16 weights W (flat,
+ * row-major; groups are G consecutive elements). Outputs, all owned by the
+ * caller: codes [S][n/16] uint32 (element e -> word e/16, bits 2(e%16)),
+ * scales [S][n/G], zeros [S][n/G].
+ */
+int rrq_oracle_construct(const uint16_t *W, int64_t n, int32_t G, int32_t S,
+                         uint32_t *codes, float *scales, float *zeros)
+{
+    if (!W || !codes || !scales || !zeros) return ORACLE_ERR_ARGS;
+    if (G <= 0 || G > 1024 || G % 16 != 0 || n <= 0 || n % G != 0) return ORACLE_ERR_ARGS;
+    if (S < 1 || S > 8) return ORACLE_ERR_ARGS;
+    const int64_t n_groups = n / G;
+    const int64_t words = n / 16;
+    int bad = 0;
+
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (int64_t g = 0; g < n_groups; ++g) {
+        float r[1024];
+        uint8_t Q[1024];
+        for (int j = 0; j < G; ++j) {
+            r[j] = bf16_to_f32(W[g * G + j]);
+            if (!isfinite(r[j])) bad = 1;
+        }
+        for (int k = 0; k < S; ++k) {
+            float s, z;
+            rtn_stage_group(r, G, 2, k + 1 < S, Q, &s, &z);
+            scales[(int64_t)k * n_groups + g] = s;
+            zeros[(int64_t)k * n_groups + g] = z;
+            for (int w = 0; w < G / 16; ++w) {
+                uint32_t word = 0;
+                for (int e = 0; e < 16; ++e)
+                    word |= (uint32_t)Q[w * 16 + e] << (2 * e);
+                codes[(int64_t)k * words + g * (G / 16) + w] = word;
+            }
+        }
+    }
+    return bad ? ORACLE_ERR_NONFINITE : ORACLE_OK;
+}
+
+/*
+ * Prefix-k reconstruction: out[e] = rhat_0[e] + rhat_1[e] + ... summed left
+ * to right in binary32, with rhat_t = (Q_t - z_t) s_t. out_bf16 selects a
+ * bfloat16 output (uint16 bit patterns, nearest-even) instead of binary32.
+ */
+int rrq_oracle_reconstruct(const uint32_t *codes, const float *scales,
+                           const float *zeros, int64_t n, int32_t G, int32_t S,
+                           int32_t k, int32_t out_bf16, void *out)
+{
+    if (!codes || !scales || !zeros || !out) return ORACLE_ERR_ARGS;
+    if (G <= 0 || G % 16 != 0 || n <= 0 || n % G != 0) return ORACLE_ERR_ARGS;
+    if (S < 1 || k < 1 || k > S) return ORACLE_ERR_ARGS;
+    const int64_t n_groups = n / G;
+    const int64_t words = n / 16;
+
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < n; ++e) {
+        const int64_t g = e / G;
+        float acc = 0.0f;
+        for (int t = 0; t < k; ++t) {
+            uint32_t word = codes[(int64_t)t * words + e / 16];
+            uint32_t q = (word >> (2 * (e % 16))) & 3u;
+            float qz = (float)q - zeros[(int64_t)t * n_groups + g];
+            float rhat = qz * scales[(int64_t)t * n_groups + g];
+            acc = (t == 0) ? rhat : acc + rhat;
+        }
+        if (out_bf16)
+            ((uint16_t *)out)[e] = f32_to_bf16(acc);
+        else
+            ((float *)out)[e] = acc;
+    }
+    return ORACLE_OK;
+}
+
+/* Number of OpenMP threads a parallel region of this library uses. */
+int rrq_oracle_threads(void)
+{
+    int n = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        n = omp_get_num_threads();
+    }
+    return n;
+}

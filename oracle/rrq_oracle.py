@@ -1,0 +1,262 @@
+"""Plain CPU oracle for Recurrent Residual Quantization (RRQ) construction and
+prefix reconstruction.
+
+TEST INFRASTRUCTURE. Only the test suite, the smoke check and the benchmark's
+CPU-baseline leg may import this module. The product path (the HIP library and
+its Python binding) never imports, links or calls anything under ``oracle/``.
+
+What it computes (paper, Sec. 3 "Recurrent Residual Quantization"):
+
+* the per-group affine quantizer of Eq. 1-3: q = x/s + z, Q = R(q),
+  residual r = x - (Q - z) s;
+* the recursion of Eq. 4-7: a base stage on the weights, then each further
+  stage quantizes the residual the stages before it left behind;
+* Algorithm 1 without a base checkpoint: quantize, store codes / scales /
+  zero-points, dequantize, subtract, repeated for every stage;
+* the prefix reconstruction of Eq. 8 (restated as Eq. 18-19 in the
+  prefill/decode appendix): the effective weight after t stages is the sum of
+  the first t dequantized stages;
+* the main configuration of Sec. 4.1: 2-bit RTN stages, 4 of them, group size
+  128, calibration-free.
+
+The paper leaves the floating-point details open; this oracle fixes them
+(readings listed in the design notes, each one also stated at its step below):
+
+* groups are G contiguous elements of the row-major (out x in) matrix, along
+  the input dimension;
+* residuals are carried in IEEE binary32 between stages;
+* range: lo = min(+0, min r), hi = max(+0, max r) (zero is always on the grid);
+* scale: s = fl(fl(hi - lo) / (2^b - 1)); a group whose s is zero or subnormal
+  is degenerate: s = z = 0, all codes 0, residual passed through unchanged;
+* inv = fl(1 / s); zero-point z = RNE(fl((0 - lo) * inv)), an integer stored
+  as binary32;
+* code: t = fl(r * inv), Q = clamp(RNE(t + z), 0, 2^b - 1) where t + z is the
+  exact sum, rounded once, ties to even;
+* dequantized stage value rhat = fl((Q - z) * s); next residual
+  r <- fl(r - rhat);
+* reconstruction after k stages: acc = rhat_0, then acc = fl(acc + rhat_t) for
+  t = 1 .. k-1 in stage order; output binary32, or bfloat16 rounded to
+  nearest-even;
+* codes are stored stage-planar, 16 two-bit codes per little-endian uint32,
+  element e of the flat matrix in word e // 16 at bits 2 (e % 16) .. +1.
+
+Inputs must be finite bfloat16 values; the oracle raises otherwise.
+
+Every step below is a separate numpy float32 operation (one IEEE rounding per
+operation, no fused multiply-add). Where a step needs an exact value (t + z),
+it is formed in float64, where it is exact; see ``_exact_round_sum``.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+F32 = np.float32
+SMALLEST_NORMAL_F32 = F32(2.0 ** -126)
+
+
+# ---------------------------------------------------------------------------
+# bfloat16 <-> binary32
+# ---------------------------------------------------------------------------
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Widen bfloat16 bit patterns (uint16) to binary32 exactly: a bfloat16 is
+    the upper half of the binary32 with the same value."""
+    bits = np.asarray(bits, dtype=np.uint16)
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round binary32 values to the nearest bfloat16, ties to even.
+
+    Written from the definition: the two bfloat16 neighbours of x are the
+    truncation of x to its upper 16 bits and the next bfloat16 away from zero;
+    pick the nearer one and on a tie the one whose last kept bit is 0. Inputs
+    here are always finite.
+    """
+    x = np.asarray(x, dtype=np.float32)
+    b = x.view(np.uint32).astype(np.uint64)
+    trunc = b >> np.uint64(16)                 # toward zero
+    rest = b & np.uint64(0xFFFF)               # dropped bits
+    half = np.uint64(0x8000)
+    odd = trunc & np.uint64(1)
+    up = (rest > half) | ((rest == half) & (odd == np.uint64(1)))
+    out = trunc + up.astype(np.uint64)         # carries into the exponent correctly
+    return out.astype(np.uint16)
+
+
+# ---------------------------------------------------------------------------
+# One RTN stage on a batch of groups (Eq. 1-3)
+# ---------------------------------------------------------------------------
+
+def _exact_round_sum(t: np.ndarray, z: np.ndarray) -> np.ndarray:
+    """RNE(t + z) of the exact sum of a binary32 t and a small integer z.
+
+    In float64 the sum is exact whenever |t| >= 1/4 (t then has no bits below
+    2^-25 and |t + z| < 8), and when |t| < 1/4 the sum lies within 1/4 of an
+    integer, so the float64 rounding cannot move it across a half-integer. In
+    both cases rounding the float64 sum to an integer, ties to even, gives the
+    rounding of the exact sum.
+    """
+    return np.rint(t.astype(np.float64) + z.astype(np.float64))
+
+
+def rtn_stage(r: np.ndarray, bits: int):
+    """Quantize a batch of groups once with asymmetric min-max RTN.
+
+    ``r``: float32 array [n_groups, G] (the weights for the base stage, the
+    residual for later stages). Returns (Q uint8 [n_groups, G], s float32
+    [n_groups], z float32 [n_groups], rhat float32 [n_groups, G]).
+
+    Eq. 1 (q = x/s + z with a scale and zero-point shared by the group),
+    Eq. 2 (Q = R(q)) and Eq. 3 (dequantized value (Q - z) s).
+    """
+    assert r.dtype == np.float32 and r.ndim == 2
+    maxq = (1 << bits) - 1
+    zero = F32(0.0)
+
+    # Range of the group, with zero included (reading: zero on the grid).
+    lo = np.minimum(r.min(axis=1), zero)
+    hi = np.maximum(r.max(axis=1), zero)
+    lo = np.where(lo == zero, zero, lo)        # canonical +0
+    hi = np.where(hi == zero, zero, hi)
+
+    d = hi - lo                                # fl(hi - lo)
+    s = d / F32(maxq)                          # fl(d / maxq), IEEE division
+    degenerate = s < SMALLEST_NORMAL_F32       # zero or subnormal scale
+
+    s_safe = np.where(degenerate, F32(1.0), s)
+    inv = F32(1.0) / s_safe                    # fl(1 / s)
+    z = np.rint((zero - lo) * inv)             # RNE(fl((0 - lo) * inv))
+    z = np.where(degenerate, zero, z) + zero   # +0 for a zero zero-point
+    inv = np.where(degenerate, zero, inv)
+    s = np.where(degenerate, zero, s)
+
+    t = r * inv[:, None]                       # fl(r * inv)
+    q = _exact_round_sum(t, z[:, None])        # RNE(t + z), one rounding
+    Q = np.clip(q, 0, maxq)
+    Q = np.where(degenerate[:, None], 0.0, Q).astype(np.uint8)
+
+    qz = Q.astype(np.float32) - z[:, None]     # exact small integer
+    rhat = qz * s[:, None]                     # fl((Q - z) * s)
+    rhat = np.where(degenerate[:, None], zero, rhat)
+    return Q, s.astype(np.float32), z.astype(np.float32), rhat.astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# Packing of 2-bit codes
+# ---------------------------------------------------------------------------
+
+def pack_codes(Q: np.ndarray) -> np.ndarray:
+    """Pack 2-bit codes [n] (n % 16 == 0) into uint32 words: element e goes to
+    word e // 16, bits 2 (e % 16) and 2 (e % 16) + 1."""
+    Q = np.asarray(Q, dtype=np.uint32).reshape(-1, 16)
+    assert int(Q.max(initial=0)) <= 3
+    shifts = (2 * np.arange(16, dtype=np.uint32))[None, :]
+    return np.bitwise_or.reduce(Q << shifts, axis=1).astype(np.uint32)
+
+
+def unpack_codes(words: np.ndarray) -> np.ndarray:
+    """Inverse of ``pack_codes``."""
+    words = np.asarray(words, dtype=np.uint32).reshape(-1, 1)
+    shifts = (2 * np.arange(16, dtype=np.uint32))[None, :]
+    return ((words >> shifts) & np.uint32(3)).astype(np.uint8).reshape(-1)
+
+
+# ---------------------------------------------------------------------------
+# Construction (Algorithm 1, no base checkpoint; Eq. 4-7)
+# ---------------------------------------------------------------------------
+
+def _check_shape(n_elems: int, group_size: int):
+    if n_elems <= 0 or n_elems % group_size != 0 or n_elems % 16 != 0:
+        raise ValueError("element count must be a positive multiple of the group size and of 16")
+
+
+def construct_f32(x: np.ndarray, group_size: int, n_stages: int, bits: int = 2):
+    """Run the RRQ recursion on binary32 weights x (flat, row-major).
+
+    Returns per-stage codes Q [S, n] (uint8), scales [S, n/G], zeros [S, n/G],
+    the dequantized stage values rhat [S, n] and the final residual [n].
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
+    _check_shape(x.size, group_size)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("RRQ oracle: inputs must be finite")
+    n_groups = x.size // group_size
+    r = x.reshape(n_groups, group_size).copy()
+    Qs, ss, zs, rhats = [], [], [], []
+    for k in range(n_stages):
+        # Stage 0 quantizes the weights (base stage), stage k >= 1 the residual
+        # left by stages 0..k-1 (Eq. 4-7; Algorithm 1's loop body).
+        Q, s, z, rhat = rtn_stage(r, bits)
+        Qs.append(Q.reshape(-1))
+        ss.append(s)
+        zs.append(z)
+        rhats.append(rhat.reshape(-1))
+        r = r - rhat                           # R_k = R_{k-1} - Rhat_k
+    return (np.stack(Qs), np.stack(ss), np.stack(zs), np.stack(rhats),
+            r.reshape(-1))
+
+
+def construct(w_bits: np.ndarray, rows: int, cols: int, group_size: int,
+              n_stages: int):
+    """The package of the C-ABI call rrq_construct: bfloat16 weights [rows, cols]
+    (as uint16 bit patterns) -> codes [S, n/16] uint32, scales [S, n/G]
+    float32, zeros [S, n/G] float32."""
+    if cols % group_size != 0:
+        raise ValueError("cols must be a multiple of the group size")
+    w_bits = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
+    assert w_bits.size == rows * cols
+    x = bf16_bits_to_f32(w_bits)
+    Q, s, z, _, _ = construct_f32(x, group_size, n_stages, bits=2)
+    codes = np.stack([pack_codes(Q[k]) for k in range(n_stages)])
+    return codes, s, z
+
+
+# ---------------------------------------------------------------------------
+# Prefix reconstruction (Eq. 8, Eq. 18-19)
+# ---------------------------------------------------------------------------
+
+def dequant_stage(codes_k: np.ndarray, s_k: np.ndarray, z_k: np.ndarray,
+                  group_size: int) -> np.ndarray:
+    """rhat = fl((Q - z) s) for one stage, from its stored codes/scales/zeros."""
+    Q = unpack_codes(codes_k).reshape(-1, group_size).astype(np.float32)
+    qz = Q - np.asarray(z_k, dtype=np.float32)[:, None]     # exact small integer
+    return (qz * np.asarray(s_k, dtype=np.float32)[:, None]).reshape(-1)
+
+
+def reconstruct_f32(codes, scales, zeros, group_size: int, k_stages: int):
+    """Effective weight after k stages: rhat_0 + rhat_1 + ... + rhat_{k-1},
+    summed left to right in binary32."""
+    codes = np.asarray(codes, dtype=np.uint32)
+    if not 1 <= k_stages <= codes.shape[0]:
+        raise ValueError("k_stages out of range")
+    acc = dequant_stage(codes[0], scales[0], zeros[0], group_size)
+    for t in range(1, k_stages):
+        acc = acc + dequant_stage(codes[t], scales[t], zeros[t], group_size)
+    return acc.astype(np.float32)
+
+
+def reconstruct(codes, scales, zeros, group_size: int, k_stages: int,
+                out_dtype: str = "f32"):
+    """Prefix-k reconstruction as float32, or as bfloat16 bit patterns
+    (uint16) rounded to nearest-even when out_dtype == "bf16"."""
+    acc = reconstruct_f32(codes, scales, zeros, group_size, k_stages)
+    if out_dtype == "f32":
+        return acc
+    if out_dtype == "bf16":
+        return f32_to_bf16_bits(acc)
+    raise ValueError(out_dtype)
+
+
+# ---------------------------------------------------------------------------
+# Direct fixed-bit RTN (the comparison quantizer of Sec. 3.4 / Eq. 9-14)
+# ---------------------------------------------------------------------------
+
+def direct_rtn_dequant(x: np.ndarray, group_size: int, bits: int) -> np.ndarray:
+    """Single-stage b-bit RTN of x with the same range/scale/zero-point rules,
+    dequantized; the "direct B-bit quantization" that Sec. 3.4 compares RRQ
+    with."""
+    x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1, group_size)
+    _, _, _, rhat = rtn_stage(x, bits)
+    return rhat.reshape(-1)

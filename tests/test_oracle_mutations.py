@@ -1,0 +1,155 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake (a dropped term, a wrong sign, a transposed
+operand, a wrong index, a missing step) in a copy of the numpy oracle, on the
+CPU, and checks that the battery of pins (hand-derived values, closed forms,
+invariants) rejects the mutant. The unmodified oracle must pass the same
+battery.
+"""
+
+import json
+import os
+import types
+
+import numpy as np
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(os.path.dirname(HERE), "oracle", "rrq_oracle.py")
+
+MUTATIONS = {
+    "zero_point_dropped": ("q = _exact_round_sum(t, z[:, None])", "q = _exact_round_sum(t, 0 * z[:, None])"),
+    "zero_point_sign": ("z = np.rint((zero - lo) * inv)", "z = np.rint((lo - zero) * inv)"),
+    "range_without_zero": ("lo = np.minimum(r.min(axis=1), zero)", "lo = r.min(axis=1)"),
+    "range_transposed": ("d = hi - lo ", "d = lo - hi "),
+    "steps_off_by_one": ("s = d / F32(maxq)", "s = d / F32(maxq + 1)"),
+    "floor_not_nearest": ("return np.rint(t.astype(np.float64) + z.astype(np.float64))",
+                          "return np.floor(t.astype(np.float64) + z.astype(np.float64))"),
+    "no_clamp": ("Q = np.clip(q, 0, maxq)", "Q = np.clip(q, -8, 8)"),
+    "dequant_without_zero_point": ("qz = Q.astype(np.float32) - z[:, None]", "qz = Q.astype(np.float32)"),
+    "residual_not_updated": ("r = r - rhat                           # R_k", "r = r                                  # R_k"),
+    "residual_sign": ("r = r - rhat                           # R_k", "r = r + rhat                           # R_k"),
+    "pack_msb_first": ("shifts = (2 * np.arange(16, dtype=np.uint32))[None, :]\n    return np.bitwise_or",
+                       "shifts = (30 - 2 * np.arange(16, dtype=np.uint32))[None, :]\n    return np.bitwise_or"),
+    "recon_reverse_order": ("    acc = dequant_stage(codes[0], scales[0], zeros[0], group_size)\n    for t in range(1, k_stages):\n        acc = acc + dequant_stage(codes[t], scales[t], zeros[t], group_size)",
+                            "    acc = dequant_stage(codes[k_stages - 1], scales[k_stages - 1], zeros[k_stages - 1], group_size)\n    for t in range(k_stages - 2, -1, -1):\n        acc = acc + dequant_stage(codes[t], scales[t], zeros[t], group_size)"),
+    "recon_drops_last_stage": ("for t in range(1, k_stages):", "for t in range(1, k_stages - 1):"),
+    "bf16_truncates": ("out = trunc + up.astype(np.uint64)", "out = trunc"),
+    "degenerate_threshold_ignored": ("degenerate = s < SMALLEST_NORMAL_F32", "degenerate = s < 0"),
+}
+
+
+def _module_from(source: str) -> types.ModuleType:
+    mod = types.ModuleType("rrq_oracle_mutant")
+    exec(compile(source, SRC, "exec"), mod.__dict__)
+    return mod
+
+
+def _f(hexbits):
+    return np.array([int(h, 16) for h in hexbits], dtype=np.uint32).view(np.float32)
+
+
+def _battery(o) -> list:
+    """Run the pins against module ``o``; return the names of failed pins."""
+    failed = []
+    with open(os.path.join(HERE, "golden", "hand_cases.json")) as fh:
+        golden = json.load(fh)
+
+    def check(name, fn):
+        try:
+            with np.errstate(all="ignore"):
+                ok = fn()
+        except Exception:
+            ok = False
+        if not ok:
+            failed.append(name)
+
+    def golden_construct():
+        for case in golden["construct"]:
+            x = _f(case["x"])
+            bits = (x.view(np.uint32) >> 16).astype(np.uint16)
+            codes, s, z = o.construct(bits, 1, x.size, case["G"], 4)
+            for k, st in enumerate(case["stages"]):
+                if "codes" in st and not np.array_equal(codes[k], [int(h, 16) for h in st["codes"]]):
+                    return False
+                if s[k].view(np.uint32)[0] != int(st["s"], 16) or z[k].view(np.uint32)[0] != int(st["z"], 16):
+                    return False
+            for key, want in case.get("recon_f32", {}).items():
+                want_bits = x.view(np.uint32) if want == "x" else _f(want).view(np.uint32)
+                if not np.array_equal(o.reconstruct(codes, s, z, case["G"], int(key)).view(np.uint32), want_bits):
+                    return False
+            for key, want in case.get("recon_bf16", {}).items():
+                got = o.reconstruct(codes, s, z, case["G"], int(key), "bf16")
+                if not np.array_equal(got, [int(h, 16) for h in want]):
+                    return False
+        return True
+
+    def golden_reconstruct():
+        for case in golden["reconstruct"]:
+            codes = np.array([[int(h, 16) for h in row] for row in case["codes"]], dtype=np.uint32)
+            sc, ze = _f(case["scales"]).reshape(-1, 1), _f(case["zeros"]).reshape(-1, 1)
+            for dt, table in (("f32", case.get("recon_f32", {})), ("bf16", case.get("recon_bf16", {}))):
+                for key, spec in table.items():
+                    got = o.reconstruct(codes, sc, ze, case["G"], int(key), dt)
+                    got = got.view(np.uint32 if dt == "f32" else np.uint16).astype(np.int64)
+                    want = np.full(got.size, int(spec["default"], 16))
+                    for nm, v in spec.items():
+                        if nm.startswith("e"):
+                            want[int(nm[1:])] = int(v, 16)
+                    if not np.array_equal(got, want):
+                        return False
+        return True
+
+    def invariants():
+        rng = np.random.default_rng(11)
+        x = (rng.standard_normal(128 * 400) * 0.02).astype(np.float32)
+        x = np.where(rng.random(x.size) < 1e-2, x * 20, x).astype(np.float32)
+        x = o.bf16_bits_to_f32(o.f32_to_bf16_bits(x))
+        Q, s, z, rhat, _ = o.construct_f32(x, 128, 4)
+        if Q.max() > 3 or not np.all(np.isin(z, [0, 1, 2, 3])):
+            return False
+        r = x.reshape(-1, 128)
+        for k in range(4):
+            r_next = (r - rhat[k].reshape(-1, 128)).astype(np.float32)
+            if np.any(np.abs(r_next) > 0.5 * s[k][:, None].astype(np.float64) * (1 + 2.0 ** -20) + (s[k][:, None] == 0) * 1e30):
+                return False
+            r = r_next
+        return True
+
+    def crossover():
+        ratios = {}
+        for K in (3.0, 4.5, 6.0):
+            x = np.concatenate([np.linspace(-0.5, 0.5, 127), [K]]).astype(np.float32)
+            _, _, _, rhat, _ = o.construct_f32(x, 128, 2)
+            rrq = (rhat[0] + rhat[1]).astype(np.float32)
+            direct = o.direct_rtn_dequant(x, 128, 4)
+            ratios[K] = np.abs(x - rrq.astype(np.float64)).sum() / np.abs(x - direct.astype(np.float64)).sum()
+        return abs(ratios[4.5] - 1) < 1e-3 and ratios[3.0] > 1.4 and ratios[6.0] < 0.9
+
+    def tiny_constant_degenerate():
+        c = np.full(32, 2.0 ** -127, dtype=np.float32)    # bfloat16-exact, s subnormal
+        bits = (c.view(np.uint32) >> 16).astype(np.uint16)
+        codes, s, z = o.construct(bits, 1, 32, 32, 4)
+        return np.all(s == 0) and np.all(codes == 0)
+
+    check("golden_construct", golden_construct)
+    check("golden_reconstruct", golden_reconstruct)
+    check("invariants", invariants)
+    check("crossover", crossover)
+    check("tiny_constant_degenerate", tiny_constant_degenerate)
+    return failed
+
+
+def test_unmodified_oracle_passes_battery():
+    with open(SRC) as fh:
+        assert _battery(_module_from(fh.read())) == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutant_is_caught(name):
+    with open(SRC) as fh:
+        src = fh.read()
+    old, new = MUTATIONS[name]
+    assert src.count(old) == 1, f"mutation anchor not found once: {old!r}"
+    failed = _battery(_module_from(src.replace(old, new)))
+    assert failed, f"mutation {name} passed every pin"

@@ -1,0 +1,380 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these tests compares the oracle with itself: each one checks a value
+derived by hand (tests/golden/hand_cases.json), a closed form from the paper,
+an invariant of round-to-nearest, a brute-force enumeration on tiny groups, or
+an exhaustive special case. Each names the passage it follows.
+"""
+
+import itertools
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import rrq_oracle as o
+import oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def _f(hexbits):
+    return np.array([int(h, 16) for h in hexbits], dtype=np.uint32).view(np.float32)
+
+
+def _load_golden():
+    with open(os.path.join(HERE, "golden", "hand_cases.json")) as fh:
+        return json.load(fh)
+
+
+GOLDEN = _load_golden()
+
+
+def _construct_both(x_f32, G, S):
+    """Run both oracle writings on bfloat16-exact inputs; they must agree."""
+    bits = (x_f32.view(np.uint32) >> 16).astype(np.uint16)
+    assert np.array_equal(o.bf16_bits_to_f32(bits).view(np.uint32), x_f32.view(np.uint32))
+    c1, s1, z1 = o.construct(bits, 1, x_f32.size, G, S)
+    c2, s2, z2 = oracle.c_construct(bits, G, S)
+    assert np.array_equal(c1, c2)
+    assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+    assert np.array_equal(z1.view(np.uint32), z2.view(np.uint32))
+    return c1, s1, z1
+
+
+# ---------------------------------------------------------------------------
+# Hand-derived cases (Eq. 1-3, Eq. 4-8, Sec. 4.1)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", GOLDEN["construct"], ids=lambda c: c["name"])
+def test_golden_construct(case):
+    x = _f(case["x"])
+    G = case["G"]
+    codes, s, z = _construct_both(x, G, 4)
+    for k, st in enumerate(case["stages"]):
+        if "codes" in st:
+            want = np.array([int(h, 16) for h in st["codes"]], dtype=np.uint32)
+            assert np.array_equal(codes[k], want), (k, [hex(v) for v in codes[k]])
+        assert s[k].view(np.uint32)[0] == int(st["s"], 16), (k, s[k])
+        assert z[k].view(np.uint32)[0] == int(st["z"], 16), (k, z[k])
+    for key, want in case.get("recon_f32", {}).items():
+        k = int(key)
+        want_bits = x.view(np.uint32) if want == "x" else _f(want).view(np.uint32)
+        for got in (o.reconstruct(codes, s, z, G, k), oracle.c_reconstruct(codes, s, z, G, k)):
+            assert np.array_equal(got.view(np.uint32), want_bits), (k, [hex(v) for v in got.view(np.uint32)])
+    for key, want in case.get("recon_bf16", {}).items():
+        k = int(key)
+        want_bits = np.array([int(h, 16) for h in want], dtype=np.uint16)
+        for got in (o.reconstruct(codes, s, z, G, k, "bf16"),
+                    oracle.c_reconstruct(codes, s, z, G, k, "bf16")):
+            assert np.array_equal(got, want_bits)
+
+
+@pytest.mark.parametrize("case", GOLDEN["reconstruct"], ids=lambda c: c["name"])
+def test_golden_reconstruct(case):
+    G = case["G"]
+    codes = np.array([[int(h, 16) for h in row] for row in case["codes"]], dtype=np.uint32)
+    scales = _f(case["scales"]).reshape(-1, 1)
+    zeros = _f(case["zeros"]).reshape(-1, 1)
+    n = codes.shape[1] * 16
+    for dt, table in (("f32", case.get("recon_f32", {})), ("bf16", case.get("recon_bf16", {}))):
+        for key, spec in table.items():
+            k = int(key)
+            width = 32 if dt == "f32" else 16
+            want = np.full(n, int(spec["default"], 16), dtype=np.uint64)
+            for name, val in spec.items():
+                if name.startswith("e"):
+                    want[int(name[1:])] = int(val, 16)
+            for got in (o.reconstruct(codes, scales, zeros, G, k, dt),
+                        oracle.c_reconstruct(codes, scales, zeros, G, k, dt)):
+                got_bits = got.view(np.uint32 if width == 32 else np.uint16).astype(np.uint64)
+                assert np.array_equal(got_bits, want), (dt, k, [hex(v) for v in got_bits[:8]])
+
+
+# ---------------------------------------------------------------------------
+# Round-to-nearest by brute force (Eq. 1-2) on tiny groups
+# ---------------------------------------------------------------------------
+
+def _grid_error(r, Q, s, z):
+    return sum(abs(Fraction(float(rj)) - (int(q) - Fraction(float(z))) * Fraction(float(s)))
+               for rj, q in zip(r, Q))
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 6])
+def test_bruteforce_nearest_codes(n):
+    """For every code vector in {0..3}^n, the oracle's codes give the least total
+    distance to the group's grid, up to the rounding of 1/s and r/s (2^-20 s
+    per element)."""
+    rng = np.random.default_rng(100 + n)
+    for trial in range(40):
+        scale = 10.0 ** rng.uniform(-4, 2)
+        r = (rng.standard_normal((1, n)) * scale).astype(np.float32)
+        if trial % 5 == 0:
+            r[0, rng.integers(n)] *= 25          # one outlier
+        Q, s, z, _ = o.rtn_stage(r, 2)
+        s0, z0 = s[0], z[0]
+        if s0 == 0:
+            continue
+        mine = _grid_error(r[0], Q[0], s0, z0)
+        best = min(_grid_error(r[0], cand, s0, z0)
+                   for cand in itertools.product(range(4), repeat=n))
+        assert mine <= best + n * Fraction(float(s0)) * Fraction(1, 2 ** 20)
+
+
+def test_grid_and_zero_point_properties():
+    """s is (hi - lo)/3 to within its rounding, z is the integer nearest -lo/s,
+    and the 4-level grid (q - z) s spans [lo, hi] to within half a step
+    (Eq. 1: a shared scale and zero-point per group)."""
+    rng = np.random.default_rng(7)
+    r = (rng.standard_normal((2000, 64)) * rng.uniform(1e-3, 10, (2000, 1))).astype(np.float32)
+    r[::3] = np.abs(r[::3])                      # all-positive groups
+    r[1::3] = -np.abs(r[1::3])                   # all-negative groups
+    Q, s, z, _ = o.rtn_stage(r, 2)
+    lo = np.minimum(r.min(1), 0).astype(np.float64)
+    hi = np.maximum(r.max(1), 0).astype(np.float64)
+    s64, z64 = s.astype(np.float64), z.astype(np.float64)
+    assert np.all(np.abs(s64 - (hi - lo) / 3) <= 2.0 ** -22 * s64)
+    assert np.all(np.isin(z, [0, 1, 2, 3]))
+    assert np.all(z64 == np.round(z64))
+    assert np.all(np.abs(z64 - (-lo / s64)) <= 0.5 + 2.0 ** -20)
+    assert np.all((0 - z64) * s64 <= lo + 0.5 * s64 * (1 + 2.0 ** -20))
+    assert np.all((3 - z64) * s64 >= hi - 0.5 * s64 * (1 + 2.0 ** -20))
+    assert np.all(z[::3] == 0)                   # all-positive: zero is the lowest level
+    assert np.all(z[1::3] == 3)                  # all-negative: zero is the top level
+
+
+# ---------------------------------------------------------------------------
+# Invariants of the recursion (Eq. 3-8)
+# ---------------------------------------------------------------------------
+
+def _workload(seed, n_groups, G, kind):
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal(n_groups * G) * 0.02
+    if kind == "outlier":
+        x = np.where(rng.random(x.size) < 1e-3, x * 20, x)
+    elif kind == "t3":
+        x = rng.standard_t(3, x.size) * 0.02 / np.sqrt(3)
+    return o.bf16_bits_to_f32(o.f32_to_bf16_bits(x.astype(np.float32)))
+
+
+@pytest.mark.parametrize("G", [32, 64, 128])
+@pytest.mark.parametrize("kind", ["gauss", "outlier", "t3"])
+def test_stage_invariants(G, kind):
+    x = _workload(11, 3000, G, kind)
+    Q, s, z, rhat, r_final = o.construct_f32(x, G, 4)
+    assert Q.max() <= 3
+    assert np.all(np.isin(z, [0, 1, 2, 3]))
+    r = x.reshape(-1, G).astype(np.float32)
+    prev_err = None
+    acc = None
+    for k in range(4):
+        r_next = (r - rhat[k].reshape(-1, G)).astype(np.float32)
+        # Each stage leaves at most half its step (round-to-nearest, Eq. 1-3).
+        bound = 0.5 * s[k].astype(np.float64)[:, None] * (1 + 2.0 ** -20)
+        live = s[k] > 0
+        assert np.all(np.abs(r_next[live]) <= bound[live])
+        # The group's largest residual shrinks at least 3-fold per stage.
+        assert np.all(np.abs(r_next).max(1)[live] <= np.abs(r).max(1)[live] / 3 * (1 + 2.0 ** -20))
+        # Eq. 10: mean absolute error about a quarter of the step, for values
+        # spread over the cells (residual stages; Gaussian base stage).
+        # Heavy-tailed groups put most weights near the zero level at the
+        # base stage, where the error is smaller.
+        ratio = (np.abs(r_next).mean(1)[live] / s[k][live]).mean()
+        if k > 0 or kind == "gauss":
+            assert 0.2 < ratio < 0.3, ratio
+        else:
+            assert ratio < 0.3, ratio
+        # Eq. 8: reconstruction error does not grow as stages are added.
+        # (a) With the stored stage values summed exactly (float64 holds these
+        # sums exactly), per element up to the rounding of r*inv (2^-20 s),
+        # and per group maximum with no slack at all; (b) the binary32
+        # reconstruction, up to its own rounding (2 ulp of x).
+        exact = np.abs(x.astype(np.float64) - rhat[:k + 1].astype(np.float64).sum(0))
+        acc = rhat[0].copy() if acc is None else (acc + rhat[k]).astype(np.float32)
+        err = np.abs(x.astype(np.float64) - acc)
+        if prev_err is not None:
+            prev_exact, prev_f32 = prev_err
+            tol = 2.0 ** -20 * np.repeat(s[k - 1].astype(np.float64), G)
+            assert np.all(exact <= prev_exact + tol)
+            assert np.all(exact.reshape(-1, G).max(1) <= prev_exact.reshape(-1, G).max(1))
+            ulp2 = 2 * np.spacing(np.abs(x)).astype(np.float64)
+            assert np.all(err <= prev_f32 + tol + ulp2)
+        prev_err = (exact, err)
+        r = r_next
+    assert np.array_equal(r.reshape(-1).view(np.uint32), r_final.view(np.uint32))
+
+
+def test_constant_groups_exhaustive_bf16():
+    """Every finite bfloat16 value as a constant group of 32. Groups whose
+    scale would be zero or subnormal (|c| < 3 * 2^-126) are degenerate and
+    reconstruct to 0; every other constant is reconstructed exactly at every
+    prefix."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    c = o.bf16_bits_to_f32(bits)
+    keep = np.isfinite(c)
+    bits, c = bits[keep], c[keep]
+    w = np.repeat(bits, 32)
+    codes, s, z = oracle.c_construct(w, 32, 4)
+    tiny = np.abs(c.astype(np.float64)) < 3 * 2.0 ** -126
+    for k in range(1, 5):
+        rec = oracle.c_reconstruct(codes, s, z, 32, k).reshape(-1, 32)
+        assert np.all(rec == rec[:, :1])
+        exact = rec[:, 0].view(np.uint32) == (c + np.float32(0)).view(np.uint32)
+        assert np.all(exact[~tiny]), c[~tiny][~exact[~tiny]][:8]
+        assert np.all(rec[tiny, 0] == 0)
+    assert np.all(s[:, tiny] == 0) and np.all(codes[:, np.repeat(tiny, 2)] == 0)
+
+
+def test_constant_groups_fp32_exact_from_second_stage():
+    """Residual stages see binary32 values: a binary32 constant group is exact
+    from the 4-bit prefix on (the base stage alone may be 1 ulp off because
+    fl(3 fl(c/3)) need not equal c)."""
+    rng = np.random.default_rng(3)
+    u = rng.integers(0, 2 ** 32, size=200000, dtype=np.uint64).astype(np.uint32)
+    c = u.view(np.float32)
+    c = c[np.isfinite(c) & (np.abs(c) >= 2.0 ** -100)]
+    Q, s, z, rhat, _ = o.construct_f32(np.repeat(c, 32), 32, 4)
+    acc = rhat[0].reshape(-1, 32)
+    first = acc[:, 0]
+    assert np.all(np.abs(first.astype(np.float64) - c) <= np.spacing(np.abs(c)).astype(np.float64))
+    for k in range(1, 4):
+        acc = (acc + rhat[k].reshape(-1, 32)).astype(np.float32)
+        assert np.array_equal(acc[:, 0].view(np.uint32), c.view(np.uint32))
+
+
+def test_all_zero_and_signed_zero_groups():
+    x = np.zeros(64, dtype=np.float32)
+    x[::2] = -0.0
+    codes, s, z = _construct_both(x, 32, 4)
+    assert np.all(codes == 0) and np.all(s.view(np.uint32) == 0) and np.all(z.view(np.uint32) == 0)
+    rec = o.reconstruct(codes, s, z, 32, 4)
+    assert np.all(rec.view(np.uint32) == 0)          # +0, never -0
+
+
+def test_first_stage_is_plain_two_bit_rtn():
+    """With one stage RRQ is ordinary asymmetric 2-bit RTN (Sec. 3.2: the base
+    stage alone is the 2-bit operating point). Check it against an exact
+    rational evaluation of nearest-grid rounding, with the same scale and
+    zero-point."""
+    x = _workload(5, 200, 128, "outlier")
+    Q, s, z, rhat, _ = o.construct_f32(x, 128, 1)
+    X = x.reshape(-1, 128)
+    for g in range(0, 200, 17):
+        for j in range(0, 128, 5):
+            xj = Fraction(float(X[g, j]))
+            sf, zf = Fraction(float(s[0, g])), Fraction(float(z[0, g]))
+            dists = [abs(xj - (q - zf) * sf) for q in range(4)]
+            best = min(dists)
+            assert dists[Q[0].reshape(-1, 128)[g, j]] <= best + sf / 2 ** 20
+
+
+# ---------------------------------------------------------------------------
+# Closed form of Sec. 3.4 (Eq. 13) and the toy example of Table 2
+# ---------------------------------------------------------------------------
+
+def _toy_group(K):
+    return np.concatenate([np.linspace(-0.5, 0.5, 127), [K]]).astype(np.float32)
+
+
+def test_outlier_threshold_crossover():
+    """Eq. 13 with r = 0.5 and a 2+2 split predicts K > 4.5 for RRQ to beat
+    direct 4-bit quantization. With dense inliers on [-r, r] and one outlier
+    K, the 4-bit RRQ prefix and direct 4-bit RTN have equal total error at
+    K = 4.5, RRQ is worse below it and better above it."""
+    r, B, n2 = 0.5, 4, 2
+    assert r * (2 * (2 ** B - 1) / (2 ** n2 - 1) - 1) == 4.5
+    ratios = {}
+    for K in [3.0, 4.0, 4.5, 5.0, 6.0, 10.0]:
+        x = _toy_group(K)
+        _, _, _, rhat, _ = o.construct_f32(x, 128, 2)
+        rrq = (rhat[0] + rhat[1]).astype(np.float32)
+        direct = o.direct_rtn_dequant(x, 128, 4)
+        x64 = x.astype(np.float64)
+        ratios[K] = np.abs(x64 - rrq).sum() / np.abs(x64 - direct).sum()
+    assert abs(ratios[4.5] - 1.0) < 1e-3
+    assert ratios[3.0] > 1.4 and ratios[4.0] > 1.02
+    assert ratios[5.0] < 0.995 and ratios[6.0] < 0.9 and ratios[10.0] < 0.45
+    assert all(ratios[a] > ratios[b] for a, b in [(3, 4), (4, 4.5), (4.5, 5), (5, 6), (6, 10)])
+
+
+def test_table2_structure_parity_unpinned():
+    """Table 2 (toy outlier example) does not give its inlier population, so
+    its printed values cannot be reproduced: parity unpinned. What it does fix
+    structurally holds: the 2-bit column is the same quantizer for RRQ and
+    fixed-bit, and RRQ error falls with every stage."""
+    for K in (5.0, 3.0):
+        x = _toy_group(K)
+        _, _, _, rhat, _ = o.construct_f32(x, 128, 4)
+        x64 = x.astype(np.float64)
+        base = np.abs(x64 - rhat[0]).sum()
+        assert base == np.abs(x64 - o.direct_rtn_dequant(x, 128, 2)).sum()
+        acc, errs = rhat[0], [base]
+        for k in range(1, 4):
+            acc = (acc + rhat[k]).astype(np.float32)
+            errs.append(np.abs(x64 - acc).sum())
+        assert all(a > b for a, b in zip(errs, errs[1:]))
+
+
+def test_split_thresholds_table3():
+    """Table 3: exact thresholds for 4-bit splits from Eq. 13."""
+    r, B = 1.0, 4
+    thr = {n1: r * (2 * (2 ** B - 1) / (2 ** (B - n1) - 1) - 1) for n1 in (1, 2, 3)}
+    assert round(thr[1], 2) == 3.29 and thr[2] == 9 and thr[3] == 29
+
+
+# ---------------------------------------------------------------------------
+# bfloat16 rounding and packing helpers
+# ---------------------------------------------------------------------------
+
+def test_bf16_rounding_ties_and_carry():
+    cases = {  # binary32 bits -> nearest-even bfloat16 bits
+        0x3F808000: 0x3F80,   # tie, even kept
+        0x3F818000: 0x3F82,   # tie, odd rounds up
+        0x3F808001: 0x3F81,   # above tie
+        0x3F807FFF: 0x3F80,   # below tie
+        0x3FFFFFFF: 0x4000,   # carry into the exponent
+        0xBF818000: 0xBF82,   # sign symmetric
+        0x7F7FFFFF: 0x7F80,   # rounds past the largest finite to infinity
+        0x00000001: 0x0000,   # smallest subnormal
+        0x80000000: 0x8000,
+    }
+    x = np.array(list(cases), dtype=np.uint32).view(np.float32)
+    want = np.array(list(cases.values()), dtype=np.uint16)
+    assert np.array_equal(o.f32_to_bf16_bits(x), want)
+    import torch
+    assert np.array_equal(torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16), want)
+
+
+def test_pack_layout():
+    Q = np.zeros(32, dtype=np.uint8)
+    Q[0], Q[1], Q[15], Q[16] = 1, 2, 3, 3
+    words = o.pack_codes(Q)
+    assert words[0] == (1 | (2 << 2) | (3 << 30)) and words[1] == 3
+    assert np.array_equal(o.unpack_codes(words), Q)
+
+
+def test_nonfinite_rejected():
+    x = np.zeros(32, dtype=np.uint16)
+    x[3] = 0x7FC0
+    with pytest.raises(ValueError):
+        o.construct(x, 1, 32, 32, 4)
+    with pytest.raises(ValueError):
+        oracle.c_construct(x, 32, 4)
+
+
+def test_two_oracles_agree_on_random_inputs():
+    for seed, G, S in [(1, 32, 4), (2, 64, 3), (3, 128, 4), (4, 128, 1)]:
+        x = _workload(seed, 4000, G, "outlier")
+        bits = o.f32_to_bf16_bits(x)
+        c1, s1, z1 = o.construct(bits, 1, x.size, G, S)
+        c2, s2, z2 = oracle.c_construct(bits, G, S)
+        assert np.array_equal(c1, c2)
+        assert np.array_equal(s1.view(np.uint32), s2.view(np.uint32))
+        assert np.array_equal(z1.view(np.uint32), z2.view(np.uint32))
+        for k in range(1, S + 1):
+            for dt in ("f32", "bf16"):
+                a = o.reconstruct(c1, s1, z1, G, k, dt)
+                b = oracle.c_reconstruct(c1, s1, z1, G, k, dt)
+                assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
