@@ -1,0 +1,193 @@
+"""Benchmark of the RRQ hot path on one MI355X.
+
+One step = the whole path over the workload, each kernel as one flat call over
+the full weight stack with every buffer resident in HBM:
+  rrq_construct    (bf16 weights -> 4-stage package, G = 128)
+  rrq_reconstruct  at every prefix the workload names (bf16 output).
+
+Default workload: the 36-layer Qwen3-8B-shaped stack (6.95e9 weights,
+13.9 GB bf16; Gaussian with 0.1% x20 outliers).
+
+Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
+weights (2 bytes x weights / mean construct kernel time). The roofline entry
+is for the construct kernel: algorithmic HBM bytes per launch (bf16 in,
+codes + fp32 scales and zeros out) / its mean duration, against 8 TB/s.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "RRQ 4-stage construction GB/s of bf16 weights (% HBM peak); reconstruct GB/s"
+
+
+def construct_bytes(n, G, S):
+    """Algorithmic HBM bytes of one construct launch: bf16 in, 2-bit codes,
+    fp32 scale and zero per group and stage."""
+    return 2 * n + S * n // 4 + 2 * 4 * S * (n // G)
+
+
+def reconstruct_bytes(n, G, k, out_bytes):
+    return k * n // 4 + 2 * 4 * k * (n // G) + out_bytes * n
+
+
+def cpu_baseline(w, W_dev, budget_s=12.0):
+    """The C oracle (as it stands) on the host cores, on whole tensors of the
+    workload taken in order until about budget_s seconds of compute."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    G, S = w.group_size, w.n_stages
+    threads = oracle.c_threads()
+    done_elems, elapsed, names = 0, 0.0, []
+    for t in w.tensors:
+        bits = (W_dev[t.offset:t.offset + t.numel].cpu().view(torch.int16).numpy()
+                .view(np.uint16))
+        t0 = time.perf_counter()
+        oracle.c_construct(bits, G, S)
+        elapsed += time.perf_counter() - t0
+        done_elems += t.numel
+        names.append(t.name)
+        if elapsed >= budget_s:
+            break
+    sample = (f"{len(names)} of {len(w.tensors)} tensors ({names[0]} .. {names[-1]}), "
+              f"{done_elems} weights, construct only, {elapsed:.1f} s")
+    return {"value": round(2 * done_elems / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle", "sample": sample}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="qwen3_8b_stack36")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build measures one GPU only (the path needs no exchange between "
+              "GPUs); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_04048_amd as rrq
+    from paper_2608_04048_amd import workloads as wl
+
+    torch.cuda.set_device(0)
+    rrq.load_library()
+    w = wl.workload(args.workload)
+    G, S, n = w.group_size, w.n_stages, w.numel
+    cols = w.tensors[0].cols
+    rows = n // cols
+    print(f"bench: materializing {w.name}: {n} weights", file=sys.stderr, flush=True)
+    W = wl.materialize(w).view(rows, cols)
+    codes = torch.empty((S, n // 16), dtype=torch.int32, device="cuda")
+    scales = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+    zeros = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+    outs = {k: torch.empty((rows, cols), dtype=torch.bfloat16, device="cuda") for k in w.recon_k}
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        if evs is not None:
+            evs[0].record(stream)
+        rrq.rrq_construct(W, rows, cols, G, S, codes, scales, zeros, stream)
+        if evs is not None:
+            evs[1].record(stream)
+        for i, k in enumerate(w.recon_k):
+            rrq.rrq_reconstruct(codes, scales, zeros, rows, cols, G, S, k, outs[k], rrq.RRQ_BF16,
+                                stream)
+            if evs is not None:
+                evs[2 + i].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"bench: warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2 + len(w.recon_k))]
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    cons_ms = [e[0].elapsed_time(e[1]) for e in events]
+    rec_ms = {k: [e[1 + i].elapsed_time(e[2 + i]) for e in events] for i, k in enumerate(w.recon_k)}
+    mean = lambda xs: sum(xs) / len(xs)
+    c_ms = mean(cons_ms)
+    bf16_gbs = 2 * n / (c_ms * 1e-3) / 1e9
+    c_bytes = construct_bytes(n, G, S)
+    c_achieved = c_bytes / (c_ms * 1e-3) / 1e9
+    recon = {}
+    for k in w.recon_k:
+        r_ms = mean(rec_ms[k])
+        recon[str(k)] = {
+            "ms": round(r_ms, 4),
+            "gbs_bf16_weights": round(2 * n / (r_ms * 1e-3) / 1e9, 2),
+            "hbm_gbs": round(reconstruct_bytes(n, G, k, 2) / (r_ms * 1e-3) / 1e9, 2),
+        }
+    print(f"bench: construct {c_ms:.3f} ms, {bf16_gbs:.1f} GB/s bf16, {c_achieved:.1f} GB/s HBM",
+          file=sys.stderr, flush=True)
+
+    result = {
+        "metric": METRIC,
+        "value": round(bf16_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "weights": n,
+            "tensors": len(w.tensors),
+            "group_size": G,
+            "n_stages": S,
+            "input": "bf16",
+            "recon_k": list(w.recon_k),
+            "recon_out": "bf16",
+            "calls": "one flat call per kernel over the whole stack",
+        },
+        "construct_ms": round(c_ms, 4),
+        "construct_ms_min": round(min(cons_ms), 4),
+        "construct_hbm_frac": round(c_achieved / HBM_PEAK_GBS, 4),
+        "reconstruct": recon,
+        "roofline": {
+            "kernel": "construct_kernel<128>",
+            "bound": "hbm",
+            "achieved": round(c_achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(c_achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "bytes_per_launch": c_bytes,
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, W.view(-1))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,153 @@
+/*
+ * rrq.h - C ABI of librrq.so: Recurrent Residual Quantization (RRQ) package
+ * construction and prefix reconstruction on AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper: "Recurrent Residual Quantization: A Progressive
+ * Multi-Precision Representation for LLMs"):
+ *   - Eq. 1-3: a group of G weights shares a scale s and zero-point z;
+ *     q = x/s + z, Q = R(q), and the stage leaves the residual
+ *     r = x - (Q - z) s.
+ *   - Eq. 4-7 and Algorithm 1: the base stage quantizes the weights, each
+ *     further stage quantizes the residual left by the stages before it; every
+ *     stage stores its own codes, scales and zero-points.
+ *   - Eq. 8 (restated as Eq. 18-19): the effective weight after t stages is
+ *     the sum of the first t dequantized stages.
+ *   - Sec. 4.1: the main configuration is four calibration-free 2-bit RTN
+ *     stages (2+2+2+2 bits) with group size 128, giving 2/4/6/8-bit prefixes.
+ *
+ * Arithmetic (the paper leaves it open; this library fixes it, and results
+ * are bit-identical to that definition):
+ *   residuals are IEEE binary32 and stay binary32 between stages;
+ *   lo = min(+0, min r), hi = max(+0, max r) over the group;
+ *   s = fl(fl(hi - lo) / 3); if s < 2^-126 (zero or subnormal) the group is
+ *     degenerate for that stage: s = z = 0, all codes 0, residual unchanged;
+ *   inv = fl(1 / s); z = RNE(fl((0 - lo) * inv)), an integer in {0,1,2,3};
+ *   Q = clamp(RNE(fl(r * inv) + z), 0, 3), where fl(r * inv) + z is rounded
+ *     once, ties to even;
+ *   rhat = fl((Q - z) * s); next residual r <- fl(r - rhat);
+ *   every operation is one correctly rounded binary32 operation, nearest-even,
+ *   with no fused multiply-add.
+ *   Reconstruction after k stages: acc = rhat_0, acc = fl(acc + rhat_t) for
+ *   t = 1..k-1 in stage order; binary32 output, or bfloat16 rounded to
+ *   nearest-even.
+ *
+ * Layout. The weight matrix is row-major [rows][cols] (out x in); a group is G
+ * consecutive elements of a row (along the input dimension), so groups never
+ * span rows and any stack of matrices stored back to back with G | cols may be
+ * passed as one call with rows = total rows. With N = rows * cols:
+ *   codes  : uint32 [n_stages][N / 16]. Element e (flat row-major index) of
+ *            stage k is bits 2*(e % 16) .. 2*(e % 16) + 1 of word
+ *            codes[k * (N / 16) + e / 16].
+ *   scales : float  [n_stages][N / G], scales[k * (N / G) + e / G].
+ *   zeros  : float  [n_stages][N / G], same indexing; integer values 0..3,
+ *            a zero zero-point is +0.0.
+ *
+ * Conventions for every call:
+ *   - All buffers are device pointers (HIP device memory of the current
+ *     device), allocated and owned by the caller. The library allocates
+ *     nothing and keeps no pointer after it returns.
+ *   - Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *     without waiting. Results are valid once the stream has reached that
+ *     point; the caller keeps the buffers alive until then.
+ *   - Arguments are checked before anything is enqueued. On an error the
+ *     call returns a nonzero status and enqueues nothing. No exception ever
+ *     crosses this interface.
+ *   - Inputs must not overlap outputs, and outputs must not overlap each
+ *     other.
+ *   - The library holds no mutable state: calls may be made concurrently
+ *     from several host threads (on different output buffers).
+ */
+#ifndef RRQ_H
+#define RRQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every call. */
+enum rrq_status {
+    RRQ_OK = 0,
+    RRQ_ERR_NULL = 1,   /* a required pointer is NULL */
+    RRQ_ERR_ALIGN = 2,  /* a pointer is not aligned as documented */
+    RRQ_ERR_SHAPE = 3,  /* rows or cols < 1, cols % group_size != 0, or rows*cols overflows */
+    RRQ_ERR_GROUP = 4,  /* group_size not in {32, 64, 128} */
+    RRQ_ERR_STAGES = 5, /* n_stages not in 1..RRQ_MAX_STAGES, or k_stages not in 1..n_stages */
+    RRQ_ERR_DTYPE = 6,  /* out_dtype not one of enum rrq_dtype */
+    RRQ_ERR_HIP = 7     /* the HIP runtime reported an error while launching */
+};
+
+/* Output element type of rrq_reconstruct. */
+enum rrq_dtype {
+    RRQ_F32 = 0,  /* IEEE binary32 */
+    RRQ_BF16 = 1  /* bfloat16 bit patterns (uint16), rounded to nearest-even */
+};
+
+#define RRQ_MAX_STAGES 4
+
+/*
+ * rrq_construct - build the RRQ package of a bfloat16 weight matrix
+ * (Algorithm 1 without a base checkpoint; Eq. 1-7; Sec. 4.1 configuration).
+ *
+ *   W          device, const uint16_t [rows][cols]: bfloat16 bit patterns.
+ *              16-byte aligned. Values must be finite (NaN or Inf inputs give
+ *              unspecified codes, scales and zeros; the call still completes
+ *              and touches no memory outside the documented buffers).
+ *   rows, cols matrix shape; cols % group_size == 0.
+ *   group_size G in {32, 64, 128}.
+ *   n_stages   S in 1..4: the base stage plus S-1 residual stages (2S bits).
+ *   codes      device, uint32 [S][rows*cols/16], 16-byte aligned (written).
+ *   scales     device, float  [S][rows*cols/G], 4-byte aligned (written).
+ *   zeros      device, float  [S][rows*cols/G], 4-byte aligned (written).
+ *   stream     HIP stream the work is enqueued on.
+ *
+ * Returns RRQ_OK, or RRQ_ERR_NULL / _ALIGN / _SHAPE / _GROUP / _STAGES with
+ * nothing enqueued, or RRQ_ERR_HIP if the kernel launch failed.
+ */
+int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                  int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
+                  hipStream_t stream);
+
+/*
+ * rrq_reconstruct - effective weight of the first k_stages stages of a
+ * package (Eq. 8, Eq. 18-19): sum of the dequantized stages (Q - z) s,
+ * binary32, in stage order (2 k_stages effective bits).
+ *
+ *   codes, scales, zeros  device, a package as written by rrq_construct for
+ *              the same rows, cols, group_size and n_stages (read only; codes
+ *              16-byte aligned, scales/zeros 4-byte aligned).
+ *   rows, cols, group_size, n_stages  the package's shape (they define the
+ *              per-stage plane strides); same rules as rrq_construct.
+ *   k_stages   1..n_stages.
+ *   W_out      device, [rows][cols] of out_dtype, 16-byte aligned (written).
+ *   out_dtype  RRQ_F32 or RRQ_BF16.
+ *   stream     HIP stream the work is enqueued on.
+ *
+ * Returns RRQ_OK, or an argument error with nothing enqueued, or RRQ_ERR_HIP.
+ */
+int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
+                    int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                    int32_t k_stages, void *W_out, int32_t out_dtype, hipStream_t stream);
+
+/*
+ * rrq_package_bytes - sizes the caller allocates for a package (host only,
+ * no device work): codes_bytes = n_stages * rows*cols/4 and scales_bytes =
+ * n_stages * (rows*cols/group_size) * 4; the zeros buffer has scales_bytes
+ * too. Either output pointer may be NULL. Returns RRQ_OK or an argument
+ * error (_SHAPE, _GROUP, _STAGES).
+ */
+int rrq_package_bytes(int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                      size_t *codes_bytes, size_t *scales_bytes);
+
+/* rrq_status_string - static, NUL-terminated description of a status code. */
+const char *rrq_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RRQ_H */

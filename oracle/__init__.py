@@ -42,7 +42,7 @@ def build_c_oracle(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not os.path.exists(_LIB):
             build_c_oracle(force=True)
         lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p

@@ -1,0 +1,172 @@
+"""RRQ (Recurrent Residual Quantization) package construction and prefix
+reconstruction on AMD Instinct MI355X.
+
+Thin Python binding of librrq.so (include/rrq.h). The functions named like the
+C ABI (``rrq_construct``, ``rrq_reconstruct``, ``rrq_package_bytes``,
+``rrq_status_string``) only marshal arguments: tensors become device pointers,
+the stream defaults to torch's current stream, and a nonzero status raises
+``RRQError``. ``construct`` and ``reconstruct`` additionally allocate the
+output tensors with torch. Every computation runs in the HIP kernels; there is
+no fallback, and a missing library raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librrq.so")
+
+RRQ_OK = 0
+RRQ_ERR_NULL = 1
+RRQ_ERR_ALIGN = 2
+RRQ_ERR_SHAPE = 3
+RRQ_ERR_GROUP = 4
+RRQ_ERR_STAGES = 5
+RRQ_ERR_DTYPE = 6
+RRQ_ERR_HIP = 7
+
+RRQ_F32 = 0
+RRQ_BF16 = 1
+
+RRQ_MAX_STAGES = 4
+GROUP_SIZES = (32, 64, 128)
+
+_lib = None
+
+
+class RRQError(RuntimeError):
+    """A librrq call returned a nonzero status."""
+
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {rrq_status_string(status)} (status {status})")
+
+
+def load_library() -> ctypes.CDLL:
+    """Load librrq.so (built by ``python -m paper_2608_04048_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2608_04048_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        lib.rrq_construct.argtypes = [P, I64, I64, I32, I32, P, P, P, P]
+        lib.rrq_construct.restype = ctypes.c_int
+        lib.rrq_reconstruct.argtypes = [P, P, P, I64, I64, I32, I32, I32, P, I32, P]
+        lib.rrq_reconstruct.restype = ctypes.c_int
+        lib.rrq_package_bytes.argtypes = [I64, I64, I32, I32, ctypes.POINTER(ctypes.c_size_t),
+                                          ctypes.POINTER(ctypes.c_size_t)]
+        lib.rrq_package_bytes.restype = ctypes.c_int
+        lib.rrq_status_string.argtypes = [ctypes.c_int]
+        lib.rrq_status_string.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def _ptr(x) -> Optional[int]:
+    """Device pointer of a tensor (or a raw integer address, or None)."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ---------------------------------------------------------------------------
+# C ABI, one to one
+# ---------------------------------------------------------------------------
+
+def rrq_status_string(status: int) -> str:
+    return load_library().rrq_status_string(int(status)).decode()
+
+
+def rrq_package_bytes(rows: int, cols: int, group_size: int, n_stages: int) -> Tuple[int, int]:
+    """(codes_bytes, scales_bytes) of a package; the zeros buffer has scales_bytes."""
+    cb, sb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    st = load_library().rrq_package_bytes(rows, cols, group_size, n_stages,
+                                          ctypes.byref(cb), ctypes.byref(sb))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_package_bytes")
+    return cb.value, sb.value
+
+
+def rrq_construct(W, rows: int, cols: int, group_size: int, n_stages: int,
+                  codes, scales, zeros, stream=None) -> None:
+    """Enqueue package construction (see include/rrq.h)."""
+    st = load_library().rrq_construct(_ptr(W), rows, cols, group_size, n_stages,
+                                      _ptr(codes), _ptr(scales), _ptr(zeros), _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_construct")
+
+
+def rrq_reconstruct(codes, scales, zeros, rows: int, cols: int, group_size: int,
+                    n_stages: int, k_stages: int, W_out, out_dtype: int, stream=None) -> None:
+    """Enqueue prefix-k reconstruction (see include/rrq.h)."""
+    st = load_library().rrq_reconstruct(_ptr(codes), _ptr(scales), _ptr(zeros), rows, cols,
+                                        group_size, n_stages, k_stages, _ptr(W_out),
+                                        out_dtype, _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_reconstruct")
+
+
+# ---------------------------------------------------------------------------
+# Tensor-level helpers (allocation + the calls above)
+# ---------------------------------------------------------------------------
+
+def _check_device_tensor(t, name, dtype):
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU device, got {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+
+
+def construct(W, group_size: int = 128, n_stages: int = 4, stream=None, out=None):
+    """RRQ package of a bfloat16 matrix W [rows, cols] (cuda, contiguous).
+
+    Returns (codes int32 [S, N/16] holding the uint32 words, scales float32
+    [S, N/G], zeros float32 [S, N/G]). ``out`` may pass preallocated buffers.
+    """
+    import torch
+    _check_device_tensor(W, "W", torch.bfloat16)
+    rows, cols = (W.shape[0], W.shape[1]) if W.dim() == 2 else (1, W.numel())
+    n = rows * cols
+    if out is None:
+        codes = torch.empty((n_stages, n // 16), dtype=torch.int32, device=W.device)
+        scales = torch.empty((n_stages, n // group_size), dtype=torch.float32, device=W.device)
+        zeros = torch.empty((n_stages, n // group_size), dtype=torch.float32, device=W.device)
+    else:
+        codes, scales, zeros = out
+    rrq_construct(W, rows, cols, group_size, n_stages, codes, scales, zeros, stream)
+    return codes, scales, zeros
+
+
+def reconstruct(codes, scales, zeros, rows: int, cols: int, group_size: int, k_stages: int,
+                out_dtype=None, stream=None, out=None):
+    """Prefix-k effective weight [rows, cols] as float32 or bfloat16."""
+    import torch
+    out_dtype = torch.bfloat16 if out_dtype is None else out_dtype
+    code = {torch.float32: RRQ_F32, torch.bfloat16: RRQ_BF16}[out_dtype]
+    n_stages = codes.shape[0]
+    if out is None:
+        out = torch.empty((rows, cols), dtype=out_dtype, device=codes.device)
+    rrq_reconstruct(codes, scales, zeros, rows, cols, group_size, n_stages, k_stages, out, code,
+                    stream)
+    return out

@@ -1,0 +1,131 @@
+// C ABI of librrq.so (declared in include/rrq.h): argument validation, package
+// sizes, launch geometry and HIP error mapping. Every entry point validates
+// its arguments before enqueueing anything and never throws.
+
+#include "rrq.h"
+
+#include <atomic>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "rrq_launch.h"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];   // 0 = not yet queried
+
+// Compute units of the current device (cached; read-only after first use).
+int current_cu_count()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return -1;
+    if (dev < kMaxDevices) {
+        int c = g_cu_count[dev].load(std::memory_order_relaxed);
+        if (c > 0) return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        return -1;
+    if (dev < kMaxDevices) g_cu_count[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Shape / group / stage checks shared by every entry point. On success *n is
+// rows * cols.
+int check_common(int64_t rows, int64_t cols, int32_t G, int32_t S, int64_t *n)
+{
+    if (G != 32 && G != 64 && G != 128) return RRQ_ERR_GROUP;
+    if (S < 1 || S > RRQ_MAX_STAGES) return RRQ_ERR_STAGES;
+    if (rows < 1 || cols < 1 || cols % G != 0) return RRQ_ERR_SHAPE;
+    int64_t prod = 0;
+    // Byte counts (up to 4 bytes per element) must fit in int64.
+    if (__builtin_mul_overflow(rows, cols, &prod) || prod > INT64_MAX / 4) return RRQ_ERR_SHAPE;
+    *n = prod;
+    return RRQ_OK;
+}
+
+int grid_for(int64_t work_items, int per_block, int blocks_per_cu, int *grid)
+{
+    const int cus = current_cu_count();
+    if (cus <= 0) return RRQ_ERR_HIP;
+    const int64_t blocks = (work_items + per_block - 1) / per_block;
+    const int64_t cap = (int64_t)cus * blocks_per_cu;
+    *grid = (int)(blocks < cap ? blocks : cap);
+    return RRQ_OK;
+}
+
+}  // namespace
+
+extern "C" int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                             int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
+                             hipStream_t stream)
+{
+    if (!W || !codes || !scales || !zeros) return RRQ_ERR_NULL;
+    int64_t n = 0;
+    int st = check_common(rows, cols, group_size, n_stages, &n);
+    if (st != RRQ_OK) return st;
+    if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4))
+        return RRQ_ERR_ALIGN;
+    const int64_t n_groups = n / group_size;
+    int grid = 0;
+    st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
+    if (st != RRQ_OK) return st;
+    hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
+                                                zeros, grid, stream);
+    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+}
+
+extern "C" int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
+                               int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                               int32_t k_stages, void *W_out, int32_t out_dtype,
+                               hipStream_t stream)
+{
+    if (!codes || !scales || !zeros || !W_out) return RRQ_ERR_NULL;
+    int64_t n = 0;
+    int st = check_common(rows, cols, group_size, n_stages, &n);
+    if (st != RRQ_OK) return st;
+    if (k_stages < 1 || k_stages > n_stages) return RRQ_ERR_STAGES;
+    if (out_dtype != RRQ_F32 && out_dtype != RRQ_BF16) return RRQ_ERR_DTYPE;
+    if (!aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4) || !aligned(W_out, 16))
+        return RRQ_ERR_ALIGN;
+    const int64_t n_groups = n / group_size;
+    int grid = 0;
+    st = grid_for(n / 16, rrq_detail::kReconstructThreads, rrq_detail::kReconstructBlocksPerCU,
+                  &grid);
+    if (st != RRQ_OK) return st;
+    hipError_t e = rrq_detail::launch_reconstruct(codes, scales, zeros, n_groups, group_size,
+                                                  n_stages, k_stages, W_out,
+                                                  out_dtype == RRQ_BF16, grid, stream);
+    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+}
+
+extern "C" int rrq_package_bytes(int64_t rows, int64_t cols, int32_t group_size,
+                                 int32_t n_stages, size_t *codes_bytes, size_t *scales_bytes)
+{
+    int64_t n = 0;
+    const int st = check_common(rows, cols, group_size, n_stages, &n);
+    if (st != RRQ_OK) return st;
+    if (codes_bytes) *codes_bytes = (size_t)n_stages * (size_t)(n / 4);
+    if (scales_bytes) *scales_bytes = (size_t)n_stages * (size_t)(n / group_size) * sizeof(float);
+    return RRQ_OK;
+}
+
+extern "C" const char *rrq_status_string(int status)
+{
+    switch (status) {
+    case RRQ_OK: return "success";
+    case RRQ_ERR_NULL: return "a required pointer is NULL";
+    case RRQ_ERR_ALIGN: return "a buffer is not aligned as required (16 bytes for W, codes and W_out; 4 for scales and zeros)";
+    case RRQ_ERR_SHAPE: return "bad shape: rows and cols must be >= 1, cols a multiple of group_size, rows*cols within range";
+    case RRQ_ERR_GROUP: return "group_size must be 32, 64 or 128";
+    case RRQ_ERR_STAGES: return "n_stages must be in 1..4 and k_stages in 1..n_stages";
+    case RRQ_ERR_DTYPE: return "out_dtype must be RRQ_F32 or RRQ_BF16";
+    case RRQ_ERR_HIP: return "the HIP runtime reported an error";
+    default: return "unknown status";
+    }
+}

@@ -1,0 +1,28 @@
+// Internal launch interface between the C ABI layer (rrq_api.cpp) and the
+// HIP kernels (rrq_kernels.hip). Arguments are already validated.
+#pragma once
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+namespace rrq_detail {
+
+// Package construction of n_groups groups of G bfloat16 weights, S stages.
+hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
+                            uint32_t *codes, float *scales, float *zeros,
+                            int grid, hipStream_t stream);
+
+// Prefix-k reconstruction of a package with n_groups groups of G, S stages.
+hipError_t launch_reconstruct(const uint32_t *codes, const float *scales,
+                              const float *zeros, int64_t n_groups, int G, int S,
+                              int k, void *out, bool out_bf16, int grid,
+                              hipStream_t stream);
+
+// Workgroups the construct kernel keeps resident per compute unit.
+constexpr int kConstructBlocksPerCU = 8;
+// Threads per workgroup and resident workgroups per CU for reconstruct.
+constexpr int kReconstructThreads = 256;
+constexpr int kReconstructBlocksPerCU = 8;
+
+}  // namespace rrq_detail

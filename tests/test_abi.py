@@ -1,0 +1,144 @@
+"""The C ABI library: loads, exports every symbol include/rrq.h declares, sizes
+packages, and rejects bad arguments with the documented status before doing
+any device work. No GPU needed (nothing here reaches a kernel launch)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_04048_amd as rrq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rrq.h")
+
+FAKE = 0x10000          # aligned, never dereferenced: every case fails validation first
+FAKE_MISALIGNED = 0x10004
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rrq_\w+)\s*\(", text)))
+
+
+def _declared_enums():
+    text = open(HEADER).read()
+    return dict((k, int(v)) for k, v in re.findall(r"\b(RRQ_[A-Z0-9_]+)\s*=\s*(\d+)", text))
+
+
+def test_library_exports_every_declared_function():
+    lib = rrq.load_library()
+    names = _declared_functions()
+    assert names == ["rrq_construct", "rrq_package_bytes", "rrq_reconstruct", "rrq_status_string"]
+    for name in names:
+        assert hasattr(lib, name), name
+    out = os.popen(f"nm -D --defined-only {rrq.LIB_PATH}").read()
+    exported = set(re.findall(r" T (rrq_\w+)", out))
+    assert set(names) <= exported
+
+
+def test_binding_constants_match_header():
+    enums = _declared_enums()
+    for name, value in enums.items():
+        assert getattr(rrq, name) == value, name
+    assert "RRQ_MAX_STAGES 4" in open(HEADER).read()
+
+
+def test_package_bytes():
+    assert rrq.rrq_package_bytes(1024, 1024, 128, 4) == (4 * 1024 * 1024 // 4, 4 * 8192 * 4)
+    assert rrq.rrq_package_bytes(4096, 12288, 64, 3) == (3 * 4096 * 12288 // 4, 3 * 4096 * 192 * 4)
+    assert rrq.rrq_package_bytes(1, 32, 32, 1) == (8, 4)
+    # Qwen3-8B-shaped 36-layer stack as one flat call
+    n = 36 * (2 * 4096 * 4096 + 2 * 1024 * 4096 + 3 * 12288 * 4096)
+    assert rrq.rrq_package_bytes(n // 4096, 4096, 128, 4) == (n, 4 * (n // 128) * 4)
+
+
+@pytest.mark.parametrize("args,status", [
+    ((1024, 1000, 128, 4), rrq.RRQ_ERR_SHAPE),
+    ((0, 1024, 128, 4), rrq.RRQ_ERR_SHAPE),
+    ((1024, -128, 128, 4), rrq.RRQ_ERR_SHAPE),
+    ((1 << 40, 1 << 40, 128, 4), rrq.RRQ_ERR_SHAPE),
+    ((1024, 1024, 96, 4), rrq.RRQ_ERR_GROUP),
+    ((1024, 1024, 256, 4), rrq.RRQ_ERR_GROUP),
+    ((1024, 1024, 128, 0), rrq.RRQ_ERR_STAGES),
+    ((1024, 1024, 128, 5), rrq.RRQ_ERR_STAGES),
+])
+def test_package_bytes_rejects(args, status):
+    with pytest.raises(rrq.RRQError) as ei:
+        rrq.rrq_package_bytes(*args)
+    assert ei.value.status == status
+
+
+def _construct_status(W=FAKE, rows=64, cols=128, G=128, S=4, codes=FAKE, scales=FAKE, zeros=FAKE):
+    lib = rrq.load_library()
+    return lib.rrq_construct(W, rows, cols, G, S, codes, scales, zeros, None)
+
+
+def _reconstruct_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128, S=4, k=4,
+                        out=FAKE, dt=rrq.RRQ_BF16):
+    lib = rrq.load_library()
+    return lib.rrq_reconstruct(codes, scales, zeros, rows, cols, G, S, k, out, dt, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(W=None), rrq.RRQ_ERR_NULL),
+    (dict(codes=None), rrq.RRQ_ERR_NULL),
+    (dict(scales=None), rrq.RRQ_ERR_NULL),
+    (dict(zeros=None), rrq.RRQ_ERR_NULL),
+    (dict(G=16), rrq.RRQ_ERR_GROUP),
+    (dict(S=0), rrq.RRQ_ERR_STAGES),
+    (dict(S=5), rrq.RRQ_ERR_STAGES),
+    (dict(cols=100), rrq.RRQ_ERR_SHAPE),
+    (dict(rows=0), rrq.RRQ_ERR_SHAPE),
+    (dict(rows=1 << 62, cols=128), rrq.RRQ_ERR_SHAPE),
+    (dict(W=FAKE + 8), rrq.RRQ_ERR_ALIGN),
+    (dict(codes=FAKE_MISALIGNED), rrq.RRQ_ERR_ALIGN),
+    (dict(scales=FAKE + 2), rrq.RRQ_ERR_ALIGN),
+    (dict(zeros=FAKE + 1), rrq.RRQ_ERR_ALIGN),
+])
+def test_construct_rejects(kw, status):
+    assert _construct_status(**kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(codes=None), rrq.RRQ_ERR_NULL),
+    (dict(out=None), rrq.RRQ_ERR_NULL),
+    (dict(G=48), rrq.RRQ_ERR_GROUP),
+    (dict(S=5, k=1), rrq.RRQ_ERR_STAGES),
+    (dict(k=0), rrq.RRQ_ERR_STAGES),
+    (dict(S=2, k=3), rrq.RRQ_ERR_STAGES),
+    (dict(dt=2), rrq.RRQ_ERR_DTYPE),
+    (dict(cols=130), rrq.RRQ_ERR_SHAPE),
+    (dict(out=FAKE + 4), rrq.RRQ_ERR_ALIGN),
+    (dict(codes=FAKE + 4), rrq.RRQ_ERR_ALIGN),
+])
+def test_reconstruct_rejects(kw, status):
+    assert _reconstruct_status(**kw) == status
+
+
+def test_status_strings():
+    for st in range(8):
+        s = rrq.rrq_status_string(st)
+        assert isinstance(s, str) and s
+    assert rrq.rrq_status_string(0) == "success"
+    assert rrq.rrq_status_string(99) == "unknown status"
+
+
+def test_binding_raises_on_error():
+    with pytest.raises(rrq.RRQError) as ei:
+        rrq.rrq_construct(FAKE, 64, 128, 128, 9, FAKE, FAKE, FAKE, stream=0)
+    assert ei.value.status == rrq.RRQ_ERR_STAGES
+
+
+def test_product_does_not_import_oracle():
+    """The HIP path and the oracle share no code: nothing in the package or
+    its C++ sources refers to oracle/."""
+    pkg = os.path.join(ROOT, "paper_2608_04048_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "from oracle" not in text, f
+                assert "rrq_oracle" not in text, f
