@@ -94,9 +94,12 @@ enum rrq_dtype {
  * (Algorithm 1 without a base checkpoint; Eq. 1-7; Sec. 4.1 configuration).
  *
  *   W          device, const uint16_t [rows][cols]: bfloat16 bit patterns.
- *              16-byte aligned. Values must be finite (NaN or Inf inputs give
- *              unspecified codes, scales and zeros; the call still completes
- *              and touches no memory outside the documented buffers).
+ *              16-byte aligned. Precondition: every value is finite and every
+ *              group's range hi - lo is finite in binary32, which holds whenever
+ *              all |W| < 2^127. Inputs outside it (NaN, Inf, or a group holding
+ *              values near +-3.4e38 of both signs) give unspecified codes,
+ *              scales and zeros; the call still completes and touches no
+ *              memory outside the documented buffers.
  *   rows, cols matrix shape; cols % group_size == 0.
  *   group_size G in {32, 64, 128}.
  *   n_stages   S in 1..4: the base stage plus S-1 residual stages (2S bits).

@@ -76,6 +76,8 @@ def c_construct(w_bits: np.ndarray, group_size: int, n_stages: int):
                                   _ptr(codes), _ptr(scales), _ptr(zeros))
     if rc == 2:
         raise ValueError("RRQ oracle: inputs must be finite")
+    if rc == 3:
+        raise ValueError("RRQ oracle: a group's range overflows binary32 (inputs need |x| < 2^127)")
     if rc != 0:
         raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
     return codes, scales, zeros

@@ -26,6 +26,7 @@
 #define ORACLE_OK 0
 #define ORACLE_ERR_ARGS 1
 #define ORACLE_ERR_NONFINITE 2
+#define ORACLE_ERR_RANGE 3
 
 static float bf16_to_f32(uint16_t b)
 {
@@ -52,8 +53,8 @@ static uint16_t f32_to_bf16(float f)
  * steps: writes the codes Q[0..G), the scale and zero-point, and replaces
  * r[j] by r[j] - rhat[j] when update_residual is set.
  */
-static void rtn_stage_group(float *r, int G, int bits, int update_residual,
-                            uint8_t *Q, float *s_out, float *z_out)
+static int rtn_stage_group(float *r, int G, int bits, int update_residual,
+                           uint8_t *Q, float *s_out, float *z_out)
 {
     const int maxq = (1 << bits) - 1;
     float lo = 0.0f, hi = 0.0f;           /* zero is always in the range */
@@ -62,12 +63,13 @@ static void rtn_stage_group(float *r, int G, int bits, int update_residual,
         if (r[j] > hi) hi = r[j];
     }
     float d = hi - lo;
+    if (!isfinite(d)) return ORACLE_ERR_RANGE;   /* precondition: finite range */
     float s = d / (float)maxq;
     if (!(s >= 0x1p-126f)) {              /* zero or subnormal: degenerate */
         for (int j = 0; j < G; ++j) Q[j] = 0;
         *s_out = 0.0f;
         *z_out = 0.0f;
-        return;                            /* residual unchanged */
+        return ORACLE_OK;                  /* residual unchanged */
     }
     float inv = 1.0f / s;
     float z = rintf((0.0f - lo) * inv);    /* integer zero-point */
@@ -88,6 +90,7 @@ static void rtn_stage_group(float *r, int G, int bits, int update_residual,
     }
     *s_out = s;
     *z_out = z;
+    return ORACLE_OK;
 }
 
 /*
@@ -104,9 +107,9 @@ int rrq_oracle_construct(const uint16_t *W, int64_t n, int32_t G, int32_t S,
     if (S < 1 || S > 8) return ORACLE_ERR_ARGS;
     const int64_t n_groups = n / G;
     const int64_t words = n / 16;
-    int bad = 0;
+    int bad = 0, bad_range = 0;
 
-#pragma omp parallel for schedule(static) reduction(| : bad)
+#pragma omp parallel for schedule(static) reduction(| : bad, bad_range)
     for (int64_t g = 0; g < n_groups; ++g) {
         float r[1024];
         uint8_t Q[1024];
@@ -115,8 +118,8 @@ int rrq_oracle_construct(const uint16_t *W, int64_t n, int32_t G, int32_t S,
             if (!isfinite(r[j])) bad = 1;
         }
         for (int k = 0; k < S; ++k) {
-            float s, z;
-            rtn_stage_group(r, G, 2, k + 1 < S, Q, &s, &z);
+            float s = 0.0f, z = 0.0f;
+            if (rtn_stage_group(r, G, 2, k + 1 < S, Q, &s, &z) != ORACLE_OK) bad_range = 1;
             scales[(int64_t)k * n_groups + g] = s;
             zeros[(int64_t)k * n_groups + g] = z;
             for (int w = 0; w < G / 16; ++w) {
@@ -127,7 +130,7 @@ int rrq_oracle_construct(const uint16_t *W, int64_t n, int32_t G, int32_t S,
             }
         }
     }
-    return bad ? ORACLE_ERR_NONFINITE : ORACLE_OK;
+    return bad ? ORACLE_ERR_NONFINITE : bad_range ? ORACLE_ERR_RANGE : ORACLE_OK;
 }
 
 /*

@@ -40,7 +40,8 @@ The paper leaves the floating-point details open; this oracle fixes them
 * codes are stored stage-planar, 16 two-bit codes per little-endian uint32,
   element e of the flat matrix in word e // 16 at bits 2 (e % 16) .. +1.
 
-Inputs must be finite bfloat16 values; the oracle raises otherwise.
+Inputs must be finite bfloat16 values whose per-group range hi - lo is finite
+in binary32 (always so when every |x| < 2^127); the oracle raises otherwise.
 
 Every step below is a separate numpy float32 operation (one IEEE rounding per
 operation, no fused multiply-add). Where a step needs an exact value (t + z),
@@ -122,6 +123,8 @@ def rtn_stage(r: np.ndarray, bits: int):
     hi = np.where(hi == zero, zero, hi)
 
     d = hi - lo                                # fl(hi - lo)
+    if not np.all(np.isfinite(d)):
+        raise ValueError("RRQ oracle: a group's range overflows binary32 (inputs need |x| < 2^127)")
     s = d / F32(maxq)                          # fl(d / maxq), IEEE division
     degenerate = s < SMALLEST_NORMAL_F32       # zero or subnormal scale
 

@@ -247,7 +247,10 @@ __global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__
             const bool degenerate = !(s >= 0x1p-126f);
             const float inv = degenerate ? 0.0f : 1.0f / s;
             const float sq = degenerate ? 0.0f : s;
-            const float z = rintf((0.0f - lo) * inv);
+            // lo <= 0, so |lo| is exactly 0 - lo, +0 included. Written as fabs:
+            // the code generator folds 0 - lo into a negate modifier, which
+            // turns lo = +0 into -0 and would store z = -0.
+            const float z = rintf(fabsf(lo) * inv);
             const float m = kMagic + z;
             const float u_hi = hi * inv + m;
             const bool clamp = __any(u_hi > kTopCode);

@@ -123,9 +123,13 @@ def test_zeros_signed_zeros_subnormals_and_extremes(gpu):
     bits[n // 8: n // 4] = 0x8000                                      # -0
     bits[n // 4: n // 2] = rng.integers(1, 0x80, n // 4).astype(np.uint16)       # subnormal +
     bits[n // 2: 5 * n // 8] = 0x8000 | rng.integers(1, 0x80, n // 8).astype(np.uint16)
-    bits[5 * n // 8: 3 * n // 4] = rng.choice([0x7F7F, 0xFF7F, 0x0080, 0x8080], n // 8)  # extremes
-    tail = rng.integers(0, 65536, n // 4).astype(np.uint16)             # any finite value
-    tail = np.where(((tail >> 7) & 0xFF) == 0xFF, 0, tail).astype(np.uint16)
+    # extremes: largest magnitudes inside the precondition (|x| < 2^127) of
+    # both signs, smallest normals
+    bits[5 * n // 8: 3 * n // 4] = rng.choice([0x7E7F, 0xFE7F, 0x0080, 0x8080], n // 8)
+    # one-signed groups may go up to the bfloat16 maximum
+    bits[5 * n // 8: 5 * n // 8 + 128] = rng.choice([0x7F7F, 0x7F00, 0x0000], 128)
+    tail = rng.integers(0, 65536, n // 4).astype(np.uint16)             # any value with
+    tail = np.where(((tail >> 7) & 0xFF) >= 0xFE, 0, tail).astype(np.uint16)  # |x| < 2^127
     bits[3 * n // 4:] = tail
     for G in (32, 64, 128):
         _check_case(gpu, bits, n // 1024, 1024, G, 4, tag=f"edges_G{G}")

@@ -364,6 +364,25 @@ def test_nonfinite_rejected():
         oracle.c_construct(x, 32, 4)
 
 
+def test_range_overflow_rejected():
+    """Opposite-sign values near the bfloat16 maximum make hi - lo overflow
+    binary32: outside the precondition, rejected by both writings. Just inside
+    it (|x| < 2^127) everything stays finite."""
+    x = np.zeros(32, dtype=np.uint16)
+    x[0], x[1] = 0x7F7F, 0xFF7F                 # +-3.39e38
+    with pytest.raises(ValueError):
+        o.construct(x, 1, 32, 32, 4)
+    with pytest.raises(ValueError):
+        oracle.c_construct(x, 32, 4)
+    x[0], x[1] = 0x7E7F, 0xFE7F                 # +-1.70e38 < 2^127
+    c1, s1, z1 = o.construct(x, 1, 32, 32, 4)
+    c2, s2, z2 = oracle.c_construct(x, 32, 4)
+    assert np.all(np.isfinite(s1)) and np.array_equal(c1, c2)
+    rec = o.reconstruct(c1, s1, z1, 32, 4)
+    assert np.all(np.isfinite(rec))
+    assert np.array_equal(rec.view(np.uint32), o.bf16_bits_to_f32(x).view(np.uint32))
+
+
 def test_two_oracles_agree_on_random_inputs():
     for seed, G, S in [(1, 32, 4), (2, 64, 3), (3, 128, 4), (4, 128, 1)]:
         x = _workload(seed, 4000, G, "outlier")
