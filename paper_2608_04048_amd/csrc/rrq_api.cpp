@@ -95,7 +95,9 @@ extern "C" int rrq_reconstruct(const uint32_t *codes, const float *scales, const
         return RRQ_ERR_ALIGN;
     const int64_t n_groups = n / group_size;
     int grid = 0;
-    st = grid_for(n / 16, rrq_detail::kReconstructThreads, rrq_detail::kReconstructBlocksPerCU,
+    // one wave tile = 64 lanes x 4 chunks x (8 or 4) elements; 4 waves per workgroup
+    const int per_lane = rrq_detail::kReconstructChunksBF16 * 8;
+    st = grid_for(n, rrq_detail::kReconstructThreads * per_lane, rrq_detail::kReconstructBlocksPerCU,
                   &grid);
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_reconstruct(codes, scales, zeros, n_groups, group_size,

@@ -92,46 +92,68 @@ __device__ __forceinline__ uint32_t lshl_add(uint32_t bits, int sh, uint32_t acc
 }
 #undef RRQ_LSHL_ADD_CASE
 
+// Per-lane dequantization tables in LDS: entry q of lane l is fl((q - z) s)
+// of the lane's group for the current stage, at float index q * 64 + l, so
+// a wave's 64 lookups always touch 64 distinct banks.
+struct DequantTable {
+    float *base;      // this wave's 4 x 64 floats
+    uint32_t adj;     // byte offset of (q, lane) minus (kMagicBits << 8), mod 2^32
+};
+
 // Element loop of one stage for one lane's group: the stage's codes into
 // words[]; with UPDATE also the residual r <- r - (Q - z) s and the range of
 // the new residual (lo, hi, zero included) for the next stage.
-template <int G, bool CLAMP, bool UPDATE>
-__device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m, float s,
+//
+// Per element: t = fl(r inv); u = min(fl(t + m), code 3) holds code Q in its
+// low mantissa bits; the code is packed by a shift-add of u's bits; with
+// UPDATE, (u << 8) + adj is the LDS byte address of the lane's table entry Q,
+// so the dequantized value fl((Q - z) s) costs one VALU op and one LDS read.
+template <int G, bool UPDATE>
+__device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m,
+                                               const DequantTable &tab,
                                                uint32_t (&words)[G / 16], float &lo, float &hi)
 {
     float l0 = 0.f, l1 = 0.f, h0 = 0.f, h1 = 0.f;
-#pragma unroll
-    for (int w = 0; w < G / 16; ++w) {
+    const char *tbase = reinterpret_cast<const char *>(tab.base);
+    float rh[2][16];   // table lookups of two consecutive words in flight
+
+    // Codes of word w and (UPDATE) the lookups of its dequantized values.
+    auto quantize_word = [&](int w, float (&rhw)[16]) {
         uint32_t acc = 0;
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            const int j = w * 16 + e;
-            const float t = r[j] * inv;
-            float u = t + m;
-            if (CLAMP) u = fminf(u, kTopCode);
-            if (e == 0) acc = __float_as_uint(u);
-            else acc = lshl_add(__float_as_uint(u), 2 * e, acc);
-            if (UPDATE) {
-                const float qz = u - m;      // Q - z, exact
-                const float rh = qz * s;     // fl((Q - z) s)
-                r[j] = r[j] - rh;
-            }
+            const float t = r[w * 16 + e] * inv;
+            const float u = fminf(t + m, kTopCode);
+            const uint32_t ub = __float_as_uint(u);
+            acc = e == 0 ? ub : lshl_add(ub, 2 * e, acc);
+            if (UPDATE)
+                rhw[e] = *reinterpret_cast<const float *>(tbase + lshl_add(ub, 8, tab.adj));
         }
         words[w] = acc - kPackBias;
-        if (UPDATE) {
-            // min3 / max3 over pairs of the new residuals, two chains each
+    };
+    // Residual update of word w and its contribution to the next range.
+    auto update_word = [&](int w, const float (&rhw)[16]) {
 #pragma unroll
-            for (int e = 0; e < 16; e += 4) {
-                const int j = w * 16 + e;
-                l0 = fminf(fminf(l0, r[j]), r[j + 1]);
-                h0 = fmaxf(fmaxf(h0, r[j]), r[j + 1]);
-                l1 = fminf(fminf(l1, r[j + 2]), r[j + 3]);
-                h1 = fmaxf(fmaxf(h1, r[j + 2]), r[j + 3]);
-            }
+        for (int e = 0; e < 16; ++e) r[w * 16 + e] = r[w * 16 + e] - rhw[e];
+#pragma unroll
+        for (int e = 0; e < 16; e += 4) {
+            const int j = w * 16 + e;
+            l0 = fminf(fminf(l0, r[j]), r[j + 1]);
+            h0 = fmaxf(fmaxf(h0, r[j]), r[j + 1]);
+            l1 = fminf(fminf(l1, r[j + 2]), r[j + 3]);
+            h1 = fmaxf(fmaxf(h1, r[j + 2]), r[j + 3]);
         }
-        // Keep the scheduler from hoisting the next word's products above
-        // this word's updates: that would hold a second G-wide array of
-        // temporaries live and spill the residuals out of the register file.
+    };
+
+    // Software pipeline: word w + 1's lookups are issued before word w's
+    // results are consumed, so LDS latency overlaps VALU work. The
+    // scheduling barriers keep the compiler from hoisting further ahead,
+    // which would hold extra G-wide temporaries and spill the residuals.
+    quantize_word(0, rh[0]);
+#pragma unroll
+    for (int w = 0; w < G / 16; ++w) {
+        if (w + 1 < G / 16) quantize_word(w + 1, rh[(w + 1) & 1]);
+        if (UPDATE) update_word(w, rh[w & 1]);
         __builtin_amdgcn_sched_barrier(0);
     }
     lo = fminf(l0, l1);
@@ -188,6 +210,72 @@ __device__ __forceinline__ void load_tile(const uint4 *__restrict__ W, int64_t n
     }
 }
 
+// Reads this lane's group from the transposed LDS tile and widens bfloat16 to
+// binary32.
+template <int G>
+__device__ __forceinline__ void gather_group(const uint4 *rd_base, float (&r)[G])
+{
+#pragma unroll
+    for (int c = 0; c < G / 8; ++c) {
+        const uint4 w = rd_base[c];
+        const uint32_t p[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h) {
+            r[8 * c + 2 * h] = __uint_as_float(p[h] << 16);
+            r[8 * c + 2 * h + 1] = __uint_as_float(p[h] & 0xFFFF0000u);
+        }
+    }
+}
+
+// Output resources of one tile: codes, scales and zeros of stage 0; stage k
+// is reached by advancing the base pointers k planes.
+struct TileOut {
+    uint32_t *codes;
+    float *scales, *zeros;
+    int64_t words_per_stage, n_groups;
+    uint32_t code_bytes, scale_bytes;
+};
+
+template <int G>
+__device__ __forceinline__ void store_stage(const TileOut &o, int k, int lane,
+                                            const uint32_t (&words)[G / 16], float s, float z)
+{
+    // Lanes past the last group fall outside the resources; their stores
+    // are dropped.
+    store_words<G>(make_rsrc(o.codes + k * o.words_per_stage, o.code_bytes),
+                   lane * (G / 16) * 4, words);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s),
+                                          make_rsrc(o.scales + k * o.n_groups, o.scale_bytes),
+                                          lane * 4, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z),
+                                          make_rsrc(o.zeros + k * o.n_groups, o.scale_bytes),
+                                          lane * 4, 0, 0);
+}
+
+// Scale, reciprocal, zero-point and magic addend of one stage from the
+// group's range (lo <= 0 <= hi).
+__device__ __forceinline__ void stage_params(float lo, float hi, float &inv, float &sq, float &z,
+                                             float &m)
+{
+    const float d = hi - lo;
+    const float s = d / 3.0f;
+    const bool degenerate = !(s >= 0x1p-126f);
+    inv = degenerate ? 0.0f : 1.0f / s;
+    sq = degenerate ? 0.0f : s;
+    // lo <= 0, so |lo| is exactly 0 - lo, +0 included. Written as fabs: the
+    // code generator folds 0 - lo into a negate modifier, which turns lo = +0
+    // into -0 and would store z = -0.
+    z = rintf(fabsf(lo) * inv);
+    m = kMagic + z;
+}
+
+// Fills this lane's dequantization table for the stage: fl((q - z) s).
+__device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, float sq, float z)
+{
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tab.base[q * 64 + lane] = ((float)q - z) * sq;
+}
+
 template <int G>
 __global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__ W,
                                                        int64_t n_groups, int n_stages,
@@ -203,12 +291,13 @@ __global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__
     // all banks: a row write (lanes -> consecutive chunks of a group) and a
     // column read (lanes -> the same chunk of consecutive groups).
     __shared__ uint4 tile_lds[64 * ROW];
+    __shared__ float table_lds[4 * 64];
 
     const int lane = threadIdx.x;
     const int64_t n_tiles = (n_groups + 63) / 64;
-    const int64_t words_per_stage = n_groups * WPG;
     uint4 *const wr_base = tile_lds + (lane / CH) * ROW + (lane % CH);
     const uint4 *const rd_base = tile_lds + lane * ROW;
+    const DequantTable tab = {table_lds, (uint32_t)(lane * 4) - (kMagicBits << 8)};
 
     int64_t tile = blockIdx.x;
     uint4 v[CH];
@@ -220,18 +309,8 @@ __global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__
         for (int i = 0; i < CH; ++i) wr_base[i * GROUPS_PER_LOAD * ROW] = v[i];
         __syncthreads();
 
-        // Each lane gathers its own group and widens bfloat16 to binary32.
         float r[G];
-#pragma unroll
-        for (int c = 0; c < CH; ++c) {
-            const uint4 w = rd_base[c];
-            const uint32_t p[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-            for (int h = 0; h < 4; ++h) {
-                r[8 * c + 2 * h] = __uint_as_float(p[h] << 16);
-                r[8 * c + 2 * h + 1] = __uint_as_float(p[h] & 0xFFFF0000u);
-            }
-        }
+        gather_group<G>(rd_base, r);
 
         // Prefetch the next tile while this one is quantized.
         const int64_t next = tile + gridDim.x;
@@ -239,84 +318,119 @@ __global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__
 
         const int64_t g0 = tile * 64;
         const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
-        float lo, hi;
-        group_range<G>(r, lo, hi);
-        for (int k = 0; k < n_stages; ++k) {
-            const float d = hi - lo;
-            const float s = d / 3.0f;
-            const bool degenerate = !(s >= 0x1p-126f);
-            const float inv = degenerate ? 0.0f : 1.0f / s;
-            const float sq = degenerate ? 0.0f : s;
-            // lo <= 0, so |lo| is exactly 0 - lo, +0 included. Written as fabs:
-            // the code generator folds 0 - lo into a negate modifier, which
-            // turns lo = +0 into -0 and would store z = -0.
-            const float z = rintf(fabsf(lo) * inv);
-            const float m = kMagic + z;
-            const float u_hi = hi * inv + m;
-            const bool clamp = __any(u_hi > kTopCode);
+        const TileOut out = {codes + g0 * WPG, scales + g0, zeros + g0,
+                             n_groups * WPG, n_groups, groups_here * WPG * 4, groups_here * 4};
 
-            uint32_t words[WPG];
-            (void)clamp;
-            stage_elements<G, true, true>(r, inv, m, sq, words, lo, hi);
-            // Lanes past the last group fall outside the resources and
-            // their stores are dropped.
-            store_words<G>(make_rsrc(codes + k * words_per_stage + g0 * WPG, groups_here * WPG * 4),
-                           lane * WPG * 4, words);
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(sq),
-                                                  make_rsrc(scales + k * n_groups + g0, groups_here * 4),
-                                                  lane * 4, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z),
-                                                  make_rsrc(zeros + k * n_groups + g0, groups_here * 4),
-                                                  lane * 4, 0, 0);
+        float lo, hi, inv, sq, z, m;
+        uint32_t words[WPG];
+        group_range<G>(r, lo, hi);
+        for (int k = 0; k + 1 < n_stages; ++k) {
+            stage_params(lo, hi, inv, sq, z, m);
+            fill_table(tab, lane, sq, z);
+            stage_elements<G, true>(r, inv, m, tab, words, lo, hi);
+            store_stage<G>(out, k, lane, words, sq, z);
         }
+        stage_params(lo, hi, inv, sq, z, m);
+        stage_elements<G, false>(r, inv, m, tab, words, lo, hi);
+        store_stage<G>(out, n_stages - 1, lane, words, sq, z);
     }
 }
 
-// Reconstruction: each thread owns 16 consecutive elements (one code word per
-// stage) and sums (Q - z) s over the first k stages, left to right.
-template <bool OUT_BF16>
-__global__ __launch_bounds__(kReconstructThreads) void reconstruct_kernel(
-    const uint32_t *__restrict__ codes, const float *__restrict__ scales,
-    const float *__restrict__ zeros, int64_t n_words, int64_t n_groups, int wpg_shift,
-    int k, void *__restrict__ out)
+// Reconstruction. Lane work unit: a chunk of E consecutive elements whose
+// output is 16 bytes (E = 8 for bfloat16, 4 for binary32), so that each store
+// instruction of a wave writes 1 KiB contiguously. A wave handles tiles of
+// 64 * U chunks; lane l owns chunks l, l + 64, ... of the tile, issues all of
+// its loads (codes, scales, zeros of the K stages) before any arithmetic, and
+// sums the stages of each element left to right: acc = rhat_0,
+// acc = fl(acc + rhat_t).
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// x & 0x03030303, opaque to the compiler so that the byte conversions below
+// stay single v_cvt_f32_ubyte instructions.
+__device__ __forceinline__ uint32_t code_bytes(uint32_t x)
 {
-    const int64_t stride = (int64_t)gridDim.x * kReconstructThreads;
-    for (int64_t w = (int64_t)blockIdx.x * kReconstructThreads + threadIdx.x; w < n_words;
-         w += stride) {
-        const int64_t g = w >> wpg_shift;
-        float acc[16];
+    uint32_t out;
+    asm("v_and_b32 %0, 0x3030303, %1" : "=v"(out) : "v"(x));
+    return out;
+}
+
+template <int K, bool OUT_BF16, int U>
+__global__ __launch_bounds__(256) void reconstruct_kernel(const uint32_t *__restrict__ codes,
+                                                          const float *__restrict__ scales,
+                                                          const float *__restrict__ zeros,
+                                                          int64_t n_elems, int64_t n_groups,
+                                                          int g_shift, void *__restrict__ out)
+{
+    constexpr int E = OUT_BF16 ? 8 : 4;          // elements per chunk (16 output bytes)
+    constexpr int CPW = 16 / E;                  // chunks per code word
+    constexpr int TILE = 64 * U;                 // chunks per tile
+    const int lane = threadIdx.x & 63;
+    const int64_t n_chunks = n_elems / E;
+    const int64_t n_words = n_elems / 16;
+    const int64_t n_tiles = (n_chunks + TILE - 1) / TILE;
+    const int64_t n_waves = (int64_t)gridDim.x * 4;
+    // The wave index is uniform across the wave; saying so keeps the buffer
+    // resources below in scalar registers.
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < n_tiles; tile += n_waves) {
+        const int64_t c0 = tile * TILE;                       // first chunk
+        const uint32_t chunks_here = (uint32_t)(n_chunks - c0 < TILE ? n_chunks - c0 : TILE);
+        const int64_t wfirst = c0 / CPW;
+        const uint32_t words_here = (chunks_here + CPW - 1) / CPW;
+        const int64_t gfirst = (c0 * E) >> g_shift;
+        const uint32_t groups_here =
+            (uint32_t)((((c0 + chunks_here) * E - 1) >> g_shift) - gfirst + 1);
+
+        uint32_t cw[K][U];
+        float sc[K][U], ze[K][U];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            if (t >= k) break;
-            const uint32_t word = codes[t * n_words + w];
-            const float s = scales[t * n_groups + g];
-            const float z = zeros[t * n_groups + g];
+        for (int t = 0; t < K; ++t) {
+            const rsrc_t rc = make_rsrc(codes + t * n_words + wfirst, words_here * 4);
+            const rsrc_t rs = make_rsrc(scales + t * n_groups + gfirst, groups_here * 4);
+            const rsrc_t rz = make_rsrc(zeros + t * n_groups + gfirst, groups_here * 4);
 #pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const float q = (float)((word >> (2 * e)) & 3u);
-                const float rh = (q - z) * s;
-                acc[e] = t == 0 ? rh : acc[e] + rh;
+            for (int j = 0; j < U; ++j) {
+                const uint32_t cl = j * 64 + lane;   // chunk within the tile
+                const uint32_t gl = (uint32_t)((((c0 + cl) * E) >> g_shift) - gfirst);
+                cw[t][j] = __builtin_amdgcn_raw_buffer_load_b32(rc, (cl / CPW) * 4, 0, 0);
+                sc[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, gl * 4, 0, 0));
+                ze[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rz, gl * 4, 0, 0));
             }
         }
-        if (OUT_BF16) {
-            uint32_t packed[8];
+
+        const rsrc_t ro = make_rsrc(static_cast<char *>(out) + c0 * 16, chunks_here * 16);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                // nearest-even binary32 -> bfloat16 of a finite value
-                uint32_t lo = __float_as_uint(acc[2 * i]);
-                uint32_t hi = __float_as_uint(acc[2 * i + 1]);
-                lo = (lo + 0x7FFFu + ((lo >> 16) & 1u)) >> 16;
-                hi = (hi + 0x7FFFu + ((hi >> 16) & 1u)) >> 16;
-                packed[i] = lo | (hi << 16);
+        for (int j = 0; j < U; ++j) {
+            const uint32_t cl = j * 64 + lane;
+            const int shift = (int)((c0 + cl) % CPW) * 2 * E;   // this chunk's codes in the word
+            float acc[E];
+#pragma unroll
+            for (int t = 0; t < K; ++t) {
+                const uint32_t bits = cw[t][j] >> shift;
+                // byte b of cb[p] holds the code of element 4 b + p
+                uint32_t cb[4];
+#pragma unroll
+                for (int p = 0; p < 4; ++p) cb[p] = code_bytes(bits >> (2 * p));
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const float q = (float)((cb[e & 3] >> (8 * (e >> 2))) & 0xFFu);
+                    const float rh = (q - ze[t][j]) * sc[t][j];
+                    acc[e] = t == 0 ? rh : acc[e] + rh;
+                }
             }
-            uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(out) + w * 16);
-            dst[0] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
-            dst[1] = make_uint4(packed[4], packed[5], packed[6], packed[7]);
-        } else {
-            float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(out) + w * 16);
+            u32x4 v;
+            if constexpr (OUT_BF16) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                dst[i] = make_float4(acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]);
+                for (int i = 0; i < 4; ++i) {
+                    const f32x2 f = {acc[2 * i], acc[2 * i + 1]};
+                    v[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(acc[i]);
+            }
+            __builtin_amdgcn_raw_buffer_store_b128(v, ro, cl * 16, 0, 0);
         }
     }
 }
@@ -345,18 +459,34 @@ hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
     }
 }
 
+template <int K, bool BF16>
+hipError_t launch_reconstruct_k(const uint32_t *codes, const float *scales, const float *zeros,
+                                int64_t n_elems, int64_t n_groups, int g_shift, void *out,
+                                int grid, hipStream_t stream)
+{
+    return launch(reconstruct_kernel<K, BF16, BF16 ? kReconstructChunksBF16 : kReconstructChunksF32>,
+                  grid, kReconstructThreads, stream, codes, scales, zeros, n_elems, n_groups,
+                  g_shift, out);
+}
+
 hipError_t launch_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
                               int64_t n_groups, int G, int S, int k, void *out, bool out_bf16,
                               int grid, hipStream_t stream)
 {
     (void)S;
-    const int64_t n_words = n_groups * (G / 16);
-    const int wpg_shift = G == 32 ? 1 : G == 64 ? 2 : 3;
-    if (out_bf16)
-        return launch(reconstruct_kernel<true>, grid, kReconstructThreads, stream, codes, scales,
-                      zeros, n_words, n_groups, wpg_shift, k, out);
-    return launch(reconstruct_kernel<false>, grid, kReconstructThreads, stream, codes, scales,
-                  zeros, n_words, n_groups, wpg_shift, k, out);
+    const int64_t n_elems = n_groups * G;
+    const int g_shift = G == 32 ? 5 : G == 64 ? 6 : 7;
+#define RRQ_RECON_CASE(K)                                                                      \
+    case K:                                                                                    \
+        return out_bf16 ? launch_reconstruct_k<K, true>(codes, scales, zeros, n_elems, n_groups, \
+                                                        g_shift, out, grid, stream)            \
+                        : launch_reconstruct_k<K, false>(codes, scales, zeros, n_elems,        \
+                                                         n_groups, g_shift, out, grid, stream);
+    switch (k) {
+        RRQ_RECON_CASE(1) RRQ_RECON_CASE(2) RRQ_RECON_CASE(3) RRQ_RECON_CASE(4)
+    default: return hipErrorInvalidValue;
+    }
+#undef RRQ_RECON_CASE
 }
 
 }  // namespace rrq_detail

@@ -21,8 +21,12 @@ hipError_t launch_reconstruct(const uint32_t *codes, const float *scales,
 
 // Workgroups the construct kernel keeps resident per compute unit.
 constexpr int kConstructBlocksPerCU = 8;
-// Threads per workgroup and resident workgroups per CU for reconstruct.
+// Reconstruct: threads per workgroup (4 waves), 16-byte output chunks per
+// lane per tile (8 bfloat16 or 4 binary32 elements each), and resident
+// workgroups per CU.
 constexpr int kReconstructThreads = 256;
+constexpr int kReconstructChunksBF16 = 4;
+constexpr int kReconstructChunksF32 = 4;
 constexpr int kReconstructBlocksPerCU = 8;
 
 }  // namespace rrq_detail
