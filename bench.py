@@ -27,6 +27,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "construct_kernel_g128_qwen3_8b_stack36_traffic.md")
 METRIC = "RRQ 4-stage construction GB/s of bf16 weights (% HBM peak); reconstruct GB/s"
 
 
@@ -194,6 +195,14 @@ def main():
             "bytes_per_launch": c_bytes,
         },
     }
+    # Measured HBM traffic of the construct kernel from the committed
+    # FETCH_SIZE / WRITE_SIZE profile, only while the kernel source is the one
+    # that was profiled.
+    from paper_2608_04048_amd import profiling
+    rec = profiling.read_traffic_profile(TRAFFIC_PROFILE)
+    if (rec is not None and w.name == "qwen3_8b_stack36"
+            and rec[0] == profiling.kernel_source_sha256()):
+        result["roofline"]["traffic"] = rec[1]
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, W.view(-1))

@@ -8,31 +8,37 @@
 // the kernels reproduce it bit for bit (build with -ffp-contract=off, no fast
 // math, denormals kept).
 //
-// Construct kernel layout:
-//   * one wave (64 lanes) per workgroup; the wave takes tiles of 64
-//     consecutive groups in a grid-stride loop, and each lane owns one whole
-//     group, held in registers (G binary32 residuals) through every stage, so
-//     the bfloat16 input is read from HBM once and residuals never leave the
-//     register file;
-//   * the tile is loaded with fully coalesced 16-byte-per-lane loads and
-//     transposed through LDS (an XOR swizzle on the 16-byte chunk index keeps
-//     both the row writes and the per-lane group reads free of bank
-//     conflicts), so every lane receives the G contiguous elements of its
-//     group;
-//   * the group's range, scale, reciprocal and zero-point are computed once
-//     per lane per stage, i.e. once per group;
-//   * per element and stage: t = r * inv; u = t + (1.5 * 2^23 + z), which is
-//     the single nearest-even rounding of the exact t + z (u lies in
-//     [2^23, 2^24), where binary32 spacing is 1) and leaves the code in the
-//     two low mantissa bits of u; codes are packed by shift-adding u's bits
-//     (the constant upper bits of the 16 shifted words sum to a known
-//     constant, subtracted once per word); Q - z = u - (1.5 * 2^23 + z) exactly;
-//     rhat = (Q - z) * s; r = r - rhat.
-//   * Lower clamp: no element can round below code 0, because z is computed
-//     from the same fl(-lo * inv) that bounds every fl(r * inv) from below.
-//     Upper clamp: only the group maximum can reach code 4, so each lane tests
-//     its maximum first and the wave runs the clamped element loop only when
-//     one of its groups needs it.
+// Construct kernel:
+//   * one wave (64 lanes) per workgroup, two waves per SIMD; the wave takes
+//     tiles of 64 consecutive groups in a grid-stride loop, and each lane owns
+//     one whole group, held in registers (G binary32 residuals) through every
+//     stage, so the bfloat16 input is read from HBM once and residuals never
+//     leave the register file. The next tile is prefetched into registers
+//     while the current one is quantized;
+//   * the tile is loaded with fully coalesced 16-byte-per-lane buffer loads
+//     and transposed through LDS half a group at a time (rows padded by 16
+//     bytes, so row writes and per-lane column reads are free of bank
+//     conflicts); every lane then holds the G contiguous elements of its group;
+//   * per group and stage (once per lane): range lo = min(0, min r),
+//     hi = max(0, max r) (two-chain min3/max3, fused into the previous stage's
+//     residual update), s = fl((hi - lo) / 3), inv = fl(1 / s),
+//     z = RNE(fl(|lo| inv)), and a per-lane LDS table of dequantized pairs;
+//   * per element and stage: t = fl(r inv); u = fl(t + 1.5 * 2^23 + z) is the
+//     single nearest-even rounding of the exact t + z (u lies in [2^23, 2^24),
+//     where binary32 spacing is 1); one clamped FMA turns u into a tiny
+//     binary32 whose bit pattern is 3 - min(Q, 3); exact FMAs on such values
+//     pack the codes and form the LDS address of each element pair's
+//     dequantized values fl((Q - z) s); r = fl(r - rhat). Lanes past the input
+//     compute on zeros and their stores fall outside the buffer resources.
+//   * Clamp: no element can round below code 0 (z comes from the same
+//     fl(|lo| inv) that bounds every fl(r inv) from below); the upper clamp
+//     is needed in most tiles (a residual range symmetric about zero gives
+//     z = RNE(1.5) = 2 and puts its top element on code 4) and costs nothing
+//     here: it is the clamp modifier of the FMA above.
+// gfx950 issues fused multiply-add, add, multiply and bitwise logic at twice
+// the rate of shifts, min/max, three-operand integer and conversion
+// instructions (two waves dual-issue the former); the element loop is written
+// with the former wherever the arithmetic allows.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -43,18 +49,18 @@ namespace rrq_detail {
 namespace {
 
 constexpr float kMagic = 12582912.0f;          // 1.5 * 2^23
-constexpr uint32_t kMagicBits = 0x4B400000u;   // its binary32 bit pattern
-constexpr float kTopCode = kMagic + 3.0f;      // u of code 3
 
-// Sum over the 16 code slots of the constant upper bits of u, shifted to each
-// slot; subtracting it from the shift-added u words leaves the packed codes.
-constexpr uint32_t pack_bias()
-{
-    uint32_t b = 0;
-    for (int e = 0; e < 16; ++e) b += kMagicBits << (2 * e);
-    return b;
-}
-constexpr uint32_t kPackBias = pack_bias();
+// Codes as bit patterns of tiny binary32 values. For u = 1.5 * 2^23 + Q
+// (Q = RNE(t + z) in 0..4), fma(u, -2^-149, (1.5 * 2^23 + 3) 2^-149) is
+// exactly (3 - Q) 2^-149, and the instruction's clamp-to-[0, 1] modifier turns
+// Q = 4 into 0: the result's bit pattern is the integer k = 3 - min(Q, 3).
+// Every value below stays under 2^24 * 2^-149, where binary32 bit patterns
+// equal the integer multiple of 2^-149 and fused multiply-adds of such values
+// by powers of two are exact; so packing codes and forming LDS addresses are
+// single exact FMAs (full-rate on gfx950, unlike shifts, min/max or
+// three-operand integer instructions, which issue at half that rate).
+constexpr float kNegTiny = -0x1p-149f;              // -2^-149
+constexpr float kTopTiny = 0x1.800006p-126f;        // (1.5 * 2^23 + 3) * 2^-149
 
 // Raw buffer resources (gfx9 family descriptor). Accesses beyond num_records
 // bytes read as zero and stores there are dropped, which handles the ragged
@@ -64,6 +70,7 @@ using rsrc_t = __amdgpu_buffer_rsrc_t;
 constexpr int kRsrcWord3 = 0x00020000;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes)
 {
@@ -71,43 +78,29 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes)
                                              kRsrcWord3);
 }
 
-// acc + (bits << sh) as one v_lshl_add_u32 (the compiler would otherwise
-// re-associate the packing sums into shift + add3 pairs). sh is a constant
-// after unrolling, so the switch folds to one instruction.
-#define RRQ_LSHL_ADD_CASE(SH)                                                      \
-    case SH:                                                                     \
-        asm("v_lshl_add_u32 %0, %1, " #SH ", %2" : "=v"(out) : "v"(bits), "v"(acc)); \
-        break;
-__device__ __forceinline__ uint32_t lshl_add(uint32_t bits, int sh, uint32_t acc)
-{
-    uint32_t out;
-    switch (sh) {
-        RRQ_LSHL_ADD_CASE(2) RRQ_LSHL_ADD_CASE(4) RRQ_LSHL_ADD_CASE(6) RRQ_LSHL_ADD_CASE(8)
-        RRQ_LSHL_ADD_CASE(10) RRQ_LSHL_ADD_CASE(12) RRQ_LSHL_ADD_CASE(14) RRQ_LSHL_ADD_CASE(16)
-        RRQ_LSHL_ADD_CASE(18) RRQ_LSHL_ADD_CASE(20) RRQ_LSHL_ADD_CASE(22) RRQ_LSHL_ADD_CASE(24)
-        RRQ_LSHL_ADD_CASE(26) RRQ_LSHL_ADD_CASE(28) RRQ_LSHL_ADD_CASE(30)
-    default: out = acc + (bits << sh); break;
-    }
-    return out;
-}
-#undef RRQ_LSHL_ADD_CASE
-
-// Per-lane dequantization tables in LDS: entry q of lane l is fl((q - z) s)
-// of the lane's group for the current stage, at float index q * 64 + l, so
-// a wave's 64 lookups always touch 64 distinct banks.
+// Per-lane dequantization tables in LDS, one per wave. Entry idx = k[e] +
+// 4 k[e + 1] (k = 3 - code) of lane l holds the pair of dequantized values
+// {fl((Q[e] - z) s), fl((Q[e + 1] - z) s)} of the lane's group for the current
+// stage, at byte offset idx * 512 + l * 8: a wave's 64 lookups of one pair
+// of elements read 512 bytes that cover all banks once per half wave.
 struct DequantTable {
-    float *base;      // this wave's 4 x 64 floats
-    uint32_t adj;     // byte offset of (q, lane) minus (kMagicBits << 8), mod 2^32
+    float *base;      // this wave's 16 x 64 x 2 floats
+    float lane_off;   // binary32 whose bit pattern is l * 8
 };
+
+// Code of one element as the tiny binary32 (3 - min(Q, 3)) 2^-149, where
+// Q = RNE(fl(r inv) + z): t = fl(r inv); u = fl(t + 1.5 * 2^23 + z) rounds the
+// exact t + z once to the nearest integer, ties to even (u lies in
+// [2^23, 2^24), where binary32 spacing is 1).
+__device__ __forceinline__ float tiny_code(float r, float inv, float m)
+{
+    const float u = r * inv + m;   // two roundings: no contraction in this build
+    return __builtin_amdgcn_fmed3f(__builtin_fmaf(u, kNegTiny, kTopTiny), 0.0f, 1.0f);
+}
 
 // Element loop of one stage for one lane's group: the stage's codes into
 // words[]; with UPDATE also the residual r <- r - (Q - z) s and the range of
 // the new residual (lo, hi, zero included) for the next stage.
-//
-// Per element: t = fl(r inv); u = min(fl(t + m), code 3) holds code Q in its
-// low mantissa bits; the code is packed by a shift-add of u's bits; with
-// UPDATE, (u << 8) + adj is the LDS byte address of the lane's table entry Q,
-// so the dequantized value fl((Q - z) s) costs one VALU op and one LDS read.
 template <int G, bool UPDATE>
 __device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m,
                                                const DequantTable &tab,
@@ -115,26 +108,35 @@ __device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m
 {
     float l0 = 0.f, l1 = 0.f, h0 = 0.f, h1 = 0.f;
     const char *tbase = reinterpret_cast<const char *>(tab.base);
-    float rh[2][16];   // table lookups of two consecutive words in flight
+    f32x2 rh[2][8];   // table lookups of two consecutive words in flight
 
     // Codes of word w and (UPDATE) the lookups of its dequantized values.
-    auto quantize_word = [&](int w, float (&rhw)[16]) {
-        uint32_t acc = 0;
+    auto quantize_word = [&](int w, f32x2 (&rhw)[8]) {
+        float x[8];   // pair p: k[2p] + 4 k[2p + 1], as a tiny binary32
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const float t = r[w * 16 + e] * inv;
-            const float u = fminf(t + m, kTopCode);
-            const uint32_t ub = __float_as_uint(u);
-            acc = e == 0 ? ub : lshl_add(ub, 2 * e, acc);
-            if (UPDATE)
-                rhw[e] = *reinterpret_cast<const float *>(tbase + lshl_add(ub, 8, tab.adj));
+        for (int p = 0; p < 8; ++p) {
+            const int j = w * 16 + 2 * p;
+            x[p] = __builtin_fmaf(tiny_code(r[j + 1], inv, m), 4.0f, tiny_code(r[j], inv, m));
+            if (UPDATE) {
+                const uint32_t off = __float_as_uint(__builtin_fmaf(x[p], 512.0f, tab.lane_off));
+                rhw[p] = *reinterpret_cast<const f32x2 *>(tbase + off);
+            }
         }
-        words[w] = acc - kPackBias;
+        float q[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) q[i] = __builtin_fmaf(x[2 * i + 1], 16.0f, x[2 * i]);
+        const uint32_t lo16 = __float_as_uint(__builtin_fmaf(q[1], 256.0f, q[0]));
+        const uint32_t hi16 = __float_as_uint(__builtin_fmaf(q[3], 256.0f, q[2]));
+        // fields hold 3 - Q = Q ^ 3: complement to get the codes
+        words[w] = ~(lo16 | (hi16 << 16));
     };
     // Residual update of word w and its contribution to the next range.
-    auto update_word = [&](int w, const float (&rhw)[16]) {
+    auto update_word = [&](int w, const f32x2 (&rhw)[8]) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) r[w * 16 + e] = r[w * 16 + e] - rhw[e];
+        for (int p = 0; p < 8; ++p) {
+            r[w * 16 + 2 * p] = r[w * 16 + 2 * p] - rhw[p].x;
+            r[w * 16 + 2 * p + 1] = r[w * 16 + 2 * p + 1] - rhw[p].y;
+        }
 #pragma unroll
         for (int e = 0; e < 16; e += 4) {
             const int j = w * 16 + e;
@@ -210,19 +212,19 @@ __device__ __forceinline__ void load_tile(const uint4 *__restrict__ W, int64_t n
     }
 }
 
-// Reads this lane's group from the transposed LDS tile and widens bfloat16 to
-// binary32.
+// Reads half h of this lane's group (G / 2 elements) from the transposed LDS
+// buffer and widens bfloat16 to binary32.
 template <int G>
-__device__ __forceinline__ void gather_group(const uint4 *rd_base, float (&r)[G])
+__device__ __forceinline__ void gather_half(const uint4 *rd_base, int h, float (&r)[G])
 {
 #pragma unroll
-    for (int c = 0; c < G / 8; ++c) {
+    for (int c = 0; c < G / 16; ++c) {
         const uint4 w = rd_base[c];
         const uint32_t p[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-        for (int h = 0; h < 4; ++h) {
-            r[8 * c + 2 * h] = __uint_as_float(p[h] << 16);
-            r[8 * c + 2 * h + 1] = __uint_as_float(p[h] & 0xFFFF0000u);
+        for (int q = 0; q < 4; ++q) {
+            r[h * (G / 2) + 8 * c + 2 * q] = __uint_as_float(p[q] << 16);
+            r[h * (G / 2) + 8 * c + 2 * q + 1] = __uint_as_float(p[q] & 0xFFFF0000u);
         }
     }
 }
@@ -269,48 +271,65 @@ __device__ __forceinline__ void stage_params(float lo, float hi, float &inv, flo
     m = kMagic + z;
 }
 
-// Fills this lane's dequantization table for the stage: fl((q - z) s).
+// Fills this lane's dequantization table for the stage: entry k0 + 4 k1 is
+// {fl((3 - k0 - z) s), fl((3 - k1 - z) s)}.
 __device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, float sq, float z)
 {
+    float t[4];   // t[k] = fl((Q - z) s) for Q = 3 - k
 #pragma unroll
-    for (int q = 0; q < 4; ++q) tab.base[q * 64 + lane] = ((float)q - z) * sq;
+    for (int k = 0; k < 4; ++k) t[k] = ((float)(3 - k) - z) * sq;
+    f32x2 *row = reinterpret_cast<f32x2 *>(tab.base) + lane;
+#pragma unroll
+    for (int idx = 0; idx < 16; ++idx) row[idx * 64] = (f32x2){t[idx & 3], t[idx >> 2]};
 }
 
+// Two waves per SIMD: the G = 128 kernel holds 128 residuals plus the
+// prefetched next tile per lane, so 256 VGPRs is the budget.
 template <int G>
-__global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__ W,
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void construct_kernel(const uint4 *__restrict__ W,
                                                        int64_t n_groups, int n_stages,
                                                        uint32_t *__restrict__ codes,
                                                        float *__restrict__ scales,
                                                        float *__restrict__ zeros)
 {
     constexpr int CH = G / 8;            // 16-byte chunks (8 bfloat16) per group
+    constexpr int HC = CH / 2;           // chunks per half group
     constexpr int WPG = G / 16;          // code words per group and stage
-    constexpr int ROW = CH + 1;          // LDS row of one group, padded by 16 bytes
+    constexpr int ROW = HC + 1;          // LDS row of one half group, padded by 16 bytes
     constexpr int GROUPS_PER_LOAD = 64 / CH;
-    // Padding each group's row by one chunk spreads both access patterns over
-    // all banks: a row write (lanes -> consecutive chunks of a group) and a
-    // column read (lanes -> the same chunk of consecutive groups).
+    // The tile is transposed through LDS half a group at a time. Padding each
+    // row by one chunk spreads both access patterns over all banks: a row
+    // write (lanes -> consecutive chunks of a group) and a column read
+    // (lanes -> the same chunk of consecutive groups).
     __shared__ uint4 tile_lds[64 * ROW];
-    __shared__ float table_lds[4 * 64];
+    __shared__ f32x2 table_lds[16 * 64];
 
     const int lane = threadIdx.x;
     const int64_t n_tiles = (n_groups + 63) / 64;
-    uint4 *const wr_base = tile_lds + (lane / CH) * ROW + (lane % CH);
+    // A lane's loaded chunks all have the same index within their group
+    // (lane % CH), so each lane writes in exactly one of the two passes.
+    const int my_half = (lane % CH) / HC;
+    uint4 *const wr_base = tile_lds + (lane / CH) * ROW + (lane % HC);
     const uint4 *const rd_base = tile_lds + lane * ROW;
-    const DequantTable tab = {table_lds, (uint32_t)(lane * 4) - (kMagicBits << 8)};
+    const DequantTable tab = {reinterpret_cast<float *>(table_lds),
+                              __uint_as_float((uint32_t)lane * 8)};
 
     int64_t tile = blockIdx.x;
     uint4 v[CH];
     if (tile < n_tiles) load_tile<CH>(W, n_groups, tile, lane, v);
 
     for (; tile < n_tiles; tile += gridDim.x) {
-        __syncthreads();   // the previous tile's LDS reads are complete
-#pragma unroll
-        for (int i = 0; i < CH; ++i) wr_base[i * GROUPS_PER_LOAD * ROW] = v[i];
-        __syncthreads();
-
         float r[G];
-        gather_group<G>(rd_base, r);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __syncthreads();   // earlier reads of the buffer are complete
+            if (my_half == h) {
+#pragma unroll
+                for (int i = 0; i < CH; ++i) wr_base[i * GROUPS_PER_LOAD * ROW] = v[i];
+            }
+            __syncthreads();
+            gather_half<G>(rd_base, h, r);
+        }
 
         // Prefetch the next tile while this one is quantized.
         const int64_t next = tile + gridDim.x;
@@ -344,7 +363,6 @@ __global__ __launch_bounds__(64) void construct_kernel(const uint4 *__restrict__
 // sums the stages of each element left to right: acc = rhat_0,
 // acc = fl(acc + rhat_t).
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // x & 0x03030303, opaque to the compiler so that the byte conversions below
 // stay single v_cvt_f32_ubyte instructions.

@@ -56,6 +56,57 @@ def counters(directory: str, match):
     return out
 
 
+KERNEL_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "rrq_kernels.hip")
+
+
+def kernel_source_sha256() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def _mean_counter(directory, kernel, counter):
+    for k, c, v, n, d in counters(directory, [kernel]):
+        if c == counter and kernel in k:
+            return v, n, d
+    raise KeyError(f"{counter} for {kernel} not found under {directory}")
+
+
+def traffic(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, kernel, copy_bytes):
+    """HBM bytes per dispatch of `kernel`: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) each scaled by bytes / counter of a plain device copy of
+    copy_bytes bytes."""
+    fetch_kib, n_f, d_f = _mean_counter(fetch_dir, kernel, "FETCH_SIZE")
+    write_kib, n_w, d_w = _mean_counter(write_dir, kernel, "WRITE_SIZE")
+    copy_fetch_kib = _mean_counter(copy_fetch_dir, "copyBuffer", "FETCH_SIZE")[0]
+    copy_write_kib = _mean_counter(copy_write_dir, "copyBuffer", "WRITE_SIZE")[0]
+    f_scale = copy_bytes / (copy_fetch_kib * 1024)
+    w_scale = copy_bytes / (copy_write_kib * 1024)
+    read = fetch_kib * 1024 * f_scale
+    written = write_kib * 1024 * w_scale
+    return {"fetch_kib": fetch_kib, "write_kib": write_kib, "copy_fetch_kib": copy_fetch_kib,
+            "copy_write_kib": copy_write_kib, "fetch_scale": f_scale, "write_scale": w_scale,
+            "read_bytes": read, "written_bytes": written, "traffic_bytes": read + written,
+            "dispatches": (n_f, n_w), "mean_us": (d_f, d_w)}
+
+
+def read_traffic_profile(path):
+    """(kernel_source_sha256, traffic_bytes_per_launch) recorded in a traffic
+    profile, or None."""
+    try:
+        text = open(path).read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        for key in ("kernel_source_sha256", "traffic_bytes_per_launch"):
+            if line.strip().startswith(key + ":"):
+                vals[key] = line.split(":", 1)[1].strip().strip("`")
+    if len(vals) != 2:
+        return None
+    return vals["kernel_source_sha256"], float(vals["traffic_bytes_per_launch"])
+
+
 def stats(path: str, match):
     rows = []
     with open(path, newline="") as fh:
@@ -75,7 +126,34 @@ def main(argv=None):
     b = sub.add_parser("stats")
     b.add_argument("path")
     b.add_argument("--match", nargs="*", default=DEFAULT_MATCH)
+    t = sub.add_parser("traffic")
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--copy-fetch", required=True)
+    t.add_argument("--copy-write", required=True)
+    t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--kernel", required=True)
     args = ap.parse_args(argv)
+    if args.cmd == "traffic":
+        r = traffic(args.fetch, args.write, args.copy_fetch, args.copy_write, args.kernel,
+                    args.copy_bytes)
+        print(f"kernel: `{args.kernel}`")
+        print(f"kernel_source_sha256: `{kernel_source_sha256()}`")
+        print(f"traffic_bytes_per_launch: `{r['traffic_bytes']:.6e}`")
+        print()
+        print("| quantity | value |")
+        print("|---|---:|")
+        print(f"| FETCH_SIZE per dispatch (KiB) | {r['fetch_kib']:.6g} |")
+        print(f"| WRITE_SIZE per dispatch (KiB) | {r['write_kib']:.6g} |")
+        print(f"| copy probe: bytes copied | {args.copy_bytes} |")
+        print(f"| copy probe FETCH_SIZE (KiB) | {r['copy_fetch_kib']:.6g} |")
+        print(f"| copy probe WRITE_SIZE (KiB) | {r['copy_write_kib']:.6g} |")
+        print(f"| fetch scale (bytes per counted byte) | {r['fetch_scale']:.4f} |")
+        print(f"| write scale | {r['write_scale']:.4f} |")
+        print(f"| HBM bytes read per launch | {r['read_bytes']:.6e} |")
+        print(f"| HBM bytes written per launch | {r['written_bytes']:.6e} |")
+        print(f"| dispatches profiled (fetch, write) | {r['dispatches']} |")
+        return 0
     if args.cmd == "counters":
         print("| kernel | counter | mean per dispatch | dispatches | mean duration (us) |")
         print("|---|---|---:|---:|---:|")
