@@ -55,6 +55,8 @@ def _load():
         lib.rrq_oracle_reconstruct.restype = ctypes.c_int
         lib.rrq_oracle_threads.argtypes = []
         lib.rrq_oracle_threads.restype = ctypes.c_int
+        lib.rrq_oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.rrq_oracle_set_threads.restype = None
         _lib = lib
     return _lib
 
@@ -104,3 +106,8 @@ def c_reconstruct(codes: np.ndarray, scales: np.ndarray, zeros: np.ndarray,
 def c_threads() -> int:
     """OpenMP threads the C oracle runs with."""
     return int(_load().rrq_oracle_threads())
+
+
+def c_set_threads(n: int) -> None:
+    """Run the C oracle's parallel regions on n OpenMP threads."""
+    _load().rrq_oracle_set_threads(int(n))

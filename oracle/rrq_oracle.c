@@ -167,6 +167,12 @@ int rrq_oracle_reconstruct(const uint32_t *codes, const float *scales,
     return ORACLE_OK;
 }
 
+/* Sets the number of OpenMP threads for later calls (n >= 1). */
+void rrq_oracle_set_threads(int n)
+{
+    if (n >= 1) omp_set_num_threads(n);
+}
+
 /* Number of OpenMP threads a parallel region of this library uses. */
 int rrq_oracle_threads(void)
 {
