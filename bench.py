@@ -8,6 +8,9 @@ the full weight stack with every buffer resident in HBM:
 Default workload: the 36-layer Qwen3-8B-shaped stack (6.95e9 weights,
 13.9 GB bf16; Gaussian with 0.1% x20 outliers).
 
+After the steps, a streaming probe with the same read/write mix gives the
+practical HBM ceiling (include/hbm_probe.h).
+
 Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
 weights (2 bytes x weights / mean construct kernel time). The roofline entry
 is for the construct kernel: algorithmic HBM bytes per launch (bf16 in,
@@ -81,10 +84,42 @@ def cpu_baseline(w, W_dev, budget_s=12.0, threads=0):
             "kind": "oracle", "sample": sample}
 
 
+def stream_probe(src_bytes, flush_buf=None, launches=10):
+    """Practical HBM ceiling for construction's read/write mix: a streaming
+    kernel reading src_bytes and writing 5/8 of that (include/hbm_probe.h),
+    mean of `launches` HIP-event-timed launches on the current stream."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+
+    src_bytes -= src_bytes % 128
+    src = torch.empty(src_bytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty(src_bytes // 8 * 5 // 4, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        probe.hbm_probe_stream(src, src_bytes, dst, stream)
+    ms = []
+    for _ in range(launches):
+        if flush_buf is not None:
+            flush_buf.fill_(1.0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        probe.hbm_probe_stream(src, src_bytes, dst, stream)
+        b.record(stream)
+        b.synchronize()
+        ms.append(a.elapsed_time(b))
+    t = sum(ms) / len(ms)
+    moved = src_bytes + src_bytes // 8 * 5
+    gbs = moved / (t * 1e-3) / 1e9
+    del src, dst
+    return {"read_bytes": src_bytes, "written_bytes": src_bytes // 8 * 5, "ms": round(t, 4),
+            "gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="qwen3_8b_stack36")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -95,6 +130,11 @@ def main():
                     help="seconds of oracle compute for the CPU baseline sample")
     ap.add_argument("--cpu-threads", type=int, default=0, metavar="N",
                     help="OpenMP threads for the CPU baseline (default: all the runtime gives)")
+    ap.add_argument("--flush-mall", choices=("auto", "on", "off"), default="auto",
+                    help="write a 512 MiB buffer before each step so no input starts in the "
+                         "256 MB MALL (auto: on when the step moves under 4 GB)")
+    ap.add_argument("--no-stream-probe", action="store_true",
+                    help="skip the 2 : 1.25 read/write streaming probe")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device-to-device copy of MIB "
                          "MiB three times (calibrates profiler byte counters)")
@@ -146,7 +186,13 @@ def main():
     else:
         calls = [(W, rows, cols, codes, scales, zeros, outs)]
 
+    step_bytes = construct_bytes(n, G, S) + sum(reconstruct_bytes(n, G, k, 2) for k in w.recon_k)
+    flush = (args.flush_mall == "on" or (args.flush_mall == "auto" and step_bytes < 4e9))
+    flush_buf = torch.empty(512 << 18, dtype=torch.float32, device="cuda") if flush else None
+
     def step(evs=None):
+        if flush_buf is not None:
+            flush_buf.fill_(1.0)
         if evs is not None:
             evs[0].record(stream)
         for Wc, r_, c_, cc, sc, zz, _ in calls:
@@ -176,6 +222,8 @@ def main():
     cons_ms = [e[0].elapsed_time(e[1]) for e in events]
     rec_ms = {k: [e[1 + i].elapsed_time(e[2 + i]) for e in events] for i, k in enumerate(w.recon_k)}
     mean = lambda xs: sum(xs) / len(xs)
+    median = lambda xs: sorted(xs)[len(xs) // 2] if len(xs) % 2 else \
+        0.5 * (sorted(xs)[len(xs) // 2 - 1] + sorted(xs)[len(xs) // 2])
     c_ms = mean(cons_ms)
     bf16_gbs = 2 * n / (c_ms * 1e-3) / 1e9
     c_bytes = construct_bytes(n, G, S)
@@ -185,6 +233,8 @@ def main():
         r_ms = mean(rec_ms[k])
         recon[str(k)] = {
             "ms": round(r_ms, 4),
+            "ms_median": round(median(rec_ms[k]), 4),
+            "ms_min": round(min(rec_ms[k]), 4),
             "gbs_bf16_weights": round(2 * n / (r_ms * 1e-3) / 1e9, 2),
             "hbm_gbs": round(reconstruct_bytes(n, G, k, 2) / (r_ms * 1e-3) / 1e9, 2),
         }
@@ -215,8 +265,10 @@ def main():
             "recon_out": "bf16",
             "calls": (f"one call per tensor ({len(calls)} per kernel)" if args.per_tensor
                       else "one flat call per kernel over the whole stack"),
+            "mall_flush": flush,
         },
         "construct_ms": round(c_ms, 4),
+        "construct_ms_median": round(median(cons_ms), 4),
         "construct_ms_min": round(min(cons_ms), 4),
         "construct_hbm_frac": round(c_achieved / HBM_PEAK_GBS, 4),
         "reconstruct": recon,
@@ -239,6 +291,9 @@ def main():
     if (rec is not None and w.name == "qwen3_8b_stack36" and not args.per_tensor
             and rec[0] == profiling.kernel_source_sha256()):
         result["roofline"]["traffic"] = rec[1]
+    if not args.no_stream_probe:
+        result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
+        result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, W.view(-1), args.cpu_budget, args.cpu_threads)

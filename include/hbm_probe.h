@@ -1,0 +1,41 @@
+/*
+ * hbm_probe.h - C ABI of libhbm_probe.so: a streaming kernel that measures
+ * the practical HBM ceiling for the read/write mix of RRQ package
+ * construction. Construction reads 2 bytes per weight (bfloat16) and writes
+ * 1.25 (four 2-bit code planes plus binary32 scale and zero per group of
+ * 128), so the probe reads B bytes and writes 5B/8 bytes with the same kind
+ * of wide, coalesced accesses, and no arithmetic. Measurement aid only: it
+ * computes nothing of the method.
+ */
+#ifndef HBM_PROBE_H
+#define HBM_PROBE_H
+
+#include <stddef.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * hbm_probe_stream - enqueue one pass: src is read in full; of every 128
+ * bytes of src, the first 80 are written to the next 80 bytes of dst.
+ *
+ *   src        device, src_bytes bytes, 16-byte aligned (read only).
+ *   src_bytes  a positive multiple of 128.
+ *   dst        device, src_bytes / 8 * 5 bytes, 16-byte aligned (written);
+ *              must not overlap src.
+ *   stream     HIP stream the work is enqueued on.
+ *
+ * Returns 0, or 1 (NULL pointer), 2 (misaligned pointer), 3 (bad size) with
+ * nothing enqueued, or 7 if the launch failed. The caller owns both buffers;
+ * the library allocates nothing.
+ */
+int hbm_probe_stream(const void *src, size_t src_bytes, void *dst, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HBM_PROBE_H */

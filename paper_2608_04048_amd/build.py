@@ -1,4 +1,5 @@
-"""Build librrq.so (the HIP kernels and the C ABI) in-tree for gfx950.
+"""Build librrq.so (the HIP kernels and the C ABI) and libhbm_probe.so (the
+HBM streaming probe) in-tree for gfx950.
 
     python -m paper_2608_04048_amd.build          # compile, write the library
     python -m paper_2608_04048_amd.build --asm    # also keep the gfx950 assembly
@@ -20,6 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librrq.so")
+PROBE_LIB = os.path.join(PKG, "libhbm_probe.so")
 
 ARCH = "gfx950"
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
@@ -71,7 +73,19 @@ def build(keep_asm: bool = False) -> str:
     tmp = LIB + ".tmp"
     _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_obj, api_obj, "-o", tmp])
     os.replace(tmp, LIB)
+    build_probe()
     return LIB
+
+
+def build_probe() -> str:
+    """Compile libhbm_probe.so (the HBM streaming probe used by the benchmark)."""
+    cc = hipcc()
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    tmp = PROBE_LIB + ".tmp"
+    _run([cc, *DEVICE_FLAGS, f"-I{INCLUDE}", "-shared",
+          os.path.join(CSRC, "hbm_probe.hip"), "-o", tmp])
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 if __name__ == "__main__":

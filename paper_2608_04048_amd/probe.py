@@ -1,0 +1,37 @@
+"""Binding of libhbm_probe.so (include/hbm_probe.h): a streaming kernel with
+package construction's read/write ratio (reads B bytes, writes 5B/8), used by
+the benchmark as the practical HBM ceiling for that mix."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhbm_probe.so")
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2608_04048_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        lib.hbm_probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                         ctypes.c_void_p]
+        lib.hbm_probe_stream.restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def hbm_probe_stream(src, src_bytes: int, dst, stream=None) -> None:
+    """Enqueue one probe pass over src (device tensor or address) into dst."""
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    sp = stream if isinstance(stream, int) else stream.cuda_stream
+    ptr = lambda x: x if isinstance(x, int) else x.data_ptr()
+    st = load_library().hbm_probe_stream(ptr(src), int(src_bytes), ptr(dst), sp)
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_stream failed with status {st}")

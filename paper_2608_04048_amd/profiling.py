@@ -21,11 +21,11 @@ import os
 import sys
 from collections import defaultdict
 
-DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "copyBuffer"]
+DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "stream_probe_kernel", "copyBuffer"]
 
 
 def _short(name: str) -> str:
-    name = name.replace("rrq_detail::(anonymous namespace)::", "")
+    name = name.replace("rrq_detail::", "").replace("(anonymous namespace)::", "")
     return name.split("(")[0] if "(" in name else name
 
 

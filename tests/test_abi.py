@@ -142,3 +142,31 @@ def test_product_does_not_import_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "from oracle" not in text, f
                 assert "rrq_oracle" not in text, f
+
+
+PROBE_HEADER = os.path.join(ROOT, "include", "hbm_probe.h")
+
+
+def test_probe_library_exports_declared_function():
+    from paper_2608_04048_amd import probe
+    text = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(hbm_probe_\w+)\s*\(", text)))
+    assert names == ["hbm_probe_stream"]
+    lib = probe.load_library()
+    out = os.popen(f"nm -D --defined-only {probe.LIB_PATH}").read()
+    for name in names:
+        assert hasattr(lib, name)
+        assert f" T {name}" in out
+
+
+@pytest.mark.parametrize("src,nbytes,dst,status", [
+    (0, 1024, FAKE, 1),
+    (FAKE, 1024, 0, 1),
+    (FAKE_MISALIGNED, 1024, FAKE, 2),
+    (FAKE, 1024, FAKE_MISALIGNED, 2),
+    (FAKE, 0, FAKE, 3),
+    (FAKE, 1000, FAKE, 3),
+])
+def test_probe_rejects(src, nbytes, dst, status):
+    from paper_2608_04048_amd import probe
+    assert probe.load_library().hbm_probe_stream(src, nbytes, dst, None) == status
