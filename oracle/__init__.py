@@ -42,13 +42,16 @@ def build_c_oracle(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
             build_c_oracle(force=True)
         lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         lib.rrq_oracle_construct.argtypes = [P, ctypes.c_int64, ctypes.c_int32,
                                              ctypes.c_int32, P, P, P]
         lib.rrq_oracle_construct.restype = ctypes.c_int
+        lib.rrq_oracle_construct_from_base.argtypes = [P, ctypes.c_int64, ctypes.c_int32,
+                                                       ctypes.c_int32, P, P, P]
+        lib.rrq_oracle_construct_from_base.restype = ctypes.c_int
         lib.rrq_oracle_reconstruct.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32,
                                                ctypes.c_int32, ctypes.c_int32,
                                                ctypes.c_int32, P]
@@ -80,6 +83,30 @@ def c_construct(w_bits: np.ndarray, group_size: int, n_stages: int):
         raise ValueError("RRQ oracle: inputs must be finite")
     if rc == 3:
         raise ValueError("RRQ oracle: a group's range overflows binary32 (inputs need |x| < 2^127)")
+    if rc != 0:
+        raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
+    return codes, scales, zeros
+
+
+def c_construct_from_base(w_bits: np.ndarray, base_codes: np.ndarray, base_scales: np.ndarray,
+                          base_zeros: np.ndarray, group_size: int, n_stages: int):
+    """C oracle construction on a given base stage -> (codes, scales, zeros),
+    plane 0 = the base as given."""
+    lib = _load()
+    w = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
+    n = w.size
+    codes = np.empty((n_stages, n // 16), dtype=np.uint32)
+    scales = np.empty((n_stages, n // group_size), dtype=np.float32)
+    zeros = np.empty((n_stages, n // group_size), dtype=np.float32)
+    codes[0] = np.asarray(base_codes, dtype=np.uint32).reshape(-1)
+    scales[0] = np.asarray(base_scales, dtype=np.float32).reshape(-1)
+    zeros[0] = np.asarray(base_zeros, dtype=np.float32).reshape(-1)
+    rc = lib.rrq_oracle_construct_from_base(_ptr(w), n, group_size, n_stages,
+                                            _ptr(codes), _ptr(scales), _ptr(zeros))
+    if rc == 2:
+        raise ValueError("RRQ oracle: inputs and the base residual W - xhat_0 must be finite")
+    if rc == 3:
+        raise ValueError("RRQ oracle: a group's range overflows binary32")
     if rc != 0:
         raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
     return codes, scales, zeros

@@ -10,7 +10,8 @@
  * time as straight C so that large inputs finish in seconds:
  *   Eq. 1-3   per-group affine quantizer and its residual;
  *   Eq. 4-7   base stage on the weights, each later stage on the residual;
- *   Alg. 1    quantize / store / dequantize / subtract, no base checkpoint;
+ *   Alg. 1    quantize / store / dequantize / subtract, without a base
+ *             checkpoint and (second entry point) on a given base stage;
  *   Eq. 8     prefix reconstruction, also Eq. 18-19;
  *   Sec. 4.1  2-bit RTN stages, group size 128 (32 and 64 also accepted).
  *
@@ -118,6 +119,54 @@ int rrq_oracle_construct(const uint16_t *W, int64_t n, int32_t G, int32_t S,
             if (!isfinite(r[j])) bad = 1;
         }
         for (int k = 0; k < S; ++k) {
+            float s = 0.0f, z = 0.0f;
+            if (rtn_stage_group(r, G, 2, k + 1 < S, Q, &s, &z) != ORACLE_OK) bad_range = 1;
+            scales[(int64_t)k * n_groups + g] = s;
+            zeros[(int64_t)k * n_groups + g] = z;
+            for (int w = 0; w < G / 16; ++w) {
+                uint32_t word = 0;
+                for (int e = 0; e < 16; ++e)
+                    word |= (uint32_t)Q[w * 16 + e] << (2 * e);
+                codes[(int64_t)k * words + g * (G / 16) + w] = word;
+            }
+        }
+    }
+    return bad ? ORACLE_ERR_NONFINITE : bad_range ? ORACLE_ERR_RANGE : ORACLE_OK;
+}
+
+/*
+ * Algorithm 1 with a base checkpoint: plane 0 of codes / scales / zeros holds
+ * the base stage on entry (read only; any finite scale and zero-point, the
+ * zero-point not necessarily an integer). Each group's base is dequantized,
+ * xhat = fl(fl(Q - z) * s), the residual r = fl(W - xhat) is formed, and
+ * planes 1 .. S-1 receive the residual stages exactly as in
+ * rrq_oracle_construct.
+ */
+int rrq_oracle_construct_from_base(const uint16_t *W, int64_t n, int32_t G, int32_t S,
+                                   uint32_t *codes, float *scales, float *zeros)
+{
+    if (!W || !codes || !scales || !zeros) return ORACLE_ERR_ARGS;
+    if (G <= 0 || G > 1024 || G % 16 != 0 || n <= 0 || n % G != 0) return ORACLE_ERR_ARGS;
+    if (S < 1 || S > 8) return ORACLE_ERR_ARGS;
+    const int64_t n_groups = n / G;
+    const int64_t words = n / 16;
+    int bad = 0, bad_range = 0;
+
+#pragma omp parallel for schedule(static) reduction(| : bad, bad_range)
+    for (int64_t g = 0; g < n_groups; ++g) {
+        float r[1024];
+        uint8_t Q[1024];
+        const float s0 = scales[g], z0 = zeros[g];
+        for (int j = 0; j < G; ++j) {
+            const float w = bf16_to_f32(W[g * G + j]);
+            if (!isfinite(w)) bad = 1;
+            const uint32_t word = codes[g * (G / 16) + j / 16];
+            const float q0 = (float)((word >> (2 * (j % 16))) & 3u);
+            const float base = (q0 - z0) * s0;     /* two roundings, no FMA */
+            r[j] = w - base;
+            if (!isfinite(r[j])) bad = 1;
+        }
+        for (int k = 1; k < S; ++k) {
             float s = 0.0f, z = 0.0f;
             if (rtn_stage_group(r, G, 2, k + 1 < S, Q, &s, &z) != ORACLE_OK) bad_range = 1;
             scales[(int64_t)k * n_groups + g] = s;

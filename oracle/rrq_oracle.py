@@ -13,6 +13,9 @@ What it computes (paper, Sec. 3 "Recurrent Residual Quantization"):
   stage quantizes the residual the stages before it left behind;
 * Algorithm 1 without a base checkpoint: quantize, store codes / scales /
   zero-points, dequantize, subtract, repeated for every stage;
+* Algorithm 1 with a base checkpoint: the base's codes, scales and zero-points
+  are loaded and dequantized (a real-valued zero-point allowed), and only the
+  residual stages are computed;
 * the prefix reconstruction of Eq. 8 (restated as Eq. 18-19 in the
   prefill/decode appendix): the effective weight after t stages is the sum of
   the first t dequantized stages;
@@ -212,6 +215,75 @@ def construct(w_bits: np.ndarray, rows: int, cols: int, group_size: int,
     assert w_bits.size == rows * cols
     x = bf16_bits_to_f32(w_bits)
     Q, s, z, _, _ = construct_f32(x, group_size, n_stages, bits=2)
+    codes = np.stack([pack_codes(Q[k]) for k in range(n_stages)])
+    return codes, s, z
+
+
+# ---------------------------------------------------------------------------
+# Construction on an existing base checkpoint (Algorithm 1, the branch that
+# loads a base; Eq. 4-7)
+# ---------------------------------------------------------------------------
+
+def construct_from_base_f32(x: np.ndarray, base_Q: np.ndarray, base_s: np.ndarray,
+                            base_z: np.ndarray, group_size: int, n_stages: int,
+                            bits: int = 2):
+    """The RRQ recursion when a base checkpoint is given (Algorithm 1's
+    first branch): the base's codes, scales and zero-points are loaded, not
+    computed, and dequantized with the same affine rule as every stage
+    (Eq. 3): xhat_0 = fl(fl(Q_0 - z_0) * s_0). Then R_0 = fl(W - xhat_0)
+    (Eq. 5) and residual stages 1 .. S-1 quantize it as in ``construct_f32``.
+    The base's zero-point need not be an integer (a foreign quantizer may store
+    a real one), so Q_0 - z_0 is rounded like any binary32 difference.
+
+    ``x`` float32 [n]; ``base_Q`` uint8 codes [n]; ``base_s``, ``base_z``
+    float32 [n/G]. Returns (Q [S, n], s [S, n/G], z [S, n/G], rhat [S, n],
+    final residual [n]) with stage 0 = the base as given and rhat[0] = xhat_0.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
+    _check_shape(x.size, group_size)
+    if not np.all(np.isfinite(x)):
+        raise ValueError("RRQ oracle: inputs must be finite")
+    n_groups = x.size // group_size
+    Q0 = np.asarray(base_Q, dtype=np.uint8).reshape(n_groups, group_size)
+    s0 = np.asarray(base_s, dtype=np.float32).reshape(n_groups)
+    z0 = np.asarray(base_z, dtype=np.float32).reshape(n_groups)
+    if int(Q0.max(initial=0)) > (1 << bits) - 1:
+        raise ValueError("RRQ oracle: base codes out of range")
+
+    # Load and dequantize the base (Algorithm 1, first branch; Eq. 3).
+    qz0 = Q0.astype(np.float32) - z0[:, None]              # fl(Q_0 - z_0)
+    xhat0 = qz0 * s0[:, None]                                # fl(. * s_0)
+    r = x.reshape(n_groups, group_size) - xhat0             # R_0 = W - What_0
+    if not np.all(np.isfinite(r)):
+        raise ValueError("RRQ oracle: the base residual W - xhat_0 must be finite")
+
+    Qs, ss, zs, rhats = [Q0.reshape(-1)], [s0], [z0], [xhat0.reshape(-1)]
+    for k in range(1, n_stages):
+        Q, s, z, rhat = rtn_stage(r, bits)                  # residual stage k
+        Qs.append(Q.reshape(-1))
+        ss.append(s)
+        zs.append(z)
+        rhats.append(rhat.reshape(-1))
+        r = r - rhat                                         # R_k = R_{k-1} - Rhat_k
+    return (np.stack(Qs), np.stack(ss), np.stack(zs), np.stack(rhats),
+            r.reshape(-1))
+
+
+def construct_from_base(w_bits: np.ndarray, rows: int, cols: int, base_codes: np.ndarray,
+                        base_scales: np.ndarray, base_zeros: np.ndarray, group_size: int,
+                        n_stages: int):
+    """The package of the C-ABI call rrq_construct_from_base: bfloat16 weights
+    [rows, cols] (uint16 bits) and a base stage (packed codes [n/16] uint32,
+    scales and zeros [n/G] float32) -> codes [S, n/16], scales [S, n/G],
+    zeros [S, n/G], whose plane 0 is the base as given."""
+    if cols % group_size != 0:
+        raise ValueError("cols must be a multiple of the group size")
+    w_bits = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
+    assert w_bits.size == rows * cols
+    x = bf16_bits_to_f32(w_bits)
+    base_Q = unpack_codes(np.asarray(base_codes, dtype=np.uint32).reshape(-1))
+    Q, s, z, _, _ = construct_from_base_f32(x, base_Q, base_scales, base_zeros, group_size,
+                                            n_stages, bits=2)
     codes = np.stack([pack_codes(Q[k]) for k in range(n_stages)])
     return codes, s, z
 

@@ -36,6 +36,17 @@ MUTATIONS = {
     "recon_drops_last_stage": ("for t in range(1, k_stages):", "for t in range(1, k_stages - 1):"),
     "bf16_truncates": ("out = trunc + up.astype(np.uint64)", "out = trunc"),
     "degenerate_threshold_ignored": ("degenerate = s < SMALLEST_NORMAL_F32", "degenerate = s < 0"),
+    "base_dequant_zero_point_sign": ("qz0 = Q0.astype(np.float32) - z0[:, None]",
+                                     "qz0 = z0[:, None] - Q0.astype(np.float32)"),
+    "base_zero_point_dropped": ("qz0 = Q0.astype(np.float32) - z0[:, None]",
+                                "qz0 = Q0.astype(np.float32) + 0 * z0[:, None]"),
+    "base_scale_dropped": ("xhat0 = qz0 * s0[:, None]", "xhat0 = qz0 * 1"),
+    "base_residual_sign": ("r = x.reshape(n_groups, group_size) - xhat0",
+                           "r = xhat0 - x.reshape(n_groups, group_size)"),
+    "base_last_residual_stage_dropped": ("for k in range(1, n_stages):\n        Q, s, z, rhat = rtn_stage(r, bits)                  # residual stage k",
+                                         "for k in range(1, n_stages - 1):\n        Q, s, z, rhat = rtn_stage(r, bits)                  # residual stage k"),
+    "base_residual_not_updated": ("r = r - rhat                                         # R_k",
+                                  "r = r                                                # R_k"),
 }
 
 
@@ -132,7 +143,37 @@ def _battery(o) -> list:
         codes, s, z = o.construct(bits, 1, 32, 32, 4)
         return np.all(s == 0) and np.all(codes == 0)
 
+    def golden_from_base():
+        with open(os.path.join(HERE, "golden", "from_base_cases.json")) as fh:
+            cases = json.load(fh)["cases"]
+        for case in cases:
+            G, S = case["G"], case["S"]
+            words = np.array([int(h, 16) for h in case["base_codes"]], dtype=np.uint32)
+            s0, z0 = _f([case["base_scale"]]), _f([case["base_zero"]])
+            Q0 = ((words[:, None] >> (2 * np.arange(16, dtype=np.uint32))) & 3).reshape(-1)
+            xhat0 = (Q0.astype(np.float64) - float(z0[0])) * float(s0[0])
+            R0 = _f(case["residual"]).astype(np.float64)[(np.arange(G) // 4) % 4]
+            x = (xhat0 + R0).astype(np.float32)
+            bits = (x.view(np.uint32) >> 16).astype(np.uint16)
+            codes, s, z = o.construct_from_base(bits, 1, G, words, s0, z0, G, S)
+            for k, st in enumerate(case["stages"]):
+                if [f"{w:08X}" for w in codes[k]] != st["codes"]:
+                    return False
+                if f"{s[k].view(np.uint32)[0]:08X}" != st["s"] or f"{z[k].view(np.uint32)[0]:08X}" != st["z"]:
+                    return False
+        return True
+
+    def from_base_identities():
+        rng = np.random.default_rng(12)
+        x = (rng.standard_normal(128 * 64) * 0.02).astype(np.float32)
+        bits = (x.view(np.uint32) >> 16).astype(np.uint16)
+        full = o.construct(bits, 1, x.size, 128, 4)
+        got = o.construct_from_base(bits, 1, x.size, full[0][0], full[1][0], full[2][0], 128, 4)
+        return all(np.array_equal(a, b) for a, b in zip(full, got))
+
     check("golden_construct", golden_construct)
+    check("golden_from_base", golden_from_base)
+    check("from_base_identities", from_base_identities)
     check("golden_reconstruct", golden_reconstruct)
     check("invariants", invariants)
     check("crossover", crossover)
