@@ -8,8 +8,10 @@ the full weight stack with every buffer resident in HBM:
 Default workload: the 36-layer Qwen3-8B-shaped stack (6.95e9 weights,
 13.9 GB bf16; Gaussian with 0.1% x20 outliers).
 
-After the steps, a streaming probe with the same read/write mix gives the
-practical HBM ceiling (include/hbm_probe.h).
+After the steps: rrq_construct_from_base (the residual stages on a given base
+checkpoint; here the package's own stage 0) is timed on the same workload, and
+a streaming probe with the same read/write mix gives the practical HBM
+ceiling (include/hbm_probe.h).
 
 Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
 weights (2 bytes x weights / mean construct kernel time). The roofline entry
@@ -84,6 +86,37 @@ def cpu_baseline(w, W_dev, budget_s=12.0, threads=0):
             "kind": "oracle", "sample": sample}
 
 
+def from_base_bytes(n, G, S):
+    """Algorithmic HBM bytes of one rrq_construct_from_base launch: bf16 in,
+    the base stage's codes, scales and zeros in, S - 1 residual stages out."""
+    return 2 * n + n // 4 + 8 * (n // G) + (S - 1) * n // 4 + 8 * (S - 1) * (n // G)
+
+
+def time_from_base(calls, G, S, stream, flush_buf=None, launches=20):
+    """Mean / min time of rrq_construct_from_base over the workload, with the
+    package's own stage 0 (already in plane 0) as the base checkpoint."""
+    import torch
+
+    import paper_2608_04048_amd as rrq
+
+    def run():
+        for Wc, r_, c_, cc, sc, zz, _ in calls:
+            rrq.rrq_construct_from_base(Wc, r_, c_, G, S, cc, sc, zz, stream)
+
+    run()
+    ms = []
+    for _ in range(launches):
+        if flush_buf is not None:
+            flush_buf.fill_(1.0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        run()
+        b.record(stream)
+        b.synchronize()
+        ms.append(a.elapsed_time(b))
+    return sum(ms) / len(ms), min(ms)
+
+
 def stream_probe(src_bytes, flush_buf=None, launches=10):
     """Practical HBM ceiling for construction's read/write mix: a streaming
     kernel reading src_bytes and writing 5/8 of that (include/hbm_probe.h),
@@ -133,6 +166,8 @@ def main():
     ap.add_argument("--flush-mall", choices=("auto", "on", "off"), default="auto",
                     help="write a 512 MiB buffer before each step so no input starts in the "
                          "256 MB MALL (auto: on when the step moves under 4 GB)")
+    ap.add_argument("--no-from-base", action="store_true",
+                    help="skip timing rrq_construct_from_base (residual stages on a given base)")
     ap.add_argument("--no-stream-probe", action="store_true",
                     help="skip the 2 : 1.25 read/write streaming probe")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -291,6 +326,18 @@ def main():
     if (rec is not None and w.name == "qwen3_8b_stack36" and not args.per_tensor
             and rec[0] == profiling.kernel_source_sha256()):
         result["roofline"]["traffic"] = rec[1]
+    if S >= 2 and not args.no_from_base:
+        fb_ms, fb_min = time_from_base(calls, G, S, stream, flush_buf)
+        fb_bytes = from_base_bytes(n, G, S)
+        result["from_base"] = {
+            "kernel": f"construct_kernel<{G}, from base>",
+            "ms": round(fb_ms, 4), "ms_min": round(fb_min, 4),
+            "gbs_bf16_weights": round(2 * n / (fb_ms * 1e-3) / 1e9, 2),
+            "hbm_gbs": round(fb_bytes / (fb_ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(fb_bytes / (fb_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "bytes_per_launch": fb_bytes,
+            "base": "stage 0 of the package built in the steps",
+        }
     if not args.no_stream_probe:
         result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
         result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)

@@ -7,9 +7,10 @@
  *   - Eq. 1-3: a group of G weights shares a scale s and zero-point z;
  *     q = x/s + z, Q = R(q), and the stage leaves the residual
  *     r = x - (Q - z) s.
- *   - Eq. 4-7 and Algorithm 1: the base stage quantizes the weights, each
- *     further stage quantizes the residual left by the stages before it; every
- *     stage stores its own codes, scales and zero-points.
+ *   - Eq. 4-7 and Algorithm 1: the base stage quantizes the weights (or an
+ *     existing base checkpoint is loaded), each further stage quantizes the
+ *     residual left by the stages before it; every stage stores its own
+ *     codes, scales and zero-points.
  *   - Eq. 8 (restated as Eq. 18-19): the effective weight after t stages is
  *     the sum of the first t dequantized stages.
  *   - Sec. 4.1: the main configuration is four calibration-free 2-bit RTN
@@ -114,6 +115,44 @@ enum rrq_dtype {
 int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
                   int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
                   hipStream_t stream);
+
+/*
+ * rrq_construct_from_base - build the residual stages of an RRQ package on
+ * an existing base checkpoint (Algorithm 1's first branch: the base stage's
+ * codes, scales and zero-points are loaded, not computed; Eq. 4-7; the paper
+ * presents this as the reuse of an existing low-bit checkpoint).
+ *
+ * On entry plane 0 of the package holds the base stage in this library's
+ * layout: 2-bit codes Q_0 packed as above, and binary32 scales s_0 and
+ * zero-points z_0 per group. Any finite s_0 and z_0 are accepted; z_0 need not
+ * be an integer (a base from another quantizer may store a real zero-point).
+ * Per element the base is dequantized as xhat_0 = fl(fl(Q_0 - z_0) * s_0)
+ * (for an integer z_0 that is exactly the stage value of rrq_construct), the
+ * residual R_0 = fl(W - xhat_0) is formed, and stages 1 .. n_stages - 1 are
+ * the residual stages of rrq_construct applied to R_0, with the same
+ * arithmetic. A base that equals rrq_construct's own stage 0 therefore
+ * reproduces rrq_construct's package bit for bit.
+ *
+ *   W          as for rrq_construct. Precondition: every W and every
+ *              R_0 = W - xhat_0 finite with a finite per-group range (holds
+ *              when all |W| < 2^126 and all |xhat_0| < 2^126); otherwise the
+ *              residual stages are unspecified (nothing outside the buffers
+ *              is touched).
+ *   rows, cols, group_size  as for rrq_construct.
+ *   n_stages   S in 1..4, counting the base: planes 1 .. S-1 are written.
+ *              S = 1 leaves the package as it is and enqueues nothing.
+ *   codes      device, uint32 [S][rows*cols/16], 16-byte aligned: plane 0 read,
+ *              planes 1 .. S-1 written.
+ *   scales     device, float [S][rows*cols/G], 4-byte aligned: same planes.
+ *   zeros      device, float [S][rows*cols/G], 4-byte aligned: same planes.
+ *   stream     HIP stream the work is enqueued on.
+ *
+ * Returns RRQ_OK, or RRQ_ERR_NULL / _ALIGN / _SHAPE / _GROUP / _STAGES with
+ * nothing enqueued, or RRQ_ERR_HIP if the kernel launch failed.
+ */
+int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                            int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
+                            hipStream_t stream);
 
 /*
  * rrq_reconstruct - effective weight of the first k_stages stages of a

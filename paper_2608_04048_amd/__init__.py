@@ -2,11 +2,11 @@
 reconstruction on AMD Instinct MI355X.
 
 Thin Python binding of librrq.so (include/rrq.h). The functions named like the
-C ABI (``rrq_construct``, ``rrq_reconstruct``, ``rrq_package_bytes``,
-``rrq_status_string``) only marshal arguments: tensors become device pointers,
+C ABI (``rrq_construct``, ``rrq_construct_from_base``, ``rrq_reconstruct``,
+``rrq_package_bytes``, ``rrq_status_string``) only marshal arguments: tensors become device pointers,
 the stream defaults to torch's current stream, and a nonzero status raises
-``RRQError``. ``construct`` and ``reconstruct`` additionally allocate the
-output tensors with torch. Every computation runs in the HIP kernels; there is
+``RRQError``. ``construct``, ``construct_from_base`` and ``reconstruct``
+additionally allocate the output tensors with torch. Every computation runs in the HIP kernels; there is
 no fallback, and a missing library raises.
 """
 
@@ -56,6 +56,8 @@ def load_library() -> ctypes.CDLL:
         P, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         lib.rrq_construct.argtypes = [P, I64, I64, I32, I32, P, P, P, P]
         lib.rrq_construct.restype = ctypes.c_int
+        lib.rrq_construct_from_base.argtypes = [P, I64, I64, I32, I32, P, P, P, P]
+        lib.rrq_construct_from_base.restype = ctypes.c_int
         lib.rrq_reconstruct.argtypes = [P, P, P, I64, I64, I32, I32, I32, P, I32, P]
         lib.rrq_reconstruct.restype = ctypes.c_int
         lib.rrq_package_bytes.argtypes = [I64, I64, I32, I32, ctypes.POINTER(ctypes.c_size_t),
@@ -112,6 +114,17 @@ def rrq_construct(W, rows: int, cols: int, group_size: int, n_stages: int,
         raise RRQError(st, "rrq_construct")
 
 
+def rrq_construct_from_base(W, rows: int, cols: int, group_size: int, n_stages: int,
+                            codes, scales, zeros, stream=None) -> None:
+    """Enqueue the residual stages on the base stage held in plane 0 of the
+    package (see include/rrq.h)."""
+    st = load_library().rrq_construct_from_base(_ptr(W), rows, cols, group_size, n_stages,
+                                                _ptr(codes), _ptr(scales), _ptr(zeros),
+                                                _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_construct_from_base")
+
+
 def rrq_reconstruct(codes, scales, zeros, rows: int, cols: int, group_size: int,
                     n_stages: int, k_stages: int, W_out, out_dtype: int, stream=None) -> None:
     """Enqueue prefix-k reconstruction (see include/rrq.h)."""
@@ -155,6 +168,27 @@ def construct(W, group_size: int = 128, n_stages: int = 4, stream=None, out=None
     else:
         codes, scales, zeros = out
     rrq_construct(W, rows, cols, group_size, n_stages, codes, scales, zeros, stream)
+    return codes, scales, zeros
+
+
+def construct_from_base(W, base_codes, base_scales, base_zeros, group_size: int = 128,
+                        n_stages: int = 4, stream=None):
+    """RRQ package of a bfloat16 matrix W [rows, cols] on an existing base
+    stage (base_codes int32 [N/16] holding uint32 words, base_scales and
+    base_zeros float32 [N/G], all on W's device). Allocates the package,
+    copies the base into plane 0 and builds planes 1 .. S-1 on the GPU.
+    Returns (codes, scales, zeros) as ``construct`` does."""
+    import torch
+    _check_device_tensor(W, "W", torch.bfloat16)
+    rows, cols = (W.shape[0], W.shape[1]) if W.dim() == 2 else (1, W.numel())
+    n = rows * cols
+    codes = torch.empty((n_stages, n // 16), dtype=torch.int32, device=W.device)
+    scales = torch.empty((n_stages, n // group_size), dtype=torch.float32, device=W.device)
+    zeros = torch.empty((n_stages, n // group_size), dtype=torch.float32, device=W.device)
+    codes[0].copy_(base_codes.reshape(-1).view(torch.int32))
+    scales[0].copy_(base_scales.reshape(-1))
+    zeros[0].copy_(base_zeros.reshape(-1))
+    rrq_construct_from_base(W, rows, cols, group_size, n_stages, codes, scales, zeros, stream)
     return codes, scales, zeros
 
 

@@ -76,7 +76,27 @@ extern "C" int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int3
     st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
-                                                zeros, grid, stream);
+                                                zeros, false, grid, stream);
+    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+}
+
+extern "C" int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols,
+                                       int32_t group_size, int32_t n_stages, uint32_t *codes,
+                                       float *scales, float *zeros, hipStream_t stream)
+{
+    if (!W || !codes || !scales || !zeros) return RRQ_ERR_NULL;
+    int64_t n = 0;
+    int st = check_common(rows, cols, group_size, n_stages, &n);
+    if (st != RRQ_OK) return st;
+    if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4))
+        return RRQ_ERR_ALIGN;
+    if (n_stages == 1) return RRQ_OK;   // the package is the base alone: nothing to build
+    const int64_t n_groups = n / group_size;
+    int grid = 0;
+    st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
+    if (st != RRQ_OK) return st;
+    hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
+                                                zeros, true, grid, stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 

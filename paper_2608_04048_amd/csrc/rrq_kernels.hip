@@ -1,9 +1,11 @@
 // HIP kernels for RRQ package construction and prefix reconstruction on
 // gfx950 (MI355X).
 //
-// Construction follows Algorithm 1 (no base checkpoint) with the per-group
-// affine RTN stage of Eq. 1-3 applied S times, each stage to the residual the
-// earlier stages left (Eq. 4-7). Reconstruction is the prefix sum of Eq. 8 /
+// Construction follows Algorithm 1 with the per-group affine RTN stage of
+// Eq. 1-3 applied S times, each stage to the residual the earlier stages left
+// (Eq. 4-7); either the base stage is quantized too, or (Algorithm 1's first
+// branch) a given base stage is dequantized and only the residual stages are
+// built. Reconstruction is the prefix sum of Eq. 8 /
 // Eq. 18-19. The arithmetic is the fixed binary32 reading stated in rrq.h;
 // the kernels reproduce it bit for bit (build with -ffp-contract=off, no fast
 // math, denormals kept).
@@ -162,6 +164,58 @@ __device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m
     hi = fmaxf(h0, h1);
 }
 
+// Base stage of a loaded checkpoint (Algorithm 1, first branch), for half
+// HALF of the lane's group (G / 2 elements): each element becomes
+// r - fl(fl(Q_0 - z_0) s_0), looked up in the lane's pair table (filled for
+// s_0, z_0), and the result's range is folded into (l0, l1, h0, h1). The
+// table index of an element pair is k0 + 4 k1 with k = 3 - Q, which is the
+// pair's nibble of the complemented code word.
+template <int G, int HALF>
+__device__ __forceinline__ void subtract_base_half(float (&r)[G], const uint32_t (&bw)[G / 16],
+                                                   const DequantTable &tab, float &l0, float &l1,
+                                                   float &h0, float &h1)
+{
+    const char *tbase = reinterpret_cast<const char *>(tab.base);
+    const uint32_t lane_off = __float_as_uint(tab.lane_off);   // lane * 8 < 512
+    f32x2 rh[2][4];   // lookups of two consecutive 8-element pieces in flight
+    constexpr int H0 = HALF * (G / 16), H1 = H0 + G / 16;    // 8-element pieces
+
+    auto lookup = [&](int h, f32x2 (&rhh)[4]) {
+        const uint32_t kw = ~bw[h >> 1];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int p = (h & 1) * 4 + i;
+            // nibble p of kw, times 512
+            const uint32_t nib = (4 * p <= 9) ? (kw << (9 - 4 * p)) & 0x1E00u
+                                              : (kw >> (4 * p - 9)) & 0x1E00u;
+            rhh[i] = *reinterpret_cast<const f32x2 *>(tbase + (nib | lane_off));
+        }
+    };
+    auto apply = [&](int h, const f32x2 (&rhh)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            r[h * 8 + 2 * i] = r[h * 8 + 2 * i] - rhh[i].x;
+            r[h * 8 + 2 * i + 1] = r[h * 8 + 2 * i + 1] - rhh[i].y;
+        }
+#pragma unroll
+        for (int e = 0; e < 8; e += 4) {
+            const int j = h * 8 + e;
+            l0 = fminf(fminf(l0, r[j]), r[j + 1]);
+            h0 = fmaxf(fmaxf(h0, r[j]), r[j + 1]);
+            l1 = fminf(fminf(l1, r[j + 2]), r[j + 3]);
+            h1 = fmaxf(fmaxf(h1, r[j + 2]), r[j + 3]);
+        }
+    };
+
+    lookup(H0, rh[0]);
+#pragma unroll
+    for (int h = H0; h < H1; ++h) {
+        if (h + 1 < H1) lookup(h + 1, rh[(h + 1) & 1]);
+        apply(h, rh[h & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 template <int G>
 __device__ __forceinline__ void group_range(const float (&r)[G], float &lo, float &hi)
 {
@@ -196,15 +250,18 @@ __device__ __forceinline__ void store_words(rsrc_t dst, uint32_t off, const uint
 
 // Loads this lane's share of one tile (64 groups): chunk q = 64 i + lane of
 // the tile's 16-byte chunks, so each load instruction covers 1 KiB
-// contiguously. Chunks past the end of the input read as zero.
+// contiguously. Chunks past the end of the input read as zero, and a tile
+// past the end reads all zeros (a zero-sized resource): the prefetch of a
+// next tile needs no branch, which keeps the compiler from moving the
+// current tile's arithmetic across one.
 template <int CH>
 __device__ __forceinline__ void load_tile(const uint4 *__restrict__ W, int64_t n_groups,
                                           int64_t tile, int lane, uint4 (&v)[CH])
 {
     const int64_t g0 = tile * 64;
     const int64_t left = n_groups - g0;
-    const uint32_t bytes = (uint32_t)(left < 64 ? left : 64) * CH * 16;
-    const rsrc_t src = make_rsrc(W + g0 * CH, bytes);
+    const uint32_t bytes = left <= 0 ? 0u : (uint32_t)(left < 64 ? left : 64) * CH * 16;
+    const rsrc_t src = make_rsrc(W + (left <= 0 ? 0 : g0 * CH), bytes);
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
         const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(src, (i * 64 + lane) * 16, 0, 0);
@@ -283,15 +340,43 @@ __device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, fl
     for (int idx = 0; idx < 16; ++idx) row[idx * 64] = (f32x2){t[idx & 3], t[idx >> 2]};
 }
 
+// Loads one lane's base stage (plane 0 of the package): its group's code
+// words, scale and zero-point. Lanes past the input read zeros.
+template <int G>
+__device__ __forceinline__ void load_base(const uint32_t *codes, const float *scales,
+                                          const float *zeros, int64_t g0, uint32_t groups_here,
+                                          int lane, uint32_t (&bw)[G / 16], float &s0, float &z0)
+{
+    const rsrc_t rc = make_rsrc(codes + g0 * (G / 16), groups_here * (G / 16) * 4);
+    if constexpr (G / 16 >= 4) {
+#pragma unroll
+        for (int i = 0; i < G / 16; i += 4) {
+            const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rc, lane * (G / 16) * 4 + 4 * i, 0, 0);
+            bw[i] = x.x; bw[i + 1] = x.y; bw[i + 2] = x.z; bw[i + 3] = x.w;
+        }
+    } else {
+        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(rc, lane * (G / 16) * 4, 0, 0);
+        bw[0] = x.x; bw[1] = x.y;
+    }
+    s0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        make_rsrc(scales + g0, groups_here * 4), lane * 4, 0, 0));
+    z0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+        make_rsrc(zeros + g0, groups_here * 4), lane * 4, 0, 0));
+}
+
 // Two waves per SIMD: the G = 128 kernel holds 128 residuals plus the
 // prefetched next tile per lane, so 256 VGPRs is the budget.
-template <int G>
+// FROM_BASE: plane 0 of codes / scales / zeros holds a base checkpoint on
+// entry (read only); the kernel forms R_0 = W - dequant(base) and writes the
+// residual stages 1 .. n_stages - 1 (n_stages >= 2).
+template <int G, bool FROM_BASE>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void construct_kernel(const uint4 *__restrict__ W,
                                                        int64_t n_groups, int n_stages,
                                                        uint32_t *__restrict__ codes,
                                                        float *__restrict__ scales,
                                                        float *__restrict__ zeros)
 {
+    if (FROM_BASE && n_stages < 2) return;
     constexpr int CH = G / 8;            // 16-byte chunks (8 bfloat16) per group
     constexpr int HC = CH / 2;           // chunks per half group
     constexpr int WPG = G / 16;          // code words per group and stage
@@ -319,7 +404,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     if (tile < n_tiles) load_tile<CH>(W, n_groups, tile, lane, v);
 
     for (; tile < n_tiles; tile += gridDim.x) {
+        const int64_t g0 = tile * 64;
+        const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
+        uint32_t bw[WPG];
+        float bs = 0.f, bz = 0.f;
+        if constexpr (FROM_BASE) load_base<G>(codes, scales, zeros, g0, groups_here, lane, bw, bs, bz);
+
         float r[G];
+        float bl0 = 0.f, bl1 = 0.f, bh0 = 0.f, bh1 = 0.f;   // range of R_0 (with a base)
+        if constexpr (FROM_BASE) fill_table(tab, lane, bs, bz);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             __syncthreads();   // earlier reads of the buffer are complete
@@ -329,21 +422,28 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             }
             __syncthreads();
             gather_half<G>(rd_base, h, r);
+            // With a base checkpoint, R_0 = W - dequant(base), half by half.
+            if constexpr (FROM_BASE) {
+                if (h == 0) subtract_base_half<G, 0>(r, bw, tab, bl0, bl1, bh0, bh1);
+                else subtract_base_half<G, 1>(r, bw, tab, bl0, bl1, bh0, bh1);
+            }
         }
 
         // Prefetch the next tile while this one is quantized.
-        const int64_t next = tile + gridDim.x;
-        if (next < n_tiles) load_tile<CH>(W, n_groups, next, lane, v);
+        load_tile<CH>(W, n_groups, tile + gridDim.x, lane, v);
 
-        const int64_t g0 = tile * 64;
-        const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
         const TileOut out = {codes + g0 * WPG, scales + g0, zeros + g0,
                              n_groups * WPG, n_groups, groups_here * WPG * 4, groups_here * 4};
 
         float lo, hi, inv, sq, z, m;
         uint32_t words[WPG];
-        group_range<G>(r, lo, hi);
-        for (int k = 0; k + 1 < n_stages; ++k) {
+        if constexpr (FROM_BASE) {
+            lo = fminf(bl0, bl1);
+            hi = fmaxf(bh0, bh1);
+        } else {
+            group_range<G>(r, lo, hi);
+        }
+        for (int k = FROM_BASE ? 1 : 0; k + 1 < n_stages; ++k) {
             stage_params(lo, hi, inv, sq, z, m);
             fill_table(tab, lane, sq, z);
             stage_elements<G, true>(r, inv, m, tab, words, lo, hi);
@@ -464,17 +564,26 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
 
 }  // namespace
 
-hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
-                            uint32_t *codes, float *scales, float *zeros, int grid,
-                            hipStream_t stream)
+template <bool FROM_BASE>
+hipError_t launch_construct_g(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
+                              float *scales, float *zeros, int grid, hipStream_t stream)
 {
-    const uint4 *w4 = reinterpret_cast<const uint4 *>(W);
     switch (G) {
-    case 32: return launch(construct_kernel<32>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
-    case 64: return launch(construct_kernel<64>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
-    case 128: return launch(construct_kernel<128>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 32: return launch(construct_kernel<32, FROM_BASE>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 64: return launch(construct_kernel<64, FROM_BASE>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 128: return launch(construct_kernel<128, FROM_BASE>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
     default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
+                            uint32_t *codes, float *scales, float *zeros, bool from_base,
+                            int grid, hipStream_t stream)
+{
+    const uint4 *w4 = reinterpret_cast<const uint4 *>(W);
+    return from_base
+               ? launch_construct_g<true>(w4, n_groups, G, S, codes, scales, zeros, grid, stream)
+               : launch_construct_g<false>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
 }
 
 template <int K, bool BF16>

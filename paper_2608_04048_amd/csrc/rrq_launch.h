@@ -9,8 +9,10 @@
 namespace rrq_detail {
 
 // Package construction of n_groups groups of G bfloat16 weights, S stages.
+// from_base: stage 0 of the package is an input (a base checkpoint) and only
+// stages 1 .. S-1 are written.
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
-                            uint32_t *codes, float *scales, float *zeros,
+                            uint32_t *codes, float *scales, float *zeros, bool from_base,
                             int grid, hipStream_t stream);
 
 // Prefix-k reconstruction of a package with n_groups groups of G, S stages.

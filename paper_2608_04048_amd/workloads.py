@@ -140,3 +140,38 @@ def materialize(w: Workload, device="cuda"):
     for t in w.tensors:
         buf[t.offset:t.offset + t.numel].view(t.rows, t.cols).copy_(draw(t, device))
     return buf
+
+
+BASE_CHECKPOINT_SEED_OFFSET = 7919
+
+
+def draw_base(n: int, group_size: int, seed: int, device="cuda"):
+    """A stand-in for a base checkpoint from another quantizer, for n weights
+    in groups of group_size: uniformly random 2-bit codes (packed, 16 per
+    uint32 word, returned as int32 [n/16]), per-group scales uniform in
+    [0.01, 0.09] (the magnitude of 2-bit min-max scales of the weights above)
+    and real-valued zero-points uniform in [0, 3) (float32 [n/G] each)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    codes = torch.randint(-2 ** 31, 2 ** 31, (n // 16,), generator=g, device=device,
+                          dtype=torch.int64).to(torch.int32)
+    scales = torch.rand(n // group_size, generator=g, device=device).mul_(0.08).add_(0.01)
+    zeros = torch.rand(n // group_size, generator=g, device=device).mul_(3.0)
+    return codes, scales, zeros
+
+
+def materialize_base(w: Workload, device="cuda"):
+    """Flat base-checkpoint buffers (codes, scales, zeros) for every tensor of
+    w, laid out like the weights (tensor t's groups at t.offset / G)."""
+    import torch
+    G = w.group_size
+    codes = torch.empty(w.numel // 16, dtype=torch.int32, device=device)
+    scales = torch.empty(w.numel // G, dtype=torch.float32, device=device)
+    zeros = torch.empty(w.numel // G, dtype=torch.float32, device=device)
+    for t in w.tensors:
+        c, s, z = draw_base(t.numel, G, t.seed + BASE_CHECKPOINT_SEED_OFFSET, device)
+        codes[t.offset // 16:(t.offset + t.numel) // 16].copy_(c)
+        scales[t.offset // G:(t.offset + t.numel) // G].copy_(s)
+        zeros[t.offset // G:(t.offset + t.numel) // G].copy_(z)
+    return codes, scales, zeros

@@ -31,7 +31,8 @@ def _declared_enums():
 def test_library_exports_every_declared_function():
     lib = rrq.load_library()
     names = _declared_functions()
-    assert names == ["rrq_construct", "rrq_package_bytes", "rrq_reconstruct", "rrq_status_string"]
+    assert names == ["rrq_construct", "rrq_construct_from_base", "rrq_package_bytes",
+                     "rrq_reconstruct", "rrq_status_string"]
     for name in names:
         assert hasattr(lib, name), name
     out = os.popen(f"nm -D --defined-only {rrq.LIB_PATH}").read()
@@ -100,6 +101,39 @@ def _reconstruct_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, 
 ])
 def test_construct_rejects(kw, status):
     assert _construct_status(**kw) == status
+
+
+def _from_base_status(W=FAKE, rows=64, cols=128, G=128, S=4, codes=FAKE, scales=FAKE, zeros=FAKE):
+    lib = rrq.load_library()
+    return lib.rrq_construct_from_base(W, rows, cols, G, S, codes, scales, zeros, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(W=None), rrq.RRQ_ERR_NULL),
+    (dict(codes=None), rrq.RRQ_ERR_NULL),
+    (dict(scales=None), rrq.RRQ_ERR_NULL),
+    (dict(zeros=None), rrq.RRQ_ERR_NULL),
+    (dict(G=16), rrq.RRQ_ERR_GROUP),
+    (dict(S=0), rrq.RRQ_ERR_STAGES),
+    (dict(S=5), rrq.RRQ_ERR_STAGES),
+    (dict(cols=100), rrq.RRQ_ERR_SHAPE),
+    (dict(rows=0), rrq.RRQ_ERR_SHAPE),
+    (dict(rows=1 << 62, cols=128), rrq.RRQ_ERR_SHAPE),
+    (dict(W=FAKE + 8), rrq.RRQ_ERR_ALIGN),
+    (dict(codes=FAKE_MISALIGNED), rrq.RRQ_ERR_ALIGN),
+    (dict(scales=FAKE + 2), rrq.RRQ_ERR_ALIGN),
+    (dict(zeros=FAKE + 1), rrq.RRQ_ERR_ALIGN),
+])
+def test_construct_from_base_rejects(kw, status):
+    assert _from_base_status(**kw) == status
+
+
+def test_construct_from_base_single_stage_is_a_no_op():
+    """n_stages = 1: the package is the base alone; the call succeeds after
+    validation and enqueues nothing (the fake pointers are never touched and
+    no device is needed)."""
+    assert _from_base_status(S=1) == rrq.RRQ_OK
+    assert _from_base_status(S=1, codes=FAKE_MISALIGNED) == rrq.RRQ_ERR_ALIGN
 
 
 @pytest.mark.parametrize("kw,status", [
