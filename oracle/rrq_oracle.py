@@ -19,6 +19,9 @@ What it computes (paper, Sec. 3 "Recurrent Residual Quantization"):
 * the prefix reconstruction of Eq. 8 (restated as Eq. 18-19 in the
   prefill/decode appendix): the effective weight after t stages is the sum of
   the first t dequantized stages;
+* the stage-sum product of Eq. 20: a linear layer on the prefix-t weight is the
+  sum of the products of the activations with each stage (``linear``,
+  evaluated in float64);
 * the main configuration of Sec. 4.1: 2-bit RTN stages, 4 of them, group size
   128, calibration-free.
 
@@ -322,6 +325,47 @@ def reconstruct(codes, scales, zeros, group_size: int, k_stages: int,
     if out_dtype == "bf16":
         return f32_to_bf16_bits(acc)
     raise ValueError(out_dtype)
+
+
+# ---------------------------------------------------------------------------
+# Stage-sum linear layer (the prefill / decode product of Eq. 20)
+# ---------------------------------------------------------------------------
+
+def stage_values_f64(codes_t: np.ndarray, s_t: np.ndarray, z_t: np.ndarray, rows: int,
+                     cols: int, group_size: int, row_index=None) -> np.ndarray:
+    """Exact values (Q - z) s of one stage as float64 [len(row_index), cols]
+    (Q - z and its product with a binary32 s are exact in float64)."""
+    words_per_row = cols // 16
+    gpr = cols // group_size
+    rows_sel = np.arange(rows) if row_index is None else np.asarray(row_index)
+    w = np.asarray(codes_t, dtype=np.uint32).reshape(rows, words_per_row)[rows_sel]
+    Q = unpack_codes(w.reshape(-1)).reshape(len(rows_sel), cols).astype(np.float64)
+    s = np.asarray(s_t, dtype=np.float32).reshape(rows, gpr)[rows_sel].astype(np.float64)
+    z = np.asarray(z_t, dtype=np.float32).reshape(rows, gpr)[rows_sel].astype(np.float64)
+    return ((Q.reshape(len(rows_sel), gpr, group_size) - z[:, :, None]) * s[:, :, None]
+            ).reshape(len(rows_sel), cols)
+
+
+def linear(codes, scales, zeros, rows: int, cols: int, group_size: int, k_stages: int,
+           x_bits: np.ndarray, row_index=None) -> np.ndarray:
+    """Y = X W~_(k)^T by the stage decomposition of Eq. 20:
+    Y[m, o] = sum_{t < k} sum_i X[m, i] (Q_t[o, i] - z_t) s_t, in exact real
+    arithmetic up to float64 summation (every product is exact in float64).
+
+    ``x_bits``: bfloat16 activations [M, cols] as uint16 bit patterns.
+    Returns float64 [M, rows] (or [M, len(row_index)] for a subset of rows).
+    """
+    codes = np.asarray(codes, dtype=np.uint32)
+    if not 1 <= k_stages <= codes.shape[0]:
+        raise ValueError("k_stages out of range")
+    x = bf16_bits_to_f32(np.asarray(x_bits, dtype=np.uint16)).astype(np.float64)
+    x = x.reshape(-1, cols)
+    y = None
+    for t in range(k_stages):
+        R = stage_values_f64(codes[t], scales[t], zeros[t], rows, cols, group_size, row_index)
+        yt = x @ R.T                               # A Rhat_t of Eq. 20
+        y = yt if y is None else y + yt            # sum over the prefix's stages
+    return y
 
 
 # ---------------------------------------------------------------------------

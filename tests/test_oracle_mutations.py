@@ -47,6 +47,12 @@ MUTATIONS = {
                                          "for k in range(1, n_stages - 1):\n        Q, s, z, rhat = rtn_stage(r, bits)                  # residual stage k"),
     "base_residual_not_updated": ("r = r - rhat                                         # R_k",
                                   "r = r                                                # R_k"),
+    "linear_zero_point_dropped": ("return ((Q.reshape(len(rows_sel), gpr, group_size) - z[:, :, None]) * s[:, :, None]",
+                                  "return ((Q.reshape(len(rows_sel), gpr, group_size) - 0 * z[:, :, None]) * s[:, :, None]"),
+    "linear_scale_rows_transposed": ("s = np.asarray(s_t, dtype=np.float32).reshape(rows, gpr)[rows_sel]",
+                                     "s = np.asarray(s_t, dtype=np.float32).reshape(gpr, rows).T[rows_sel]"),
+    "linear_last_stage_dropped": ("    for t in range(k_stages):\n        R = stage_values_f64",
+                                  "    for t in range(max(1, k_stages - 1)):\n        R = stage_values_f64"),
 }
 
 
@@ -171,6 +177,43 @@ def _battery(o) -> list:
         got = o.construct_from_base(bits, 1, x.size, full[0][0], full[1][0], full[2][0], 128, 4)
         return all(np.array_equal(a, b) for a, b in zip(full, got))
 
+    def golden_linear():
+        cases = json.load(open(os.path.join(HERE, "golden", "from_base_cases.json")))["cases"]
+        st = cases[0]["stages"]
+        codes = np.array([[int(h, 16) for h in x["codes"]] for x in st], dtype=np.uint32)
+        sc = np.stack([_f([x["s"]]) for x in st])
+        ze = np.stack([_f([x["z"]]) for x in st])
+        for case in json.load(open(os.path.join(HERE, "golden", "linear_cases.json")))["cases"]:
+            xv = np.zeros(32, dtype=np.float32)
+            if case["x"] == "ones":
+                xv[:] = 1
+            elif case["x"] == "alternating":
+                xv[:] = np.where(np.arange(32) % 2 == 0, 1.0, -1.0)
+            else:
+                xv[int(case["x"].rsplit("_", 1)[1])] = 1
+            xb = (xv.view(np.uint32) >> 16).astype(np.uint16).reshape(1, 32)
+            for k, want in case["y"].items():
+                if o.linear(codes, sc, ze, 1, 32, 32, int(k), xb)[0, 0] != want:
+                    return False
+        return True
+
+    def linear_one_hot():
+        rng = np.random.default_rng(13)
+        rows, cols, G = 4, 128, 32
+        codes = rng.integers(0, 2 ** 32, (2, rows * cols // 16), dtype=np.uint64).astype(np.uint32)
+        sc = (2.0 ** rng.integers(-8, -2, (2, rows * cols // G))).astype(np.float32)
+        ze = rng.integers(0, 4, (2, rows * cols // G)).astype(np.float32)
+        W = o.reconstruct(codes, sc, ze, G, 2).reshape(rows, cols)
+        for j in (0, 33, 127):
+            xv = np.zeros(cols, dtype=np.float32)
+            xv[j] = 1
+            xb = (xv.view(np.uint32) >> 16).astype(np.uint16).reshape(1, cols)
+            if not np.array_equal(o.linear(codes, sc, ze, rows, cols, G, 2, xb)[0], W[:, j]):
+                return False
+        return True
+
+    check("golden_linear", golden_linear)
+    check("linear_one_hot", linear_one_hot)
     check("golden_construct", golden_construct)
     check("golden_from_base", golden_from_base)
     check("from_base_identities", from_base_identities)
