@@ -12,7 +12,8 @@
  *     residual left by the stages before it; every stage stores its own
  *     codes, scales and zero-points.
  *   - Eq. 8 (restated as Eq. 18-19): the effective weight after t stages is
- *     the sum of the first t dequantized stages.
+ *     the sum of the first t dequantized stages; Eq. 20: a linear layer on
+ *     that weight is the sum of the stages' products.
  *   - Sec. 4.1: the main configuration is four calibration-free 2-bit RTN
  *     stages (2+2+2+2 bits) with group size 128, giving 2/4/6/8-bit prefixes.
  *
@@ -174,6 +175,39 @@ int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols, int32
 int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
                     int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
                     int32_t k_stages, void *W_out, int32_t out_dtype, hipStream_t stream);
+
+/*
+ * rrq_linear - a linear layer on the prefix-k weight of a package, by the
+ * stage decomposition of the prefill / decode product (Eq. 20; the prefix
+ * weight of Eq. 19):
+ *     Y[m][o] = sum_{t < k} sum_i X[m][i] (Q_t[o][i] - z_t) s_t ,
+ * i.e. Y = X W~_(k)^T for the row-major [rows][cols] (out x in) weight, the
+ * nn.Linear convention. The product is formed per group and stage as
+ * s_t (sum_i X Q_t - z_t sum_i X) on the matrix cores.
+ *
+ *   codes, scales, zeros  device, a package (as rrq_reconstruct reads it).
+ *   rows, cols, group_size, n_stages  the package's shape; same rules as
+ *              rrq_construct, and rows, cols < 2^26.
+ *   k_stages   1..n_stages (2 k_stages effective bits).
+ *   X          device, bfloat16 bit patterns [n_tokens][cols], 16-byte
+ *              aligned (read only).
+ *   n_tokens   >= 1; tokens are processed 16 at a time (the package is read
+ *              once per 16 tokens), so decode (1..16 tokens) reads it once.
+ *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
+ *   stream     HIP stream the work is enqueued on.
+ *
+ * Arithmetic: every product X * (1 + Q/4), X * 1 is exact in the matrix
+ * cores; fp32 rounding enters in the accumulations only, in a fixed order
+ * (results are deterministic). With u = 2^-24, A = sum_{t, g} |s_t,g|
+ * (11 + |z_t,g|) sum_{i in g} |X[m][i]| and n = k_stages * ceil(groups per
+ * row / 8), |Y[m][o] - exact| <= 1.05 u A (group_size + 2 n + 16).
+ *
+ * Returns RRQ_OK, or RRQ_ERR_NULL / _ALIGN / _SHAPE / _GROUP / _STAGES with
+ * nothing enqueued, or RRQ_ERR_HIP if the kernel launch failed.
+ */
+int rrq_linear(const uint32_t *codes, const float *scales, const float *zeros, int64_t rows,
+               int64_t cols, int32_t group_size, int32_t n_stages, int32_t k_stages,
+               const uint16_t *X, int64_t n_tokens, float *Y, hipStream_t stream);
 
 /*
  * rrq_package_bytes - sizes the caller allocates for a package (host only,

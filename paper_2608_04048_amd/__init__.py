@@ -3,10 +3,10 @@ reconstruction on AMD Instinct MI355X.
 
 Thin Python binding of librrq.so (include/rrq.h). The functions named like the
 C ABI (``rrq_construct``, ``rrq_construct_from_base``, ``rrq_reconstruct``,
-``rrq_package_bytes``, ``rrq_status_string``) only marshal arguments: tensors become device pointers,
+``rrq_linear``, ``rrq_package_bytes``, ``rrq_status_string``) only marshal arguments: tensors become device pointers,
 the stream defaults to torch's current stream, and a nonzero status raises
-``RRQError``. ``construct``, ``construct_from_base`` and ``reconstruct``
-additionally allocate the output tensors with torch. Every computation runs in the HIP kernels; there is
+``RRQError``. ``construct``, ``construct_from_base``, ``reconstruct`` and
+``linear`` additionally allocate the output tensors with torch. Every computation runs in the HIP kernels; there is
 no fallback, and a missing library raises.
 """
 
@@ -60,6 +60,8 @@ def load_library() -> ctypes.CDLL:
         lib.rrq_construct_from_base.restype = ctypes.c_int
         lib.rrq_reconstruct.argtypes = [P, P, P, I64, I64, I32, I32, I32, P, I32, P]
         lib.rrq_reconstruct.restype = ctypes.c_int
+        lib.rrq_linear.argtypes = [P, P, P, I64, I64, I32, I32, I32, P, I64, P, P]
+        lib.rrq_linear.restype = ctypes.c_int
         lib.rrq_package_bytes.argtypes = [I64, I64, I32, I32, ctypes.POINTER(ctypes.c_size_t),
                                           ctypes.POINTER(ctypes.c_size_t)]
         lib.rrq_package_bytes.restype = ctypes.c_int
@@ -135,6 +137,16 @@ def rrq_reconstruct(codes, scales, zeros, rows: int, cols: int, group_size: int,
         raise RRQError(st, "rrq_reconstruct")
 
 
+def rrq_linear(codes, scales, zeros, rows: int, cols: int, group_size: int, n_stages: int,
+               k_stages: int, X, n_tokens: int, Y, stream=None) -> None:
+    """Enqueue Y = X W~_(k)^T on a package (see include/rrq.h)."""
+    st = load_library().rrq_linear(_ptr(codes), _ptr(scales), _ptr(zeros), rows, cols,
+                                   group_size, n_stages, k_stages, _ptr(X), n_tokens, _ptr(Y),
+                                   _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_linear")
+
+
 # ---------------------------------------------------------------------------
 # Tensor-level helpers (allocation + the calls above)
 # ---------------------------------------------------------------------------
@@ -203,4 +215,17 @@ def reconstruct(codes, scales, zeros, rows: int, cols: int, group_size: int, k_s
         out = torch.empty((rows, cols), dtype=out_dtype, device=codes.device)
     rrq_reconstruct(codes, scales, zeros, rows, cols, group_size, n_stages, k_stages, out, code,
                     stream)
+    return out
+
+
+def linear(X, codes, scales, zeros, rows: int, cols: int, group_size: int, k_stages: int,
+           stream=None, out=None):
+    """Y = X W~_(k)^T (float32 [n_tokens, rows]) for bfloat16 X [n_tokens, cols]."""
+    import torch
+    _check_device_tensor(X, "X", torch.bfloat16)
+    n_tokens = X.numel() // cols
+    if out is None:
+        out = torch.empty((n_tokens, rows), dtype=torch.float32, device=X.device)
+    rrq_linear(codes, scales, zeros, rows, cols, group_size, codes.shape[0], k_stages, X,
+               n_tokens, out, stream)
     return out

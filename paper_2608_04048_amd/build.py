@@ -60,18 +60,21 @@ def build(keep_asm: bool = False) -> str:
     """Compile every source and link librrq.so; returns the library path."""
     cc = hipcc()
     os.makedirs(BUILD_DIR, exist_ok=True)
-    kern_obj = os.path.join(BUILD_DIR, "rrq_kernels.o")
+    kern_objs = []
+    for name in ("rrq_kernels", "rrq_linear"):
+        obj = os.path.join(BUILD_DIR, name + ".o")
+        cmd = [cc, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+               os.path.join(CSRC, name + ".hip"), "-o", obj]
+        if keep_asm:
+            cmd += ["-save-temps=obj"]
+        _run(cmd)
+        kern_objs.append(obj)
     api_obj = os.path.join(BUILD_DIR, "rrq_api.o")
-    kern_cmd = [cc, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
-                os.path.join(CSRC, "rrq_kernels.hip"), "-o", kern_obj]
-    if keep_asm:
-        kern_cmd += ["-save-temps=obj"]
-    _run(kern_cmd)
     _run([cc, "-x", "c++", *HOST_FLAGS, "-D__HIP_PLATFORM_AMD__", f"-I{INCLUDE}", f"-I{CSRC}",
           f"-I{ROCM}/include",
           "-c", os.path.join(CSRC, "rrq_api.cpp"), "-o", api_obj])
     tmp = LIB + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", kern_obj, api_obj, "-o", tmp])
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *kern_objs, api_obj, "-o", tmp])
     os.replace(tmp, LIB)
     build_probe()
     return LIB

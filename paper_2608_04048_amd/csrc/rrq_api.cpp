@@ -126,6 +126,27 @@ extern "C" int rrq_reconstruct(const uint32_t *codes, const float *scales, const
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 
+extern "C" int rrq_linear(const uint32_t *codes, const float *scales, const float *zeros,
+                          int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                          int32_t k_stages, const uint16_t *X, int64_t n_tokens, float *Y,
+                          hipStream_t stream)
+{
+    if (!codes || !scales || !zeros || !X || !Y) return RRQ_ERR_NULL;
+    int64_t n = 0;
+    int st = check_common(rows, cols, group_size, n_stages, &n);
+    if (st != RRQ_OK) return st;
+    if (k_stages < 1 || k_stages > n_stages) return RRQ_ERR_STAGES;
+    if (n_tokens < 1 || rows >= rrq_detail::kLinearMaxDim || cols >= rrq_detail::kLinearMaxDim)
+        return RRQ_ERR_SHAPE;
+    if (!aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4) || !aligned(X, 16) ||
+        !aligned(Y, 4))
+        return RRQ_ERR_ALIGN;
+    if (current_cu_count() <= 0) return RRQ_ERR_HIP;
+    hipError_t e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,
+                                             n_stages, k_stages, X, n_tokens, Y, stream);
+    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+}
+
 extern "C" int rrq_package_bytes(int64_t rows, int64_t cols, int32_t group_size,
                                  int32_t n_stages, size_t *codes_bytes, size_t *scales_bytes)
 {
@@ -142,8 +163,8 @@ extern "C" const char *rrq_status_string(int status)
     switch (status) {
     case RRQ_OK: return "success";
     case RRQ_ERR_NULL: return "a required pointer is NULL";
-    case RRQ_ERR_ALIGN: return "a buffer is not aligned as required (16 bytes for W, codes and W_out; 4 for scales and zeros)";
-    case RRQ_ERR_SHAPE: return "bad shape: rows and cols must be >= 1, cols a multiple of group_size, rows*cols within range";
+    case RRQ_ERR_ALIGN: return "a buffer is not aligned as required (16 bytes for W, codes, W_out and X; 4 for scales, zeros and Y)";
+    case RRQ_ERR_SHAPE: return "bad shape: rows and cols must be >= 1, cols a multiple of group_size, rows*cols within range (and for rrq_linear rows, cols < 2^26, n_tokens >= 1)";
     case RRQ_ERR_GROUP: return "group_size must be 32, 64 or 128";
     case RRQ_ERR_STAGES: return "n_stages must be in 1..4 and k_stages in 1..n_stages";
     case RRQ_ERR_DTYPE: return "out_dtype must be RRQ_F32 or RRQ_BF16";

@@ -21,6 +21,17 @@ hipError_t launch_reconstruct(const uint32_t *codes, const float *scales,
                               int k, void *out, bool out_bf16, int grid,
                               hipStream_t stream);
 
+// Stage-sum linear layer Y = X W~_(k)^T on a package of rows x cols weights.
+hipError_t launch_linear(const uint32_t *codes, const float *scales, const float *zeros,
+                         int64_t rows, int64_t cols, int G, int S, int k, const uint16_t *X,
+                         int64_t n_tokens, float *Y, hipStream_t stream);
+
+// Linear layer: threads per workgroup (8 waves sharing 16 output rows).
+constexpr int kLinearThreads = 512;
+// rows and cols of the linear kernel stay below this bound, so its 32-bit
+// buffer sizes and offsets (at most 16 * rows * 4 bytes) cannot wrap.
+constexpr int64_t kLinearMaxDim = int64_t(1) << 26;
+
 // Workgroups the construct kernel keeps resident per compute unit.
 constexpr int kConstructBlocksPerCU = 8;
 // Reconstruct: threads per workgroup (4 waves), 16-byte output chunks per

@@ -31,8 +31,8 @@ def _declared_enums():
 def test_library_exports_every_declared_function():
     lib = rrq.load_library()
     names = _declared_functions()
-    assert names == ["rrq_construct", "rrq_construct_from_base", "rrq_package_bytes",
-                     "rrq_reconstruct", "rrq_status_string"]
+    assert names == ["rrq_construct", "rrq_construct_from_base", "rrq_linear",
+                     "rrq_package_bytes", "rrq_reconstruct", "rrq_status_string"]
     for name in names:
         assert hasattr(lib, name), name
     out = os.popen(f"nm -D --defined-only {rrq.LIB_PATH}").read()
@@ -204,3 +204,29 @@ def test_probe_library_exports_declared_function():
 def test_probe_rejects(src, nbytes, dst, status):
     from paper_2608_04048_amd import probe
     assert probe.load_library().hbm_probe_stream(src, nbytes, dst, None) == status
+
+
+def _linear_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128, S=4, k=4,
+                   X=FAKE, M=1, Y=FAKE):
+    lib = rrq.load_library()
+    return lib.rrq_linear(codes, scales, zeros, rows, cols, G, S, k, X, M, Y, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(codes=None), rrq.RRQ_ERR_NULL),
+    (dict(X=None), rrq.RRQ_ERR_NULL),
+    (dict(Y=None), rrq.RRQ_ERR_NULL),
+    (dict(G=48), rrq.RRQ_ERR_GROUP),
+    (dict(S=5, k=1), rrq.RRQ_ERR_STAGES),
+    (dict(k=0), rrq.RRQ_ERR_STAGES),
+    (dict(S=2, k=3), rrq.RRQ_ERR_STAGES),
+    (dict(cols=130), rrq.RRQ_ERR_SHAPE),
+    (dict(M=0), rrq.RRQ_ERR_SHAPE),
+    (dict(rows=1 << 26), rrq.RRQ_ERR_SHAPE),
+    (dict(cols=1 << 27), rrq.RRQ_ERR_SHAPE),
+    (dict(X=FAKE + 8), rrq.RRQ_ERR_ALIGN),
+    (dict(codes=FAKE + 4), rrq.RRQ_ERR_ALIGN),
+    (dict(Y=FAKE + 2), rrq.RRQ_ERR_ALIGN),
+])
+def test_linear_rejects(kw, status):
+    assert _linear_status(**kw) == status
