@@ -9,8 +9,9 @@ Default workload: the 36-layer Qwen3-8B-shaped stack (6.95e9 weights,
 13.9 GB bf16; Gaussian with 0.1% x20 outliers).
 
 After the steps: rrq_construct_from_base (the residual stages on a given base
-checkpoint; here the package's own stage 0) is timed on the same workload, and
-a streaming probe with the same read/write mix gives the practical HBM
+checkpoint; here the package's own stage 0) is timed on the same workload,
+rrq_linear decode passes (1 and 16 tokens, prefixes k = 1..4, one call per
+tensor on per-tensor packages) are timed, and a streaming probe with the same read/write mix gives the practical HBM
 ceiling (include/hbm_probe.h).
 
 Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
@@ -117,6 +118,64 @@ def time_from_base(calls, G, S, stream, flush_buf=None, launches=20):
     return sum(ms) / len(ms), min(ms)
 
 
+def linear_bytes(w, k, M):
+    """Algorithmic HBM bytes of one decode pass of rrq_linear over every
+    tensor of w: k code planes + k (s, z) per group, X in, Y out."""
+    G = w.group_size
+    total = 0
+    for t in w.tensors:
+        total += k * t.numel // 4 + 8 * k * (t.numel // G) + 2 * M * t.cols + 4 * M * t.rows
+    return total
+
+
+def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 2, 3, 4),
+                launches=10):
+    """Decode-style passes of rrq_linear over every tensor of w (one call per
+    tensor, each tensor its own package), timed with HIP events around the
+    whole pass. Builds the per-tensor packages first (untimed)."""
+    import torch
+
+    import paper_2608_04048_amd as rrq
+
+    G, S = w.group_size, w.n_stages
+    cflat, sflat, zflat = codes.view(-1), scales.view(-1), zeros.view(-1)
+    pk = []
+    for t in w.tensors:
+        c = cflat[S * t.offset // 16:S * (t.offset + t.numel) // 16].view(S, t.numel // 16)
+        sc = sflat[S * t.offset // G:S * (t.offset + t.numel) // G].view(S, t.numel // G)
+        zz = zflat[S * t.offset // G:S * (t.offset + t.numel) // G].view(S, t.numel // G)
+        rrq.rrq_construct(W_flat[t.offset:t.offset + t.numel], t.rows, t.cols, G, S, c, sc, zz,
+                          stream)
+        pk.append((t, c, sc, zz))
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2608)
+    max_m = max(tokens)
+    xs = {c: torch.randn((max_m, c), generator=g, device="cuda").to(torch.bfloat16)
+          for c in sorted({t.cols for t in w.tensors})}
+    y = torch.empty(max_m * max(t.rows for t in w.tensors), dtype=torch.float32, device="cuda")
+    out = {}
+    for M in tokens:
+        for k in ks:
+            def run():
+                for t, c, sc, zz in pk:
+                    rrq.rrq_linear(c, sc, zz, t.rows, t.cols, G, S, k, xs[t.cols], M, y, stream)
+            run()
+            ms = []
+            for _ in range(launches):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                run()
+                b.record(stream)
+                b.synchronize()
+                ms.append(a.elapsed_time(b))
+            t_ms = sum(ms) / len(ms)
+            nbytes = linear_bytes(w, k, M)
+            out[f"M{M}_k{k}"] = {"ms": round(t_ms, 4), "bytes": nbytes,
+                                 "hbm_gbs": round(nbytes / (t_ms * 1e-3) / 1e9, 1),
+                                 "hbm_frac": round(nbytes / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    return out
+
+
 def stream_probe(src_bytes, flush_buf=None, launches=10):
     """Practical HBM ceiling for construction's read/write mix: a streaming
     kernel reading src_bytes and writing 5/8 of that (include/hbm_probe.h),
@@ -168,6 +227,8 @@ def main():
                          "256 MB MALL (auto: on when the step moves under 4 GB)")
     ap.add_argument("--no-from-base", action="store_true",
                     help="skip timing rrq_construct_from_base (residual stages on a given base)")
+    ap.add_argument("--no-linear", action="store_true",
+                    help="skip timing rrq_linear (decode passes over every tensor)")
     ap.add_argument("--no-stream-probe", action="store_true",
                     help="skip the 2 : 1.25 read/write streaming probe")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -338,6 +399,10 @@ def main():
             "bytes_per_launch": fb_bytes,
             "base": "stage 0 of the package built in the steps",
         }
+    if not args.no_linear:
+        print("bench: timing rrq_linear decode passes", file=sys.stderr, flush=True)
+        result["linear"] = time_linear(w, W.view(-1), codes, scales, zeros, stream)
+        result["linear"]["calls"] = f"one rrq_linear call per tensor ({len(w.tensors)} per pass)"
     if not args.no_stream_probe:
         result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
         result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)

@@ -199,8 +199,8 @@ int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zer
  * Arithmetic: every product X * (1 + Q/4), X * 1 is exact in the matrix
  * cores; fp32 rounding enters in the accumulations only, in a fixed order
  * (results are deterministic). With u = 2^-24, A = sum_{t, g} |s_t,g|
- * (11 + |z_t,g|) sum_{i in g} |X[m][i]| and n = k_stages * ceil(groups per
- * row / 8), |Y[m][o] - exact| <= 1.05 u A (group_size + 2 n + 16).
+ * (11 + |z_t,g|) sum_{i in g} |X[m][i]| and n = k_stages * (ceil(groups
+ * per row / 8) + 1), |Y[m][o] - exact| <= 1.05 u A (group_size + 2 n + 24).
  *
  * Returns RRQ_OK, or RRQ_ERR_NULL / _ALIGN / _SHAPE / _GROUP / _STAGES with
  * nothing enqueued, or RRQ_ERR_HIP if the kernel launch failed.

@@ -20,14 +20,13 @@
 // tests).
 //
 // Work split: a workgroup of 8 waves owns 16 output rows; the groups of a
-// row are split into 8 contiguous ranges, one per wave; the 8 partial
-// results are summed through LDS in wave order (deterministic). Tokens are
-// processed 16 at a time. Lane l of a wave: A row / B column l % 16, input
-// slice j = l / 16 of each 32-input block. With nb = G / 32 blocks per group,
-// block b takes code word b + (j / 2) nb of the row's group (so a lane loads
-// its nb words with one load per stage) and, of that word, the element pairs
-// (p, p + 8) for p = 4 (j % 2) .. 4 (j % 2) + 3; the A operand holds the
-// activations of the same inputs in the same order.
+// row are split into 8 contiguous ranges, one per wave, each wave keeping
+// the loads of two groups in flight; the partial results are summed through
+// LDS in wave order (deterministic). Tokens are processed 16 at a time. The
+// loads are shaped for the vector-memory address path, which bounds this
+// kernel before HBM does: no lane loads a code word another lane of its row
+// loads (G = 128, 64), activations come in 16-byte loads and only for live
+// tokens, scales and zero-points for two groups per load.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -84,17 +83,131 @@ __device__ __forceinline__ u32x4 act_operand(const u32x2 &run1, const u32x2 &run
     return a;
 }
 
-template <int NB>
-__device__ __forceinline__ void load_words(rsrc_t r, uint32_t off, uint32_t (&w)[NB])
+// Lane layout of one group (G inputs of 16 output rows, nb = G / 32 MFMA
+// blocks of 32 inputs). Lane l: row / token r = l % 16, slice j = l / 16.
+//   G = 128: lane j owns code words 2j, 2j + 1 of the row's group (one 8-byte
+//            load per stage) and the activations of their 32 inputs; block b
+//            takes word 2j + b / 2, element pairs of half b % 2.
+//   G = 64:  lane j owns word j; block b takes its half b.
+//   G = 32:  lanes j = 2w, 2w + 1 share word w; block 0 takes half j % 2.
+// Half h of a word holds the element pairs (p, p + 8), p = 4h .. 4h + 3.
+template <int G>
+struct LaneMap {
+    static constexpr int NB = G / 32;
+    static constexpr int WL = G == 128 ? 2 : 1;        // words loaded per lane
+    static constexpr int XD = G == 32 ? 4 : 8 * WL;    // activation dwords per lane
+};
+
+template <int G, int K>
+struct GroupLoads {
+    uint32_t w[K][LaneMap<G>::WL];        // code words, per stage
+    uint32_t x[LaneMap<G>::XD];           // activations (bfloat16 pairs)
+};
+
+// A group at or past g_end (the next wave's, or past the row) is not fetched:
+// its offsets are moved 2^31 bytes up, past every resource's size (all are
+// below 2^28 bytes), so the loads return zeros without touching memory.
+// Token lanes past the tile's last token skip their activation loads.
+template <int G, int K>
+__device__ __forceinline__ void load_group(GroupLoads<G, K> &d, int64_t g, int64_t g_end,
+                                           rsrc_t rx, uint32_t tok_off, bool tok_live,
+                                           const rsrc_t (&rc)[K], uint32_t row_word_off,
+                                           int j)
 {
-    if constexpr (NB == 4) {
-        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
-        w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
-    } else if constexpr (NB == 2) {
-        const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
-        w[0] = v[0]; w[1] = v[1];
+    constexpr int WPG = G / 16;
+    const uint32_t skip = g < g_end ? 0u : 0x80000000u;
+    // first word of this lane within the group, and its first input
+    const int w0 = G == 128 ? 2 * j : G == 64 ? j : (j >> 1);
+    const uint32_t word_off = skip + row_word_off + (uint32_t)(g * WPG + w0) * 4;
+#pragma unroll
+    for (int t = 0; t < K; ++t) {
+        if constexpr (G == 128) {
+            const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rc[t], word_off, 0, 0);
+            d.w[t][0] = v[0];
+            d.w[t][1] = v[1];
+        } else {
+            d.w[t][0] = __builtin_amdgcn_raw_buffer_load_b32(rc[t], word_off, 0, 0);
+        }
+    }
+    const uint32_t in0 = (uint32_t)(g * G) + 16 * w0;
+    const uint32_t xoff = skip + tok_off + in0 * 2;
+#pragma unroll
+    for (int i = 0; i < LaneMap<G>::XD; ++i) d.x[i] = 0u;
+    if (tok_live) {
+        if constexpr (G == 32) {
+            // only this lane's half: inputs 4h .. 4h + 3 and 8 + 4h .. 8 + 4h + 3
+            const uint32_t h = (uint32_t)(j & 1);
+            const u32x2 a = __builtin_amdgcn_raw_buffer_load_b64(rx, xoff + 8 * h, 0, 0);
+            const u32x2 b = __builtin_amdgcn_raw_buffer_load_b64(rx, xoff + 16 + 8 * h, 0, 0);
+            d.x[0] = a[0]; d.x[1] = a[1]; d.x[2] = b[0]; d.x[3] = b[1];
+        } else {
+#pragma unroll
+            for (int q = 0; q < LaneMap<G>::XD / 4; ++q) {
+                const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff + 16 * q, 0, 0);
+                d.x[4 * q] = v[0]; d.x[4 * q + 1] = v[1]; d.x[4 * q + 2] = v[2]; d.x[4 * q + 3] = v[3];
+            }
+        }
+    }
+}
+
+// Scales and zero-points of groups g, g + 1 (one 8-byte load each per stage).
+template <int K>
+__device__ __forceinline__ void load_sz(u32x2 (&s)[K], u32x2 (&z)[K], int64_t g, int64_t g_end,
+                                        const rsrc_t (&rs)[K], const rsrc_t (&rz)[K],
+                                        uint32_t row_group_off)
+{
+    const uint32_t skip = g < g_end ? 0u : 0x80000000u;
+    const uint32_t off = skip + row_group_off + (uint32_t)g * 4;
+#pragma unroll
+    for (int t = 0; t < K; ++t) {
+        s[t] = __builtin_amdgcn_raw_buffer_load_b64(rs[t], off, 0, 0);
+        z[t] = __builtin_amdgcn_raw_buffer_load_b64(rz[t], off, 0, 0);
+    }
+}
+
+// One group's contribution to the lane's 4 outputs: Sx, then per stage P and
+// acc += 4 s P - s (4 + z) Sx.
+template <int G, int K>
+__device__ __forceinline__ void compute_group(const GroupLoads<G, K> &d, const float (&s)[K],
+                                              const float (&z)[K], int j, f32x4 &acc)
+{
+    constexpr int NB = G / 32;
+    const u32x4 ones = {kOnePair, kOnePair, kOnePair, kOnePair};
+    u32x4 a[NB];
+    if constexpr (G == 32) {
+        a[0] = act_operand((u32x2){d.x[0], d.x[1]}, (u32x2){d.x[2], d.x[3]});
     } else {
-        w[0] = __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            // word b / 2 of the lane (G = 128) or its only word (G = 64), half b % 2
+            const int base = (G == 128 ? 8 * (b >> 1) : 0) + 2 * (b & 1);
+            a[b] = act_operand((u32x2){d.x[base], d.x[base + 1]},
+                               (u32x2){d.x[base + 4], d.x[base + 5]});
+        }
+    }
+    f32x4 sx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int b = 0; b < NB; ++b) sx = mfma(a[b], ones, sx);
+#pragma unroll
+    for (int t = 0; t < K; ++t) {
+        f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            uint32_t word;
+            int h;
+            if constexpr (G == 128) { word = d.w[t][b >> 1]; h = b & 1; }
+            else if constexpr (G == 64) { word = d.w[t][0]; h = b; }
+            else { word = d.w[t][0]; h = j & 1; }
+            p = mfma(a[b], code_operand(h ? word >> 8 : word), p);
+        }
+        // s (sum x Q - z Sx) = 4 s P - s (4 + z) Sx
+        const float s4 = 4.0f * s[t];
+        const float scz = s[t] * (4.0f + z[t]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
+            acc[i] = __builtin_fmaf(-scz, sx[i], acc[i]);
+        }
     }
 }
 
@@ -105,24 +218,21 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
     int64_t plane_groups, const uint16_t *__restrict__ X, int64_t n_tokens,
     float *__restrict__ Y)
 {
-    constexpr int NB = G / 32;          // 32-input blocks per group
-    constexpr int WPG = G / 16;         // code words per group and row
     constexpr int NW = kLinearThreads / 64;
     __shared__ f32x4 red[NW][64];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15;            // B column (output row) and A row (token)
-    const int j = lane >> 4;            // input slice within a 32-input block
-    const int half = j & 1;             // element pairs 4 half .. 4 half + 3
-    const int wsel = j >> 1;            // which of the block's two words
+    const int j = lane >> 4;            // input slice
 
     const int64_t o0 = (int64_t)blockIdx.x * 16;
     const uint32_t rows_here = (uint32_t)(rows - o0 < 16 ? rows - o0 : 16);
     const int64_t gpr = cols / G;       // groups per row
     const int64_t wpr = cols / 16;      // code words per row
-    // This wave's contiguous range of groups.
-    const int64_t per_wave = (gpr + NW - 1) / NW;
+    // This wave's contiguous range of groups (an even count, so that scales
+    // and zero-points come in pairs of groups).
+    const int64_t per_wave = ((gpr + NW - 1) / NW + 1) & ~int64_t(1);
     const int64_t g_begin = per_wave * wave < gpr ? per_wave * wave : gpr;
     const int64_t g_end = g_begin + per_wave < gpr ? g_begin + per_wave : gpr;
 
@@ -137,51 +247,32 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
     }
     const uint32_t row_word_off = (uint32_t)(r * wpr) * 4;
     const uint32_t row_group_off = (uint32_t)(r * gpr) * 4;
-    const u32x4 ones = {kOnePair, kOnePair, kOnePair, kOnePair};
 
     for (int64_t m0 = 0; m0 < n_tokens; m0 += 16) {
         const uint32_t m_here = (uint32_t)(n_tokens - m0 < 16 ? n_tokens - m0 : 16);
         const rsrc_t rx = make_rsrc(X + m0 * cols, m_here * (uint32_t)cols * 2);
         const uint32_t tok_off = (uint32_t)(r * cols) * 2;
+        const bool tok_live = (uint32_t)r < m_here;
 
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        for (int64_t g = g_begin; g < g_end; ++g) {
-            // Activations of this lane's inputs of group g, all blocks.
-            u32x4 a[NB];
-#pragma unroll
-            for (int b = 0; b < NB; ++b) {
-                const uint32_t in0 = (uint32_t)(g * G) + 16 * (b + wsel * NB) + 4 * half;
-                const u32x2 run1 = __builtin_amdgcn_raw_buffer_load_b64(rx, tok_off + in0 * 2, 0, 0);
-                const u32x2 run2 = __builtin_amdgcn_raw_buffer_load_b64(rx, tok_off + (in0 + 8) * 2, 0, 0);
-                a[b] = act_operand(run1, run2);
-            }
-            // Package data of group g for every stage.
-            uint32_t w[K][NB];
+        // Groups in pairs; the loads of the next group are issued before the
+        // current one is computed.
+        GroupLoads<G, K> cur, nxt;
+        u32x2 s2[K], z2[K];
+        load_group<G, K>(cur, g_begin, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
+        load_sz<K>(s2, z2, g_begin, g_end, rs, rz, row_group_off);
+        for (int64_t g = g_begin; g < g_end; g += 2) {
             float s[K], z[K];
+            load_group<G, K>(nxt, g + 1, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
 #pragma unroll
-            for (int t = 0; t < K; ++t) {
-                load_words<NB>(rc[t], row_word_off + (uint32_t)(g * WPG + wsel * NB) * 4, w[t]);
-                s[t] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs[t], row_group_off + (uint32_t)g * 4, 0, 0));
-                z[t] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rz[t], row_group_off + (uint32_t)g * 4, 0, 0));
-            }
-
-            f32x4 sx = {0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < K; ++t) { s[t] = __uint_as_float(s2[t][0]); z[t] = __uint_as_float(z2[t][0]); }
+            compute_group<G, K>(cur, s, z, j, acc);
+            if (g + 1 >= g_end) break;
 #pragma unroll
-            for (int b = 0; b < NB; ++b) sx = mfma(a[b], ones, sx);
-#pragma unroll
-            for (int t = 0; t < K; ++t) {
-                f32x4 p = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int b = 0; b < NB; ++b) p = mfma(a[b], code_operand(w[t][b] >> (8 * half)), p);
-                // s (sum x Q - z Sx) = 4 s P - s (4 + z) Sx
-                const float s4 = 4.0f * s[t];
-                const float scz = s[t] * (4.0f + z[t]);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
-                    acc[i] = __builtin_fmaf(-scz, sx[i], acc[i]);
-                }
-            }
+            for (int t = 0; t < K; ++t) { s[t] = __uint_as_float(s2[t][1]); z[t] = __uint_as_float(z2[t][1]); }
+            load_group<G, K>(cur, g + 2, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
+            load_sz<K>(s2, z2, g + 2, g_end, rs, rz, row_group_off);
+            compute_group<G, K>(nxt, s, z, j, acc);
         }
 
         // Sum the waves' partial results in wave order and store: lane l

@@ -38,8 +38,8 @@ def _bound(codes, s, z, rows, cols, G, k, x_bits):
     for t in range(k):
         w = (np.abs(s[t].astype(np.float64)) * (11 + np.abs(z[t].astype(np.float64)))).reshape(rows, cols // G)
         A += T @ w.T
-    n = k * math.ceil((cols // G) / 8)
-    return 1.05 * U * A * (G + 2 * n + 16) + 1e-300
+    n = k * (math.ceil((cols // G) / 8) + 1)
+    return 1.05 * U * A * (G + 2 * n + 24) + 1e-300
 
 
 def _gpu_linear(rrq, codes, s, z, rows, cols, G, k, x_bits):
