@@ -52,6 +52,17 @@ def _load():
         lib.rrq_oracle_construct_from_base.argtypes = [P, ctypes.c_int64, ctypes.c_int32,
                                                        ctypes.c_int32, P, P, P]
         lib.rrq_oracle_construct_from_base.restype = ctypes.c_int
+        lib.rrq_oracle_construct_format.argtypes = [P, ctypes.c_int64, ctypes.c_int32,
+                                                    ctypes.c_int32, ctypes.c_int32,
+                                                    ctypes.c_int32, P, P, P]
+        lib.rrq_oracle_construct_format.restype = ctypes.c_int
+        lib.rrq_oracle_reconstruct_format.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32,
+                                                      ctypes.c_int32, ctypes.c_int32,
+                                                      ctypes.c_int32, ctypes.c_int32,
+                                                      ctypes.c_int32, P]
+        lib.rrq_oracle_reconstruct_format.restype = ctypes.c_int
+        lib.rrq_oracle_f32_to_f16.argtypes = [P, ctypes.c_int64, P]
+        lib.rrq_oracle_f32_to_f16.restype = None
         lib.rrq_oracle_reconstruct.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32,
                                                ctypes.c_int32, ctypes.c_int32,
                                                ctypes.c_int32, P]
@@ -138,3 +149,57 @@ def c_threads() -> int:
 def c_set_threads(n: int) -> None:
     """Run the C oracle's parallel regions on n OpenMP threads."""
     _load().rrq_oracle_set_threads(int(n))
+
+
+ZP_CODES = {"int": 0, "real": 1, "sym": 2}
+SCALE_CODES = {"f32": 0, "f16": 1, "bf16": 2}
+
+
+def c_construct_format(w_bits: np.ndarray, group_size: int, n_stages: int, zero_point: str,
+                       scale_dtype: str):
+    """C oracle construction in a stage format -> (codes, scales as stored,
+    zeros; for symmetric stages the zeros hold the implicit 2)."""
+    lib = _load()
+    w = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
+    n = w.size
+    codes = np.empty((n_stages, n // 16), dtype=np.uint32)
+    scales = np.empty((n_stages, n // group_size),
+                      dtype=np.float32 if scale_dtype == "f32" else np.uint16)
+    zeros = np.empty((n_stages, n // group_size), dtype=np.float32)
+    rc = lib.rrq_oracle_construct_format(_ptr(w), n, group_size, n_stages, ZP_CODES[zero_point],
+                                         SCALE_CODES[scale_dtype], _ptr(codes), _ptr(scales),
+                                         _ptr(zeros))
+    if rc == 2:
+        raise ValueError("RRQ oracle: inputs must be finite")
+    if rc == 3:
+        raise ValueError("RRQ oracle: a group's range or scale overflows its type")
+    if rc != 0:
+        raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
+    return codes, scales, zeros
+
+
+def c_reconstruct_format(codes, scales, zeros, group_size: int, k_stages: int, zero_point: str,
+                         scale_dtype: str, out_dtype: str = "f32"):
+    lib = _load()
+    codes = np.ascontiguousarray(codes, dtype=np.uint32)
+    scales = np.ascontiguousarray(scales)
+    zeros = np.ascontiguousarray(zeros, dtype=np.float32)
+    S = codes.shape[0]
+    n = codes.shape[1] * 16
+    bf16 = out_dtype == "bf16"
+    out = np.empty(n, dtype=np.uint16 if bf16 else np.float32)
+    rc = lib.rrq_oracle_reconstruct_format(_ptr(codes), _ptr(scales), _ptr(zeros), n,
+                                           group_size, S, ZP_CODES[zero_point],
+                                           SCALE_CODES[scale_dtype], k_stages, int(bf16),
+                                           _ptr(out))
+    if rc != 0:
+        raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
+    return out
+
+
+def c_f32_to_f16(x: np.ndarray) -> np.ndarray:
+    """The C oracle's own binary32 -> binary16 rounding (bit patterns)."""
+    x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
+    out = np.empty(x.size, dtype=np.uint16)
+    _load().rrq_oracle_f32_to_f16(_ptr(x), x.size, _ptr(out))
+    return out

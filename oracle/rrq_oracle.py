@@ -108,8 +108,25 @@ def _exact_round_sum(t: np.ndarray, z: np.ndarray) -> np.ndarray:
     return np.rint(t.astype(np.float64) + z.astype(np.float64))
 
 
-def rtn_stage(r: np.ndarray, bits: int):
-    """Quantize a batch of groups once with asymmetric min-max RTN.
+ZERO_POINTS = ("int", "real", "sym")
+SCALE_DTYPES = ("f32", "f16", "bf16")
+
+
+def round_scale(s: np.ndarray, scale_dtype: str) -> np.ndarray:
+    """The binary32 value of a stage scale stored in ``scale_dtype``: itself,
+    or the nearest (ties to even) binary16 / bfloat16 value, widened back."""
+    s = np.asarray(s, dtype=np.float32)
+    if scale_dtype == "f32":
+        return s
+    if scale_dtype == "f16":
+        return s.astype(np.float16).astype(np.float32)
+    if scale_dtype == "bf16":
+        return bf16_bits_to_f32(f32_to_bf16_bits(s))
+    raise ValueError(scale_dtype)
+
+
+def rtn_stage(r: np.ndarray, bits: int, zero_point: str = "int", scale_dtype: str = "f32"):
+    """Quantize a batch of groups once with min-max RTN.
 
     ``r``: float32 array [n_groups, G] (the weights for the base stage, the
     residual for later stages). Returns (Q uint8 [n_groups, G], s float32
@@ -117,8 +134,18 @@ def rtn_stage(r: np.ndarray, bits: int):
 
     Eq. 1 (q = x/s + z with a scale and zero-point shared by the group),
     Eq. 2 (Q = R(q)) and Eq. 3 (dequantized value (Q - z) s).
+
+    ``zero_point``: "int" (the default reading: z = RNE(fl(-lo inv)), Q the
+    single rounding of the exact t + z); "real" (z = fl(-lo inv) kept real,
+    Q = RNE(fl(t + z))); "sym" (symmetric stage: the range is widened to
+    [-amax, amax], amax = max(-lo, hi), and z is fixed at 2^(b-1), not
+    stored; a degenerate group gets the zero code Q = z).
+    ``scale_dtype``: the scale is rounded to its storage type ("f16", "bf16")
+    before it is used, and the rounded value quantizes and dequantizes.
     """
     assert r.dtype == np.float32 and r.ndim == 2
+    if zero_point not in ZERO_POINTS or scale_dtype not in SCALE_DTYPES:
+        raise ValueError("unknown stage format")
     maxq = (1 << bits) - 1
     zero = F32(0.0)
 
@@ -127,26 +154,41 @@ def rtn_stage(r: np.ndarray, bits: int):
     hi = np.maximum(r.max(axis=1), zero)
     lo = np.where(lo == zero, zero, lo)        # canonical +0
     hi = np.where(hi == zero, zero, hi)
+    if zero_point == "sym":
+        amax = np.maximum(zero - lo, hi)       # exact
+        lo, hi = zero - amax, amax
 
     d = hi - lo                                # fl(hi - lo)
     if not np.all(np.isfinite(d)):
         raise ValueError("RRQ oracle: a group's range overflows binary32 (inputs need |x| < 2^127)")
     s = d / F32(maxq)                          # fl(d / maxq), IEEE division
+    s = round_scale(s, scale_dtype)            # the stored scale is the one used
+    if not np.all(np.isfinite(s)):
+        raise ValueError("RRQ oracle: a stage scale overflows its storage type")
     degenerate = s < SMALLEST_NORMAL_F32       # zero or subnormal scale
 
     s_safe = np.where(degenerate, F32(1.0), s)
     inv = F32(1.0) / s_safe                    # fl(1 / s)
-    z = np.rint((zero - lo) * inv)             # RNE(fl((0 - lo) * inv))
-    z = np.where(degenerate, zero, z) + zero   # +0 for a zero zero-point
+    if zero_point == "int":
+        z = np.rint((zero - lo) * inv)         # RNE(fl((0 - lo) * inv))
+    elif zero_point == "real":
+        z = (zero - lo) * inv                  # fl((0 - lo) * inv)
+    else:
+        z = np.full(lo.shape, F32(1 << (bits - 1)))
+    z_deg = F32(1 << (bits - 1)) if zero_point == "sym" else zero
+    z = (np.where(degenerate, z_deg, z) + zero).astype(np.float32)   # +0, not -0
     inv = np.where(degenerate, zero, inv)
     s = np.where(degenerate, zero, s)
 
     t = r * inv[:, None]                       # fl(r * inv)
-    q = _exact_round_sum(t, z[:, None])        # RNE(t + z), one rounding
+    if zero_point == "real":
+        q = np.rint(t + z[:, None])            # RNE(fl(t + z))
+    else:
+        q = _exact_round_sum(t, z[:, None])    # RNE(t + z), one rounding
     Q = np.clip(q, 0, maxq)
-    Q = np.where(degenerate[:, None], 0.0, Q).astype(np.uint8)
+    Q = np.where(degenerate[:, None], z_deg, Q).astype(np.uint8)
 
-    qz = Q.astype(np.float32) - z[:, None]     # exact small integer
+    qz = Q.astype(np.float32) - z[:, None]     # fl(Q - z) (exact for an integer z)
     rhat = qz * s[:, None]                     # fl((Q - z) * s)
     rhat = np.where(degenerate[:, None], zero, rhat)
     return Q, s.astype(np.float32), z.astype(np.float32), rhat.astype(np.float32)
@@ -181,11 +223,14 @@ def _check_shape(n_elems: int, group_size: int):
         raise ValueError("element count must be a positive multiple of the group size and of 16")
 
 
-def construct_f32(x: np.ndarray, group_size: int, n_stages: int, bits: int = 2):
+def construct_f32(x: np.ndarray, group_size: int, n_stages: int, bits: int = 2,
+                  zero_point: str = "int", scale_dtype: str = "f32"):
     """Run the RRQ recursion on binary32 weights x (flat, row-major).
 
     Returns per-stage codes Q [S, n] (uint8), scales [S, n/G], zeros [S, n/G],
     the dequantized stage values rhat [S, n] and the final residual [n].
+    Every stage uses the stage format (zero_point, scale_dtype) of
+    ``rtn_stage``; scales are returned as their binary32 values.
     """
     x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
     _check_shape(x.size, group_size)
@@ -197,7 +242,7 @@ def construct_f32(x: np.ndarray, group_size: int, n_stages: int, bits: int = 2):
     for k in range(n_stages):
         # Stage 0 quantizes the weights (base stage), stage k >= 1 the residual
         # left by stages 0..k-1 (Eq. 4-7; Algorithm 1's loop body).
-        Q, s, z, rhat = rtn_stage(r, bits)
+        Q, s, z, rhat = rtn_stage(r, bits, zero_point, scale_dtype)
         Qs.append(Q.reshape(-1))
         ss.append(s)
         zs.append(z)
@@ -207,19 +252,42 @@ def construct_f32(x: np.ndarray, group_size: int, n_stages: int, bits: int = 2):
             r.reshape(-1))
 
 
+def store_scales(s: np.ndarray, scale_dtype: str) -> np.ndarray:
+    """Scales as stored: float32, or float16 / bfloat16 bit patterns (uint16)."""
+    s = np.asarray(s, dtype=np.float32)
+    if scale_dtype == "f32":
+        return s
+    if scale_dtype == "f16":
+        return s.astype(np.float16).view(np.uint16)
+    return f32_to_bf16_bits(s)
+
+
+def load_scales(stored: np.ndarray, scale_dtype: str) -> np.ndarray:
+    """Binary32 values of stored scales (inverse of ``store_scales``)."""
+    if scale_dtype == "f32":
+        return np.asarray(stored, dtype=np.float32)
+    u = np.asarray(stored, dtype=np.uint16)
+    if scale_dtype == "f16":
+        return u.view(np.float16).astype(np.float32)
+    return bf16_bits_to_f32(u)
+
+
 def construct(w_bits: np.ndarray, rows: int, cols: int, group_size: int,
-              n_stages: int):
-    """The package of the C-ABI call rrq_construct: bfloat16 weights [rows, cols]
-    (as uint16 bit patterns) -> codes [S, n/16] uint32, scales [S, n/G]
-    float32, zeros [S, n/G] float32."""
+              n_stages: int, zero_point: str = "int", scale_dtype: str = "f32"):
+    """The package of the C-ABI call rrq_construct (default format) or
+    rrq_construct_format: bfloat16 weights [rows, cols] (as uint16 bit
+    patterns) -> codes [S, n/16] uint32, scales [S, n/G] (float32, or uint16
+    bit patterns for 16-bit scales), zeros [S, n/G] float32 (for symmetric
+    stages these hold the implicit zero-point 2, which is not stored)."""
     if cols % group_size != 0:
         raise ValueError("cols must be a multiple of the group size")
     w_bits = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
     assert w_bits.size == rows * cols
     x = bf16_bits_to_f32(w_bits)
-    Q, s, z, _, _ = construct_f32(x, group_size, n_stages, bits=2)
+    Q, s, z, _, _ = construct_f32(x, group_size, n_stages, bits=2, zero_point=zero_point,
+                                  scale_dtype=scale_dtype)
     codes = np.stack([pack_codes(Q[k]) for k in range(n_stages)])
-    return codes, s, z
+    return codes, store_scales(s, scale_dtype), z
 
 
 # ---------------------------------------------------------------------------
@@ -297,29 +365,41 @@ def construct_from_base(w_bits: np.ndarray, rows: int, cols: int, base_codes: np
 
 def dequant_stage(codes_k: np.ndarray, s_k: np.ndarray, z_k: np.ndarray,
                   group_size: int) -> np.ndarray:
-    """rhat = fl((Q - z) s) for one stage, from its stored codes/scales/zeros."""
+    """rhat = fl(fl(Q - z) s) for one stage, from its codes and the binary32
+    values of its scale and zero-point (Q - z is exact for an integer z)."""
     Q = unpack_codes(codes_k).reshape(-1, group_size).astype(np.float32)
-    qz = Q - np.asarray(z_k, dtype=np.float32)[:, None]     # exact small integer
+    qz = Q - np.asarray(z_k, dtype=np.float32)[:, None]
     return (qz * np.asarray(s_k, dtype=np.float32)[:, None]).reshape(-1)
 
 
-def reconstruct_f32(codes, scales, zeros, group_size: int, k_stages: int):
+def _stage_zeros(zeros, k, n_groups, zero_point):
+    if zero_point == "sym":
+        return np.full(n_groups, F32(2.0))
+    return np.asarray(zeros[k], dtype=np.float32)
+
+
+def reconstruct_f32(codes, scales, zeros, group_size: int, k_stages: int,
+                    zero_point: str = "int", scale_dtype: str = "f32"):
     """Effective weight after k stages: rhat_0 + rhat_1 + ... + rhat_{k-1},
-    summed left to right in binary32."""
+    summed left to right in binary32. ``scales`` as stored (see
+    ``store_scales``); for symmetric stages ``zeros`` is ignored (z = 2)."""
     codes = np.asarray(codes, dtype=np.uint32)
     if not 1 <= k_stages <= codes.shape[0]:
         raise ValueError("k_stages out of range")
-    acc = dequant_stage(codes[0], scales[0], zeros[0], group_size)
+    ng = codes.shape[1] * 16 // group_size
+    sv = lambda k: load_scales(scales[k], scale_dtype)
+    acc = dequant_stage(codes[0], sv(0), _stage_zeros(zeros, 0, ng, zero_point), group_size)
     for t in range(1, k_stages):
-        acc = acc + dequant_stage(codes[t], scales[t], zeros[t], group_size)
+        acc = acc + dequant_stage(codes[t], sv(t), _stage_zeros(zeros, t, ng, zero_point),
+                                  group_size)
     return acc.astype(np.float32)
 
 
 def reconstruct(codes, scales, zeros, group_size: int, k_stages: int,
-                out_dtype: str = "f32"):
+                out_dtype: str = "f32", zero_point: str = "int", scale_dtype: str = "f32"):
     """Prefix-k reconstruction as float32, or as bfloat16 bit patterns
     (uint16) rounded to nearest-even when out_dtype == "bf16"."""
-    acc = reconstruct_f32(codes, scales, zeros, group_size, k_stages)
+    acc = reconstruct_f32(codes, scales, zeros, group_size, k_stages, zero_point, scale_dtype)
     if out_dtype == "f32":
         return acc
     if out_dtype == "bf16":

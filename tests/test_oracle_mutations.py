@@ -31,8 +31,8 @@ MUTATIONS = {
     "residual_sign": ("r = r - rhat                           # R_k", "r = r + rhat                           # R_k"),
     "pack_msb_first": ("shifts = (2 * np.arange(16, dtype=np.uint32))[None, :]\n    return np.bitwise_or",
                        "shifts = (30 - 2 * np.arange(16, dtype=np.uint32))[None, :]\n    return np.bitwise_or"),
-    "recon_reverse_order": ("    acc = dequant_stage(codes[0], scales[0], zeros[0], group_size)\n    for t in range(1, k_stages):\n        acc = acc + dequant_stage(codes[t], scales[t], zeros[t], group_size)",
-                            "    acc = dequant_stage(codes[k_stages - 1], scales[k_stages - 1], zeros[k_stages - 1], group_size)\n    for t in range(k_stages - 2, -1, -1):\n        acc = acc + dequant_stage(codes[t], scales[t], zeros[t], group_size)"),
+    "recon_reverse_order": ("    acc = dequant_stage(codes[0], sv(0), _stage_zeros(zeros, 0, ng, zero_point), group_size)\n    for t in range(1, k_stages):\n        acc = acc + dequant_stage(codes[t], sv(t), _stage_zeros(zeros, t, ng, zero_point),\n                                  group_size)",
+                            "    last = k_stages - 1\n    acc = dequant_stage(codes[last], sv(last), _stage_zeros(zeros, last, ng, zero_point), group_size)\n    for t in range(k_stages - 2, -1, -1):\n        acc = acc + dequant_stage(codes[t], sv(t), _stage_zeros(zeros, t, ng, zero_point),\n                                  group_size)"),
     "recon_drops_last_stage": ("for t in range(1, k_stages):", "for t in range(1, k_stages - 1):"),
     "bf16_truncates": ("out = trunc + up.astype(np.uint64)", "out = trunc"),
     "degenerate_threshold_ignored": ("degenerate = s < SMALLEST_NORMAL_F32", "degenerate = s < 0"),
@@ -53,6 +53,13 @@ MUTATIONS = {
                                      "s = np.asarray(s_t, dtype=np.float32).reshape(gpr, rows).T[rows_sel]"),
     "linear_last_stage_dropped": ("    for t in range(k_stages):\n        R = stage_values_f64",
                                   "    for t in range(max(1, k_stages - 1)):\n        R = stage_values_f64"),
+    "sym_zero_point_not_fixed": ("        z = np.full(lo.shape, F32(1 << (bits - 1)))",
+                                 "        z = np.rint((zero - lo) * inv)"),
+    "sym_range_not_widened": ("        lo, hi = zero - amax, amax", "        lo, hi = lo, hi"),
+    "real_zero_point_rounded": ("        z = (zero - lo) * inv                  # fl((0 - lo) * inv)",
+                                "        z = np.rint((zero - lo) * inv)"),
+    "scale_not_rounded_to_storage": ("    s = round_scale(s, scale_dtype)            # the stored scale is the one used",
+                                     "    s = s"),
 }
 
 
@@ -212,6 +219,34 @@ def _battery(o) -> list:
                 return False
         return True
 
+    def golden_variants():
+        for case in json.load(open(os.path.join(HERE, "golden", "variant_cases.json")))["cases"]:
+            x = np.full(32, case["pad"], dtype=np.float32)
+            x[:len(case["x"])] = case["x"]
+            bits = (x.view(np.uint32) >> 16).astype(np.uint16)
+            S = 2 if "stage1" in case else 1
+            codes, sc, ze = o.construct(bits, 1, 32, 32, S, case["zero_point"], case["scale_dtype"])
+            for k in range(S):
+                st = case[f"stage{k}"]
+                Q = ((codes[k][:, None] >> (2 * np.arange(16, dtype=np.uint32))) & 3).reshape(-1)
+                want = np.full(32, st["pad_code"])
+                want[:len(st["codes"])] = st["codes"]
+                if not np.array_equal(Q, want):
+                    return False
+                got_s = (f"{int(np.asarray(sc[k]).view(np.uint16)[0]):04X}" if "s16" in st
+                         else f"{int(np.asarray(sc[k]).view(np.uint32)[0]):08X}")
+                if got_s != st.get("s16", st.get("s")) or f"{int(ze[k].view(np.uint32)[0]):08X}" != st["z"]:
+                    return False
+        return True
+
+    def symmetric_zero_point_fixed():
+        rng = np.random.default_rng(21)
+        r = (rng.standard_normal((400, 32)) * 0.01).astype(np.float32)
+        _, s, z, _ = o.rtn_stage(r, 2, "sym")
+        return bool(np.all(z == 2.0))
+
+    check("golden_variants", golden_variants)
+    check("symmetric_zero_point_fixed", symmetric_zero_point_fixed)
     check("golden_linear", golden_linear)
     check("linear_one_hot", linear_one_hot)
     check("golden_construct", golden_construct)
