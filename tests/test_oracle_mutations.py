@@ -225,6 +225,10 @@ def _battery(o) -> list:
             x[:len(case["x"])] = case["x"]
             bits = (x.view(np.uint32) >> 16).astype(np.uint16)
             S = 2 if "stage1" in case else 1
+            _, _, _, rh = o.rtn_stage(o.bf16_bits_to_f32(bits).reshape(1, 32), 2,
+                                      case["zero_point"], case["scale_dtype"])
+            if [f"{int(v):08X}" for v in rh[0, :len(case["rhat0"])].view(np.uint32)] != case["rhat0"]:
+                return False
             codes, sc, ze = o.construct(bits, 1, 32, 32, S, case["zero_point"], case["scale_dtype"])
             for k in range(S):
                 st = case[f"stage{k}"]
