@@ -80,7 +80,8 @@ enum rrq_status {
     RRQ_ERR_GROUP = 4,  /* group_size not in {32, 64, 128} */
     RRQ_ERR_STAGES = 5, /* n_stages not in 1..RRQ_MAX_STAGES, or k_stages not in 1..n_stages */
     RRQ_ERR_DTYPE = 6,  /* out_dtype not one of enum rrq_dtype */
-    RRQ_ERR_HIP = 7     /* the HIP runtime reported an error while launching */
+    RRQ_ERR_HIP = 7,    /* the HIP runtime reported an error while launching */
+    RRQ_ERR_FORMAT = 8  /* zero_point or scale_type not one of the enums below */
 };
 
 /* Output element type of rrq_reconstruct. */
@@ -90,6 +91,47 @@ enum rrq_dtype {
 };
 
 #define RRQ_MAX_STAGES 4
+
+/*
+ * Stage formats (the *_format calls). The paper's main configuration stores
+ * 2-bit codes with per-group scales and zero-points (Eq. 1-3); its symmetric
+ * configuration stores no zero-points and its package-size estimate assumes a
+ * 16-bit scale per group (Sec. 4.1, Eq. 21, Table 14). Every stage of a
+ * package has the same format. The calls without _format use
+ * RRQ_ZP_INTEGER and RRQ_SCALE_F32, the arithmetic stated above.
+ *
+ * Zero-point kind:
+ *   RRQ_ZP_INTEGER    z = RNE(fl(|lo| inv)), stored as float (the default).
+ *   RRQ_ZP_REAL       z = fl(|lo| inv) is kept real and stored; the code is
+ *                     Q = clamp(RNE(fl(fl(r inv) + z)), 0, 3) (the sum is
+ *                     rounded to binary32 first); dequantized values are
+ *                     fl(fl(Q - z) s). The group's min and max land exactly
+ *                     on codes 0 and 3.
+ *   RRQ_ZP_SYMMETRIC  the range is widened to [-amax, amax], amax =
+ *                     max(|lo|, hi), so s = fl(fl(2 amax) / 3), and z = 2
+ *                     for every group (grid {-2s, -s, 0, s}); no zero-points
+ *                     are stored (zeros may be NULL). A degenerate group gets
+ *                     code 2 (value 0).
+ * Scale storage:
+ *   RRQ_SCALE_F32     float per group and stage (the default).
+ *   RRQ_SCALE_F16     IEEE binary16 bit patterns (uint16_t), nearest-even.
+ *   RRQ_SCALE_BF16    bfloat16 bit patterns (uint16_t), nearest-even.
+ *   With a 16-bit type the scale fl(d / 3) is rounded to it first and the
+ *   rounded value is the one that quantizes, dequantizes and is stored (a
+ *   value that overflows the type is outside the precondition). A scale
+ *   buffer then holds n_stages * rows*cols/G uint16_t, 2-byte aligned.
+ */
+enum rrq_zero_point {
+    RRQ_ZP_INTEGER = 0,
+    RRQ_ZP_REAL = 1,
+    RRQ_ZP_SYMMETRIC = 2
+};
+
+enum rrq_scale_type {
+    RRQ_SCALE_F32 = 0,
+    RRQ_SCALE_F16 = 1,
+    RRQ_SCALE_BF16 = 2
+};
 
 /*
  * rrq_construct - build the RRQ package of a bfloat16 weight matrix
@@ -116,6 +158,17 @@ enum rrq_dtype {
 int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
                   int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
                   hipStream_t stream);
+
+/*
+ * rrq_construct_format - rrq_construct in a stage format (see enum
+ * rrq_zero_point, enum rrq_scale_type). scales is float or uint16_t per group
+ * and stage (4- or 2-byte aligned); zeros is written unless zero_point is
+ * RRQ_ZP_SYMMETRIC (then it may be NULL). Returns as rrq_construct, or
+ * RRQ_ERR_FORMAT for an unknown zero_point or scale_type.
+ */
+int rrq_construct_format(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                         int32_t n_stages, int32_t zero_point, int32_t scale_type,
+                         uint32_t *codes, void *scales, float *zeros, hipStream_t stream);
 
 /*
  * rrq_construct_from_base - build the residual stages of an RRQ package on
@@ -156,6 +209,17 @@ int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols, int32
                             hipStream_t stream);
 
 /*
+ * rrq_construct_from_base_format - rrq_construct_from_base in a stage format:
+ * the base plane is read in that format (a 16-bit scale widened exactly; for
+ * RRQ_ZP_SYMMETRIC z_0 = 2 and zeros may be NULL) and the residual stages
+ * are built in it.
+ */
+int rrq_construct_from_base_format(const uint16_t *W, int64_t rows, int64_t cols,
+                                   int32_t group_size, int32_t n_stages, int32_t zero_point,
+                                   int32_t scale_type, uint32_t *codes, void *scales,
+                                   float *zeros, hipStream_t stream);
+
+/*
  * rrq_reconstruct - effective weight of the first k_stages stages of a
  * package (Eq. 8, Eq. 18-19): sum of the dequantized stages (Q - z) s,
  * binary32, in stage order (2 k_stages effective bits).
@@ -175,6 +239,16 @@ int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols, int32
 int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
                     int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
                     int32_t k_stages, void *W_out, int32_t out_dtype, hipStream_t stream);
+
+/*
+ * rrq_reconstruct_format - rrq_reconstruct of a package in a stage format:
+ * rhat = fl(fl(Q - z) s) with s the widened stored scale and z = 2 for
+ * symmetric stages (zeros may then be NULL).
+ */
+int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const float *zeros,
+                           int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                           int32_t zero_point, int32_t scale_type, int32_t k_stages, void *W_out,
+                           int32_t out_dtype, hipStream_t stream);
 
 /*
  * rrq_linear - a linear layer on the prefix-k weight of a package, by the
@@ -208,6 +282,16 @@ int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zer
 int rrq_linear(const uint32_t *codes, const float *scales, const float *zeros, int64_t rows,
                int64_t cols, int32_t group_size, int32_t n_stages, int32_t k_stages,
                const uint16_t *X, int64_t n_tokens, float *Y, hipStream_t stream);
+
+/*
+ * rrq_linear_format - rrq_linear on a package in a stage format (the exact
+ * value uses the widened stored scales and z = 2 for symmetric stages; the
+ * same error bound holds).
+ */
+int rrq_linear_format(const uint32_t *codes, const void *scales, const float *zeros,
+                      int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                      int32_t zero_point, int32_t scale_type, int32_t k_stages,
+                      const uint16_t *X, int64_t n_tokens, float *Y, hipStream_t stream);
 
 /*
  * rrq_package_bytes - sizes the caller allocates for a package (host only,

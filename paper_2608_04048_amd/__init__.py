@@ -27,6 +27,16 @@ RRQ_ERR_GROUP = 4
 RRQ_ERR_STAGES = 5
 RRQ_ERR_DTYPE = 6
 RRQ_ERR_HIP = 7
+RRQ_ERR_FORMAT = 8
+
+RRQ_ZP_INTEGER = 0
+RRQ_ZP_REAL = 1
+RRQ_ZP_SYMMETRIC = 2
+RRQ_SCALE_F32 = 0
+RRQ_SCALE_F16 = 1
+RRQ_SCALE_BF16 = 2
+ZERO_POINTS = {"int": RRQ_ZP_INTEGER, "real": RRQ_ZP_REAL, "sym": RRQ_ZP_SYMMETRIC}
+SCALE_TYPES = {"f32": RRQ_SCALE_F32, "f16": RRQ_SCALE_F16, "bf16": RRQ_SCALE_BF16}
 
 RRQ_F32 = 0
 RRQ_BF16 = 1
@@ -62,6 +72,17 @@ def load_library() -> ctypes.CDLL:
         lib.rrq_reconstruct.restype = ctypes.c_int
         lib.rrq_linear.argtypes = [P, P, P, I64, I64, I32, I32, I32, P, I64, P, P]
         lib.rrq_linear.restype = ctypes.c_int
+        lib.rrq_construct_format.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P, P, P]
+        lib.rrq_construct_format.restype = ctypes.c_int
+        lib.rrq_construct_from_base_format.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P,
+                                                       P, P]
+        lib.rrq_construct_from_base_format.restype = ctypes.c_int
+        lib.rrq_reconstruct_format.argtypes = [P, P, P, I64, I64, I32, I32, I32, I32, I32, P,
+                                               I32, P]
+        lib.rrq_reconstruct_format.restype = ctypes.c_int
+        lib.rrq_linear_format.argtypes = [P, P, P, I64, I64, I32, I32, I32, I32, I32, P, I64,
+                                          P, P]
+        lib.rrq_linear_format.restype = ctypes.c_int
         lib.rrq_package_bytes.argtypes = [I64, I64, I32, I32, ctypes.POINTER(ctypes.c_size_t),
                                           ctypes.POINTER(ctypes.c_size_t)]
         lib.rrq_package_bytes.restype = ctypes.c_int
@@ -147,6 +168,51 @@ def rrq_linear(codes, scales, zeros, rows: int, cols: int, group_size: int, n_st
         raise RRQError(st, "rrq_linear")
 
 
+def rrq_construct_format(W, rows: int, cols: int, group_size: int, n_stages: int,
+                         zero_point: int, scale_type: int, codes, scales, zeros,
+                         stream=None) -> None:
+    """Enqueue package construction in a stage format (see include/rrq.h)."""
+    st = load_library().rrq_construct_format(_ptr(W), rows, cols, group_size, n_stages,
+                                             zero_point, scale_type, _ptr(codes), _ptr(scales),
+                                             _ptr(zeros), _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_construct_format")
+
+
+def rrq_construct_from_base_format(W, rows: int, cols: int, group_size: int, n_stages: int,
+                                   zero_point: int, scale_type: int, codes, scales, zeros,
+                                   stream=None) -> None:
+    """Enqueue the residual stages on a base stage in a stage format."""
+    st = load_library().rrq_construct_from_base_format(
+        _ptr(W), rows, cols, group_size, n_stages, zero_point, scale_type, _ptr(codes),
+        _ptr(scales), _ptr(zeros), _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_construct_from_base_format")
+
+
+def rrq_reconstruct_format(codes, scales, zeros, rows: int, cols: int, group_size: int,
+                           n_stages: int, zero_point: int, scale_type: int, k_stages: int,
+                           W_out, out_dtype: int, stream=None) -> None:
+    """Enqueue prefix-k reconstruction of a package in a stage format."""
+    st = load_library().rrq_reconstruct_format(_ptr(codes), _ptr(scales), _ptr(zeros), rows,
+                                               cols, group_size, n_stages, zero_point,
+                                               scale_type, k_stages, _ptr(W_out), out_dtype,
+                                               _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_reconstruct_format")
+
+
+def rrq_linear_format(codes, scales, zeros, rows: int, cols: int, group_size: int,
+                      n_stages: int, zero_point: int, scale_type: int, k_stages: int, X,
+                      n_tokens: int, Y, stream=None) -> None:
+    """Enqueue Y = X W~_(k)^T on a package in a stage format."""
+    st = load_library().rrq_linear_format(_ptr(codes), _ptr(scales), _ptr(zeros), rows, cols,
+                                          group_size, n_stages, zero_point, scale_type,
+                                          k_stages, _ptr(X), n_tokens, _ptr(Y), _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_linear_format")
+
+
 # ---------------------------------------------------------------------------
 # Tensor-level helpers (allocation + the calls above)
 # ---------------------------------------------------------------------------
@@ -228,4 +294,39 @@ def linear(X, codes, scales, zeros, rows: int, cols: int, group_size: int, k_sta
         out = torch.empty((n_tokens, rows), dtype=torch.float32, device=X.device)
     rrq_linear(codes, scales, zeros, rows, cols, group_size, codes.shape[0], k_stages, X,
                n_tokens, out, stream)
+    return out
+
+
+def construct_format(W, group_size: int = 128, n_stages: int = 4, zero_point: str = "int",
+                     scale_type: str = "f32", stream=None):
+    """Package of a bfloat16 matrix in a stage format ("int" / "real" / "sym"
+    zero-points, "f32" / "f16" / "bf16" scales). Returns (codes int32,
+    scales float32 or int16 holding 16-bit patterns, zeros float32 or None
+    for symmetric stages)."""
+    import torch
+    _check_device_tensor(W, "W", torch.bfloat16)
+    rows, cols = (W.shape[0], W.shape[1]) if W.dim() == 2 else (1, W.numel())
+    n = rows * cols
+    codes = torch.empty((n_stages, n // 16), dtype=torch.int32, device=W.device)
+    scales = torch.empty((n_stages, n // group_size),
+                         dtype=torch.float32 if scale_type == "f32" else torch.int16,
+                         device=W.device)
+    zeros = (None if zero_point == "sym" else
+             torch.empty((n_stages, n // group_size), dtype=torch.float32, device=W.device))
+    rrq_construct_format(W, rows, cols, group_size, n_stages, ZERO_POINTS[zero_point],
+                         SCALE_TYPES[scale_type], codes, scales, zeros, stream)
+    return codes, scales, zeros
+
+
+def reconstruct_format(codes, scales, zeros, rows: int, cols: int, group_size: int,
+                       k_stages: int, zero_point: str = "int", scale_type: str = "f32",
+                       out_dtype=None, stream=None):
+    """Prefix-k effective weight of a package in a stage format."""
+    import torch
+    out_dtype = torch.bfloat16 if out_dtype is None else out_dtype
+    code = {torch.float32: RRQ_F32, torch.bfloat16: RRQ_BF16}[out_dtype]
+    out = torch.empty((rows, cols), dtype=out_dtype, device=codes.device)
+    rrq_reconstruct_format(codes, scales, zeros, rows, cols, group_size, codes.shape[0],
+                           ZERO_POINTS[zero_point], SCALE_TYPES[scale_type], k_stages, out, code,
+                           stream)
     return out

@@ -49,6 +49,22 @@ int check_common(int64_t rows, int64_t cols, int32_t G, int32_t S, int64_t *n)
     return RRQ_OK;
 }
 
+// Stage-format checks: zero-point kind, scale type, and the alignment and
+// presence of the scales and zeros buffers they imply (zeros may be NULL for
+// symmetric stages, which store none).
+int check_format(int32_t zero_point, int32_t scale_type, const void *scales, const void *zeros)
+{
+    if (zero_point != RRQ_ZP_INTEGER && zero_point != RRQ_ZP_REAL &&
+        zero_point != RRQ_ZP_SYMMETRIC)
+        return RRQ_ERR_FORMAT;
+    if (scale_type != RRQ_SCALE_F32 && scale_type != RRQ_SCALE_F16 && scale_type != RRQ_SCALE_BF16)
+        return RRQ_ERR_FORMAT;
+    if (!scales || (zero_point != RRQ_ZP_SYMMETRIC && !zeros)) return RRQ_ERR_NULL;
+    if (!aligned(scales, scale_type == RRQ_SCALE_F32 ? 4 : 2) || (zeros && !aligned(zeros, 4)))
+        return RRQ_ERR_ALIGN;
+    return RRQ_OK;
+}
+
 int grid_for(int64_t work_items, int per_block, int blocks_per_cu, int *grid)
 {
     const int cus = current_cu_count();
@@ -59,60 +75,43 @@ int grid_for(int64_t work_items, int per_block, int blocks_per_cu, int *grid)
     return RRQ_OK;
 }
 
-}  // namespace
-
-extern "C" int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
-                             int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
-                             hipStream_t stream)
+// Construction with or without a base stage, in any stage format.
+int construct_common(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                     int32_t n_stages, int32_t zero_point, int32_t scale_type, uint32_t *codes,
+                     void *scales, float *zeros, bool from_base, hipStream_t stream)
 {
-    if (!W || !codes || !scales || !zeros) return RRQ_ERR_NULL;
+    if (!W || !codes) return RRQ_ERR_NULL;
     int64_t n = 0;
     int st = check_common(rows, cols, group_size, n_stages, &n);
     if (st != RRQ_OK) return st;
-    if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4))
-        return RRQ_ERR_ALIGN;
+    st = check_format(zero_point, scale_type, scales, zeros);
+    if (st != RRQ_OK) return st;
+    if (!aligned(W, 16) || !aligned(codes, 16)) return RRQ_ERR_ALIGN;
+    if (from_base && n_stages == 1) return RRQ_OK;   // the package is the base alone
     const int64_t n_groups = n / group_size;
     int grid = 0;
     st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
-                                                zeros, false, grid, stream);
+                                                zeros, from_base, zero_point, scale_type, grid,
+                                                stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 
-extern "C" int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols,
-                                       int32_t group_size, int32_t n_stages, uint32_t *codes,
-                                       float *scales, float *zeros, hipStream_t stream)
+int reconstruct_common(const uint32_t *codes, const void *scales, const float *zeros,
+                       int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                       int32_t zero_point, int32_t scale_type, int32_t k_stages, void *W_out,
+                       int32_t out_dtype, hipStream_t stream)
 {
-    if (!W || !codes || !scales || !zeros) return RRQ_ERR_NULL;
+    if (!codes || !W_out) return RRQ_ERR_NULL;
     int64_t n = 0;
     int st = check_common(rows, cols, group_size, n_stages, &n);
     if (st != RRQ_OK) return st;
-    if (!aligned(W, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4))
-        return RRQ_ERR_ALIGN;
-    if (n_stages == 1) return RRQ_OK;   // the package is the base alone: nothing to build
-    const int64_t n_groups = n / group_size;
-    int grid = 0;
-    st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
-    if (st != RRQ_OK) return st;
-    hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
-                                                zeros, true, grid, stream);
-    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
-}
-
-extern "C" int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
-                               int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
-                               int32_t k_stages, void *W_out, int32_t out_dtype,
-                               hipStream_t stream)
-{
-    if (!codes || !scales || !zeros || !W_out) return RRQ_ERR_NULL;
-    int64_t n = 0;
-    int st = check_common(rows, cols, group_size, n_stages, &n);
+    st = check_format(zero_point, scale_type, scales, zeros);
     if (st != RRQ_OK) return st;
     if (k_stages < 1 || k_stages > n_stages) return RRQ_ERR_STAGES;
     if (out_dtype != RRQ_F32 && out_dtype != RRQ_BF16) return RRQ_ERR_DTYPE;
-    if (!aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4) || !aligned(W_out, 16))
-        return RRQ_ERR_ALIGN;
+    if (!aligned(codes, 16) || !aligned(W_out, 16)) return RRQ_ERR_ALIGN;
     const int64_t n_groups = n / group_size;
     int grid = 0;
     // one wave tile = 64 lanes x 4 chunks x (8 or 4) elements; 4 waves per workgroup
@@ -122,8 +121,87 @@ extern "C" int rrq_reconstruct(const uint32_t *codes, const float *scales, const
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_reconstruct(codes, scales, zeros, n_groups, group_size,
                                                   n_stages, k_stages, W_out,
-                                                  out_dtype == RRQ_BF16, grid, stream);
+                                                  out_dtype == RRQ_BF16, zero_point, scale_type,
+                                                  grid, stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+}
+
+int linear_common(const uint32_t *codes, const void *scales, const float *zeros, int64_t rows,
+                  int64_t cols, int32_t group_size, int32_t n_stages, int32_t zero_point,
+                  int32_t scale_type, int32_t k_stages, const uint16_t *X, int64_t n_tokens,
+                  float *Y, hipStream_t stream)
+{
+    if (!codes || !X || !Y) return RRQ_ERR_NULL;
+    int64_t n = 0;
+    int st = check_common(rows, cols, group_size, n_stages, &n);
+    if (st != RRQ_OK) return st;
+    st = check_format(zero_point, scale_type, scales, zeros);
+    if (st != RRQ_OK) return st;
+    if (k_stages < 1 || k_stages > n_stages) return RRQ_ERR_STAGES;
+    if (n_tokens < 1 || rows >= rrq_detail::kLinearMaxDim || cols >= rrq_detail::kLinearMaxDim)
+        return RRQ_ERR_SHAPE;
+    if (!aligned(codes, 16) || !aligned(X, 16) || !aligned(Y, 4)) return RRQ_ERR_ALIGN;
+    if (current_cu_count() <= 0) return RRQ_ERR_HIP;
+    hipError_t e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,
+                                             n_stages, k_stages, zero_point, scale_type, X,
+                                             n_tokens, Y, stream);
+    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                             int32_t n_stages, uint32_t *codes, float *scales, float *zeros,
+                             hipStream_t stream)
+{
+    return construct_common(W, rows, cols, group_size, n_stages, RRQ_ZP_INTEGER, RRQ_SCALE_F32,
+                            codes, scales, zeros, false, stream);
+}
+
+extern "C" int rrq_construct_format(const uint16_t *W, int64_t rows, int64_t cols,
+                                    int32_t group_size, int32_t n_stages, int32_t zero_point,
+                                    int32_t scale_type, uint32_t *codes, void *scales,
+                                    float *zeros, hipStream_t stream)
+{
+    return construct_common(W, rows, cols, group_size, n_stages, zero_point, scale_type, codes,
+                            scales, zeros, false, stream);
+}
+
+extern "C" int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols,
+                                       int32_t group_size, int32_t n_stages, uint32_t *codes,
+                                       float *scales, float *zeros, hipStream_t stream)
+{
+    return construct_common(W, rows, cols, group_size, n_stages, RRQ_ZP_INTEGER, RRQ_SCALE_F32,
+                            codes, scales, zeros, true, stream);
+}
+
+extern "C" int rrq_construct_from_base_format(const uint16_t *W, int64_t rows, int64_t cols,
+                                              int32_t group_size, int32_t n_stages,
+                                              int32_t zero_point, int32_t scale_type,
+                                              uint32_t *codes, void *scales, float *zeros,
+                                              hipStream_t stream)
+{
+    return construct_common(W, rows, cols, group_size, n_stages, zero_point, scale_type, codes,
+                            scales, zeros, true, stream);
+}
+
+extern "C" int rrq_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
+                               int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                               int32_t k_stages, void *W_out, int32_t out_dtype,
+                               hipStream_t stream)
+{
+    return reconstruct_common(codes, scales, zeros, rows, cols, group_size, n_stages,
+                              RRQ_ZP_INTEGER, RRQ_SCALE_F32, k_stages, W_out, out_dtype, stream);
+}
+
+extern "C" int rrq_reconstruct_format(const uint32_t *codes, const void *scales,
+                                      const float *zeros, int64_t rows, int64_t cols,
+                                      int32_t group_size, int32_t n_stages, int32_t zero_point,
+                                      int32_t scale_type, int32_t k_stages, void *W_out,
+                                      int32_t out_dtype, hipStream_t stream)
+{
+    return reconstruct_common(codes, scales, zeros, rows, cols, group_size, n_stages, zero_point,
+                              scale_type, k_stages, W_out, out_dtype, stream);
 }
 
 extern "C" int rrq_linear(const uint32_t *codes, const float *scales, const float *zeros,
@@ -131,20 +209,17 @@ extern "C" int rrq_linear(const uint32_t *codes, const float *scales, const floa
                           int32_t k_stages, const uint16_t *X, int64_t n_tokens, float *Y,
                           hipStream_t stream)
 {
-    if (!codes || !scales || !zeros || !X || !Y) return RRQ_ERR_NULL;
-    int64_t n = 0;
-    int st = check_common(rows, cols, group_size, n_stages, &n);
-    if (st != RRQ_OK) return st;
-    if (k_stages < 1 || k_stages > n_stages) return RRQ_ERR_STAGES;
-    if (n_tokens < 1 || rows >= rrq_detail::kLinearMaxDim || cols >= rrq_detail::kLinearMaxDim)
-        return RRQ_ERR_SHAPE;
-    if (!aligned(codes, 16) || !aligned(scales, 4) || !aligned(zeros, 4) || !aligned(X, 16) ||
-        !aligned(Y, 4))
-        return RRQ_ERR_ALIGN;
-    if (current_cu_count() <= 0) return RRQ_ERR_HIP;
-    hipError_t e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,
-                                             n_stages, k_stages, X, n_tokens, Y, stream);
-    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
+    return linear_common(codes, scales, zeros, rows, cols, group_size, n_stages, RRQ_ZP_INTEGER,
+                         RRQ_SCALE_F32, k_stages, X, n_tokens, Y, stream);
+}
+
+extern "C" int rrq_linear_format(const uint32_t *codes, const void *scales, const float *zeros,
+                                 int64_t rows, int64_t cols, int32_t group_size, int32_t n_stages,
+                                 int32_t zero_point, int32_t scale_type, int32_t k_stages,
+                                 const uint16_t *X, int64_t n_tokens, float *Y, hipStream_t stream)
+{
+    return linear_common(codes, scales, zeros, rows, cols, group_size, n_stages, zero_point,
+                         scale_type, k_stages, X, n_tokens, Y, stream);
 }
 
 extern "C" int rrq_package_bytes(int64_t rows, int64_t cols, int32_t group_size,
@@ -163,12 +238,13 @@ extern "C" const char *rrq_status_string(int status)
     switch (status) {
     case RRQ_OK: return "success";
     case RRQ_ERR_NULL: return "a required pointer is NULL";
-    case RRQ_ERR_ALIGN: return "a buffer is not aligned as required (16 bytes for W, codes, W_out and X; 4 for scales, zeros and Y)";
+    case RRQ_ERR_ALIGN: return "a buffer is not aligned as required (16 bytes for W, codes, W_out and X; 4 for binary32 scales, zeros and Y; 2 for 16-bit scales)";
     case RRQ_ERR_SHAPE: return "bad shape: rows and cols must be >= 1, cols a multiple of group_size, rows*cols within range (and for rrq_linear rows, cols < 2^26, n_tokens >= 1)";
     case RRQ_ERR_GROUP: return "group_size must be 32, 64 or 128";
     case RRQ_ERR_STAGES: return "n_stages must be in 1..4 and k_stages in 1..n_stages";
     case RRQ_ERR_DTYPE: return "out_dtype must be RRQ_F32 or RRQ_BF16";
     case RRQ_ERR_HIP: return "the HIP runtime reported an error";
+    case RRQ_ERR_FORMAT: return "zero_point must be an enum rrq_zero_point value and scale_type an enum rrq_scale_type value";
     default: return "unknown status";
     }
 }

@@ -52,6 +52,12 @@ namespace {
 
 constexpr float kMagic = 12582912.0f;          // 1.5 * 2^23
 
+// Stage formats (values of the C ABI's zero-point and scale-type enums).
+constexpr int kZpInteger = 0;    // z = RNE(fl(|lo| inv)), stored
+constexpr int kZpReal = 1;       // z = fl(|lo| inv), stored
+constexpr int kZpSymmetric = 2;  // range [-amax, amax], z = 2, not stored
+constexpr int kScaleF32 = 0, kScaleF16 = 1, kScaleBF16 = 2;
+
 // Codes as bit patterns of tiny binary32 values. For u = 1.5 * 2^23 + Q
 // (Q = RNE(t + z) in 0..4), fma(u, -2^-149, (1.5 * 2^23 + 3) 2^-149) is
 // exactly (3 - Q) 2^-149, and the instruction's clamp-to-[0, 1] modifier turns
@@ -100,11 +106,21 @@ __device__ __forceinline__ float tiny_code(float r, float inv, float m)
     return __builtin_amdgcn_fmed3f(__builtin_fmaf(u, kNegTiny, kTopTiny), 0.0f, 1.0f);
 }
 
+// With a real-valued zero-point, Q = RNE(fl(t + z)): the sum is rounded to
+// binary32 first, then to the nearest integer by the magic addend.
+__device__ __forceinline__ float tiny_code_real(float r, float inv, float z)
+{
+    const float v = r * inv + z;   // fl(fl(r inv) + z)
+    const float u = v + kMagic;
+    return __builtin_amdgcn_fmed3f(__builtin_fmaf(u, kNegTiny, kTopTiny), 0.0f, 1.0f);
+}
+
 // Element loop of one stage for one lane's group: the stage's codes into
 // words[]; with UPDATE also the residual r <- r - (Q - z) s and the range of
-// the new residual (lo, hi, zero included) for the next stage.
-template <int G, bool UPDATE>
-__device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m,
+// the new residual (lo, hi, zero included) for the next stage. ZP selects the
+// zero-point kind (integer and symmetric stages round t + z in one step).
+template <int G, bool UPDATE, int ZP>
+__device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m, float z,
                                                const DequantTable &tab,
                                                uint32_t (&words)[G / 16], float &lo, float &hi)
 {
@@ -118,7 +134,11 @@ __device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             const int j = w * 16 + 2 * p;
-            x[p] = __builtin_fmaf(tiny_code(r[j + 1], inv, m), 4.0f, tiny_code(r[j], inv, m));
+            if constexpr (ZP == kZpReal)
+                x[p] = __builtin_fmaf(tiny_code_real(r[j + 1], inv, z), 4.0f,
+                                      tiny_code_real(r[j], inv, z));
+            else
+                x[p] = __builtin_fmaf(tiny_code(r[j + 1], inv, m), 4.0f, tiny_code(r[j], inv, m));
             if (UPDATE) {
                 const uint32_t off = __float_as_uint(__builtin_fmaf(x[p], 512.0f, tab.lane_off));
                 rhw[p] = *reinterpret_cast<const f32x2 *>(tbase + off);
@@ -290,12 +310,29 @@ __device__ __forceinline__ void gather_half(const uint4 *rd_base, int h, float (
 // is reached by advancing the base pointers k planes.
 struct TileOut {
     uint32_t *codes;
-    float *scales, *zeros;
+    char *scales;        // binary32, or 16-bit patterns (the kernel's SC)
+    float *zeros;
     int64_t words_per_stage, n_groups;
-    uint32_t code_bytes, scale_bytes;
+    uint32_t code_bytes, groups_here;
 };
 
-template <int G>
+// Scale storage SC (kScaleF32, kScaleF16, kScaleBF16): the binary32 value of
+// the stored scale, nearest-even, and its stored bit pattern.
+template <int SC>
+__device__ __forceinline__ float round_scale(float s)
+{
+    if constexpr (SC == kScaleF16) {
+        return (float)(_Float16)s;
+    } else if constexpr (SC == kScaleBF16) {
+        uint32_t u = __float_as_uint(s);
+        u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;   // finite, non-negative s
+        return __uint_as_float(u);
+    } else {
+        return s;
+    }
+}
+
+template <int G, int ZP, int SC>
 __device__ __forceinline__ void store_stage(const TileOut &o, int k, int lane,
                                             const uint32_t (&words)[G / 16], float s, float z)
 {
@@ -303,28 +340,47 @@ __device__ __forceinline__ void store_stage(const TileOut &o, int k, int lane,
     // are dropped.
     store_words<G>(make_rsrc(o.codes + k * o.words_per_stage, o.code_bytes),
                    lane * (G / 16) * 4, words);
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(s),
-                                          make_rsrc(o.scales + k * o.n_groups, o.scale_bytes),
-                                          lane * 4, 0, 0);
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z),
-                                          make_rsrc(o.zeros + k * o.n_groups, o.scale_bytes),
-                                          lane * 4, 0, 0);
+    if constexpr (SC == kScaleF32) {
+        __builtin_amdgcn_raw_buffer_store_b32(
+            __float_as_uint(s), make_rsrc(o.scales + k * o.n_groups * 4, o.groups_here * 4),
+            lane * 4, 0, 0);
+    } else {
+        // s already holds a value of the 16-bit type: the conversion is exact
+        const uint16_t b = SC == kScaleF16 ? __builtin_bit_cast(uint16_t, (_Float16)s)
+                                           : (uint16_t)(__float_as_uint(s) >> 16);
+        __builtin_amdgcn_raw_buffer_store_b16(
+            b, make_rsrc(o.scales + k * o.n_groups * 2, o.groups_here * 2), lane * 2, 0, 0);
+    }
+    if constexpr (ZP != kZpSymmetric)
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z),
+                                              make_rsrc(o.zeros + k * o.n_groups, o.groups_here * 4),
+                                              lane * 4, 0, 0);
 }
 
 // Scale, reciprocal, zero-point and magic addend of one stage from the
-// group's range (lo <= 0 <= hi).
+// group's range (lo <= 0 <= hi), in stage format (ZP, SC): the scale
+// is rounded to its storage type first and the rounded value is used.
+template <int ZP, int SC>
 __device__ __forceinline__ void stage_params(float lo, float hi, float &inv, float &sq, float &z,
                                              float &m)
 {
-    const float d = hi - lo;
-    const float s = d / 3.0f;
-    const bool degenerate = !(s >= 0x1p-126f);
-    inv = degenerate ? 0.0f : 1.0f / s;
-    sq = degenerate ? 0.0f : s;
     // lo <= 0, so |lo| is exactly 0 - lo, +0 included. Written as fabs: the
     // code generator folds 0 - lo into a negate modifier, which turns lo = +0
     // into -0 and would store z = -0.
-    z = rintf(fabsf(lo) * inv);
+    float d;
+    if constexpr (ZP == kZpSymmetric) {
+        const float amax = fmaxf(fabsf(lo), hi);
+        d = amax + amax;                     // range [-amax, amax]
+    } else {
+        d = hi - lo;
+    }
+    const float s = round_scale<SC>(d / 3.0f);
+    const bool degenerate = !(s >= 0x1p-126f);
+    inv = degenerate ? 0.0f : 1.0f / s;
+    sq = degenerate ? 0.0f : s;
+    if constexpr (ZP == kZpInteger) z = rintf(fabsf(lo) * inv);
+    else if constexpr (ZP == kZpReal) z = fabsf(lo) * inv;
+    else z = 2.0f;
     m = kMagic + z;
 }
 
@@ -342,10 +398,11 @@ __device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, fl
 
 // Loads one lane's base stage (plane 0 of the package): its group's code
 // words, scale and zero-point. Lanes past the input read zeros.
-template <int G>
-__device__ __forceinline__ void load_base(const uint32_t *codes, const float *scales,
-                                          const float *zeros, int64_t g0, uint32_t groups_here,
-                                          int lane, uint32_t (&bw)[G / 16], float &s0, float &z0)
+template <int G, int ZP, int SC>
+__device__ __forceinline__ void load_base(const uint32_t *codes, const char *scales,
+                                          const float *zeros, int64_t g0,
+                                          uint32_t groups_here, int lane, uint32_t (&bw)[G / 16],
+                                          float &s0, float &z0)
 {
     const rsrc_t rc = make_rsrc(codes + g0 * (G / 16), groups_here * (G / 16) * 4);
     if constexpr (G / 16 >= 4) {
@@ -358,10 +415,20 @@ __device__ __forceinline__ void load_base(const uint32_t *codes, const float *sc
         const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(rc, lane * (G / 16) * 4, 0, 0);
         bw[0] = x.x; bw[1] = x.y;
     }
-    s0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-        make_rsrc(scales + g0, groups_here * 4), lane * 4, 0, 0));
-    z0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-        make_rsrc(zeros + g0, groups_here * 4), lane * 4, 0, 0));
+    if constexpr (SC == kScaleF32) {
+        s0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+            make_rsrc(scales + g0 * 4, groups_here * 4), lane * 4, 0, 0));
+    } else {
+        const uint16_t b = __builtin_amdgcn_raw_buffer_load_b16(
+            make_rsrc(scales + g0 * 2, groups_here * 2), lane * 2, 0, 0);
+        s0 = SC == kScaleF16 ? (float)__builtin_bit_cast(_Float16, b)
+                             : __uint_as_float((uint32_t)b << 16);
+    }
+    if constexpr (ZP == kZpSymmetric)
+        z0 = 2.0f;
+    else
+        z0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+            make_rsrc(zeros + g0, groups_here * 4), lane * 4, 0, 0));
 }
 
 // Two waves per SIMD: the G = 128 kernel holds 128 residuals plus the
@@ -369,11 +436,12 @@ __device__ __forceinline__ void load_base(const uint32_t *codes, const float *sc
 // FROM_BASE: plane 0 of codes / scales / zeros holds a base checkpoint on
 // entry (read only); the kernel forms R_0 = W - dequant(base) and writes the
 // residual stages 1 .. n_stages - 1 (n_stages >= 2).
-template <int G, bool FROM_BASE>
+// ZP: zero-point kind; SC: scale storage type.
+template <int G, bool FROM_BASE, int ZP, int SC>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void construct_kernel(const uint4 *__restrict__ W,
                                                        int64_t n_groups, int n_stages,
                                                        uint32_t *__restrict__ codes,
-                                                       float *__restrict__ scales,
+                                                       char *__restrict__ scales,
                                                        float *__restrict__ zeros)
 {
     if (FROM_BASE && n_stages < 2) return;
@@ -408,7 +476,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
         const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
         uint32_t bw[WPG];
         float bs = 0.f, bz = 0.f;
-        if constexpr (FROM_BASE) load_base<G>(codes, scales, zeros, g0, groups_here, lane, bw, bs, bz);
+        if constexpr (FROM_BASE)
+            load_base<G, ZP, SC>(codes, scales, zeros, g0, groups_here, lane, bw, bs, bz);
 
         float r[G];
         float bl0 = 0.f, bl1 = 0.f, bh0 = 0.f, bh1 = 0.f;   // range of R_0 (with a base)
@@ -432,8 +501,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
         // Prefetch the next tile while this one is quantized.
         load_tile<CH>(W, n_groups, tile + gridDim.x, lane, v);
 
-        const TileOut out = {codes + g0 * WPG, scales + g0, zeros + g0,
-                             n_groups * WPG, n_groups, groups_here * WPG * 4, groups_here * 4};
+        constexpr int64_t scale_bytes = SC == kScaleF32 ? 4 : 2;
+        const TileOut out = {codes + g0 * WPG, scales + g0 * scale_bytes, zeros + g0,
+                             n_groups * WPG, n_groups, groups_here * WPG * 4, groups_here};
 
         float lo, hi, inv, sq, z, m;
         uint32_t words[WPG];
@@ -444,14 +514,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             group_range<G>(r, lo, hi);
         }
         for (int k = FROM_BASE ? 1 : 0; k + 1 < n_stages; ++k) {
-            stage_params(lo, hi, inv, sq, z, m);
+            stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
             fill_table(tab, lane, sq, z);
-            stage_elements<G, true>(r, inv, m, tab, words, lo, hi);
-            store_stage<G>(out, k, lane, words, sq, z);
+            stage_elements<G, true, ZP>(r, inv, m, z, tab, words, lo, hi);
+            store_stage<G, ZP, SC>(out, k, lane, words, sq, z);
         }
-        stage_params(lo, hi, inv, sq, z, m);
-        stage_elements<G, false>(r, inv, m, tab, words, lo, hi);
-        store_stage<G>(out, n_stages - 1, lane, words, sq, z);
+        stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
+        stage_elements<G, false, ZP>(r, inv, m, z, tab, words, lo, hi);
+        store_stage<G, ZP, SC>(out, n_stages - 1, lane, words, sq, z);
     }
 }
 
@@ -473,13 +543,17 @@ __device__ __forceinline__ uint32_t code_bytes(uint32_t x)
     return out;
 }
 
-template <int K, bool OUT_BF16, int U>
+// SC16: 16-bit scales (binary16 when f16 is set, else bfloat16); SYM:
+// symmetric stages (z = 2, no zeros stored).
+template <int K, bool OUT_BF16, int U, bool SC16, bool SYM>
 __global__ __launch_bounds__(256) void reconstruct_kernel(const uint32_t *__restrict__ codes,
-                                                          const float *__restrict__ scales,
+                                                          const char *__restrict__ scales,
                                                           const float *__restrict__ zeros,
                                                           int64_t n_elems, int64_t n_groups,
-                                                          int g_shift, void *__restrict__ out)
+                                                          int g_shift, void *__restrict__ out,
+                                                          int f16)
 {
+    constexpr int SB = SC16 ? 2 : 4;             // bytes per stored scale
     constexpr int E = OUT_BF16 ? 8 : 4;          // elements per chunk (16 output bytes)
     constexpr int CPW = 16 / E;                  // chunks per code word
     constexpr int TILE = 64 * U;                 // chunks per tile
@@ -505,15 +579,24 @@ __global__ __launch_bounds__(256) void reconstruct_kernel(const uint32_t *__rest
 #pragma unroll
         for (int t = 0; t < K; ++t) {
             const rsrc_t rc = make_rsrc(codes + t * n_words + wfirst, words_here * 4);
-            const rsrc_t rs = make_rsrc(scales + t * n_groups + gfirst, groups_here * 4);
+            const rsrc_t rs = make_rsrc(scales + (t * n_groups + gfirst) * SB, groups_here * SB);
             const rsrc_t rz = make_rsrc(zeros + t * n_groups + gfirst, groups_here * 4);
 #pragma unroll
             for (int j = 0; j < U; ++j) {
                 const uint32_t cl = j * 64 + lane;   // chunk within the tile
                 const uint32_t gl = (uint32_t)((((c0 + cl) * E) >> g_shift) - gfirst);
                 cw[t][j] = __builtin_amdgcn_raw_buffer_load_b32(rc, (cl / CPW) * 4, 0, 0);
-                sc[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, gl * 4, 0, 0));
-                ze[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rz, gl * 4, 0, 0));
+                if constexpr (SC16) {
+                    const uint16_t b = __builtin_amdgcn_raw_buffer_load_b16(rs, gl * 2, 0, 0);
+                    sc[t][j] = f16 ? (float)__builtin_bit_cast(_Float16, b)
+                                   : __uint_as_float((uint32_t)b << 16);
+                } else {
+                    sc[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, gl * 4, 0, 0));
+                }
+                if constexpr (SYM)
+                    ze[t][j] = 2.0f;
+                else
+                    ze[t][j] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rz, gl * 4, 0, 0));
             }
         }
 
@@ -564,56 +647,104 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
 
 }  // namespace
 
-template <bool FROM_BASE>
-hipError_t launch_construct_g(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
-                              float *scales, float *zeros, int grid, hipStream_t stream)
+template <bool FROM_BASE, int ZP, int SC>
+hipError_t launch_construct_s(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
+                              char *scales, float *zeros, int grid, hipStream_t stream)
 {
     switch (G) {
-    case 32: return launch(construct_kernel<32, FROM_BASE>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
-    case 64: return launch(construct_kernel<64, FROM_BASE>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
-    case 128: return launch(construct_kernel<128, FROM_BASE>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 32: return launch(construct_kernel<32, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 64: return launch(construct_kernel<64, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 128: return launch(construct_kernel<128, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <bool FROM_BASE, int ZP>
+hipError_t launch_construct_g(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
+                              char *scales, float *zeros, int scale_type, int grid,
+                              hipStream_t stream)
+{
+    switch (scale_type) {
+    case kScaleF32: return launch_construct_s<FROM_BASE, ZP, kScaleF32>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
+    case kScaleF16: return launch_construct_s<FROM_BASE, ZP, kScaleF16>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
+    case kScaleBF16: return launch_construct_s<FROM_BASE, ZP, kScaleBF16>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+template <bool FROM_BASE>
+hipError_t launch_construct_b(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
+                              char *scales, float *zeros, int zero_point, int scale_type,
+                              int grid, hipStream_t stream)
+{
+    switch (zero_point) {
+    case kZpInteger: return launch_construct_g<FROM_BASE, kZpInteger>(w4, n_groups, G, S, codes, scales, zeros, scale_type, grid, stream);
+    case kZpReal: return launch_construct_g<FROM_BASE, kZpReal>(w4, n_groups, G, S, codes, scales, zeros, scale_type, grid, stream);
+    case kZpSymmetric: return launch_construct_g<FROM_BASE, kZpSymmetric>(w4, n_groups, G, S, codes, scales, zeros, scale_type, grid, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
-                            uint32_t *codes, float *scales, float *zeros, bool from_base,
-                            int grid, hipStream_t stream)
+                            uint32_t *codes, void *scales, float *zeros, bool from_base,
+                            int zero_point, int scale_type, int grid, hipStream_t stream)
 {
     const uint4 *w4 = reinterpret_cast<const uint4 *>(W);
-    return from_base
-               ? launch_construct_g<true>(w4, n_groups, G, S, codes, scales, zeros, grid, stream)
-               : launch_construct_g<false>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
+    char *sc = static_cast<char *>(scales);
+    return from_base ? launch_construct_b<true>(w4, n_groups, G, S, codes, sc, zeros, zero_point,
+                                                scale_type, grid, stream)
+                     : launch_construct_b<false>(w4, n_groups, G, S, codes, sc, zeros, zero_point,
+                                                 scale_type, grid, stream);
 }
 
-template <int K, bool BF16>
-hipError_t launch_reconstruct_k(const uint32_t *codes, const float *scales, const float *zeros,
+template <int K, bool BF16, bool SC16, bool SYM>
+hipError_t launch_reconstruct_k(const uint32_t *codes, const char *scales, const float *zeros,
                                 int64_t n_elems, int64_t n_groups, int g_shift, void *out,
-                                int grid, hipStream_t stream)
+                                int f16, int grid, hipStream_t stream)
 {
-    return launch(reconstruct_kernel<K, BF16, BF16 ? kReconstructChunksBF16 : kReconstructChunksF32>,
+    return launch(reconstruct_kernel<K, BF16, BF16 ? kReconstructChunksBF16 : kReconstructChunksF32,
+                                     SC16, SYM>,
                   grid, kReconstructThreads, stream, codes, scales, zeros, n_elems, n_groups,
-                  g_shift, out);
+                  g_shift, out, f16);
 }
 
-hipError_t launch_reconstruct(const uint32_t *codes, const float *scales, const float *zeros,
-                              int64_t n_groups, int G, int S, int k, void *out, bool out_bf16,
-                              int grid, hipStream_t stream)
+template <bool SC16, bool SYM>
+hipError_t launch_reconstruct_f(const uint32_t *codes, const char *scales, const float *zeros,
+                                int64_t n_elems, int64_t n_groups, int g_shift, int k, void *out,
+                                bool out_bf16, int f16, int grid, hipStream_t stream)
 {
-    (void)S;
-    const int64_t n_elems = n_groups * G;
-    const int g_shift = G == 32 ? 5 : G == 64 ? 6 : 7;
-#define RRQ_RECON_CASE(K)                                                                      \
-    case K:                                                                                    \
-        return out_bf16 ? launch_reconstruct_k<K, true>(codes, scales, zeros, n_elems, n_groups, \
-                                                        g_shift, out, grid, stream)            \
-                        : launch_reconstruct_k<K, false>(codes, scales, zeros, n_elems,        \
-                                                         n_groups, g_shift, out, grid, stream);
+#define RRQ_RECON_CASE(K)                                                                          \
+    case K:                                                                                        \
+        return out_bf16 ? launch_reconstruct_k<K, true, SC16, SYM>(codes, scales, zeros, n_elems,  \
+                                                                   n_groups, g_shift, out, f16,    \
+                                                                   grid, stream)                   \
+                        : launch_reconstruct_k<K, false, SC16, SYM>(codes, scales, zeros, n_elems, \
+                                                                    n_groups, g_shift, out, f16,   \
+                                                                    grid, stream);
     switch (k) {
         RRQ_RECON_CASE(1) RRQ_RECON_CASE(2) RRQ_RECON_CASE(3) RRQ_RECON_CASE(4)
     default: return hipErrorInvalidValue;
     }
 #undef RRQ_RECON_CASE
+}
+
+hipError_t launch_reconstruct(const uint32_t *codes, const void *scales, const float *zeros,
+                              int64_t n_groups, int G, int S, int k, void *out, bool out_bf16,
+                              int zero_point, int scale_type, int grid, hipStream_t stream)
+{
+    (void)S;
+    const int64_t n_elems = n_groups * G;
+    const int g_shift = G == 32 ? 5 : G == 64 ? 6 : 7;
+    const char *sc = static_cast<const char *>(scales);
+    const bool sc16 = scale_type != kScaleF32, sym = zero_point == kZpSymmetric;
+    const int f16 = scale_type == kScaleF16;
+    if (!sc16 && !sym)
+        return launch_reconstruct_f<false, false>(codes, sc, zeros, n_elems, n_groups, g_shift, k, out, out_bf16, f16, grid, stream);
+    if (!sc16 && sym)
+        return launch_reconstruct_f<false, true>(codes, sc, zeros, n_elems, n_groups, g_shift, k, out, out_bf16, f16, grid, stream);
+    if (sc16 && !sym)
+        return launch_reconstruct_f<true, false>(codes, sc, zeros, n_elems, n_groups, g_shift, k, out, out_bf16, f16, grid, stream);
+    return launch_reconstruct_f<true, true>(codes, sc, zeros, n_elems, n_groups, g_shift, k, out, out_bf16, f16, grid, stream);
 }
 
 }  // namespace rrq_detail

@@ -8,23 +8,26 @@
 
 namespace rrq_detail {
 
-// Package construction of n_groups groups of G bfloat16 weights, S stages.
+// Package construction of n_groups groups of G bfloat16 weights, S stages,
+// in stage format (zero_point, scale_type) of rrq.h (scales are binary32 or
+// 16-bit patterns; zeros are not written for symmetric stages).
 // from_base: stage 0 of the package is an input (a base checkpoint) and only
 // stages 1 .. S-1 are written.
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
-                            uint32_t *codes, float *scales, float *zeros, bool from_base,
-                            int grid, hipStream_t stream);
+                            uint32_t *codes, void *scales, float *zeros, bool from_base,
+                            int zero_point, int scale_type, int grid, hipStream_t stream);
 
 // Prefix-k reconstruction of a package with n_groups groups of G, S stages.
-hipError_t launch_reconstruct(const uint32_t *codes, const float *scales,
+hipError_t launch_reconstruct(const uint32_t *codes, const void *scales,
                               const float *zeros, int64_t n_groups, int G, int S,
-                              int k, void *out, bool out_bf16, int grid,
-                              hipStream_t stream);
+                              int k, void *out, bool out_bf16, int zero_point,
+                              int scale_type, int grid, hipStream_t stream);
 
 // Stage-sum linear layer Y = X W~_(k)^T on a package of rows x cols weights.
-hipError_t launch_linear(const uint32_t *codes, const float *scales, const float *zeros,
-                         int64_t rows, int64_t cols, int G, int S, int k, const uint16_t *X,
-                         int64_t n_tokens, float *Y, hipStream_t stream);
+hipError_t launch_linear(const uint32_t *codes, const void *scales, const float *zeros,
+                         int64_t rows, int64_t cols, int G, int S, int k, int zero_point,
+                         int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
+                         hipStream_t stream);
 
 // Linear layer: threads per workgroup (8 waves sharing 16 output rows).
 constexpr int kLinearThreads = 512;

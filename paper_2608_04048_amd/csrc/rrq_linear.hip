@@ -150,18 +150,41 @@ __device__ __forceinline__ void load_group(GroupLoads<G, K> &d, int64_t g, int64
     }
 }
 
-// Scales and zero-points of groups g, g + 1 (one 8-byte load each per stage).
+// Package stage format (values of the C ABI's enums).
+constexpr int kZpSymmetric = 2;
+constexpr int kScaleF32 = 0, kScaleF16 = 1;
+
+// Scales and zero-points of groups g, g + 1, as binary32 (one load each per
+// stage): 16-bit scales are widened, symmetric stages have z = 2. gi is the
+// group's index within the row tile's plane segment.
 template <int K>
 __device__ __forceinline__ void load_sz(u32x2 (&s)[K], u32x2 (&z)[K], int64_t g, int64_t g_end,
                                         const rsrc_t (&rs)[K], const rsrc_t (&rz)[K],
-                                        uint32_t row_group_off)
+                                        uint32_t row_group, int scale_type, bool sym)
 {
     const uint32_t skip = g < g_end ? 0u : 0x80000000u;
-    const uint32_t off = skip + row_group_off + (uint32_t)g * 4;
+    const uint32_t gi = row_group + (uint32_t)g;     // group index within the row tile
 #pragma unroll
     for (int t = 0; t < K; ++t) {
-        s[t] = __builtin_amdgcn_raw_buffer_load_b64(rs[t], off, 0, 0);
-        z[t] = __builtin_amdgcn_raw_buffer_load_b64(rz[t], off, 0, 0);
+        if (scale_type == kScaleF32) {
+            s[t] = __builtin_amdgcn_raw_buffer_load_b64(rs[t], skip + gi * 4, 0, 0);
+        } else {
+            // two 16-bit scales (2-byte aligned: a row may start at an odd group)
+            const uint16_t b0 = __builtin_amdgcn_raw_buffer_load_b16(rs[t], skip + gi * 2, 0, 0);
+            const uint16_t b1 = __builtin_amdgcn_raw_buffer_load_b16(rs[t], skip + gi * 2 + 2, 0, 0);
+            if (scale_type == kScaleF16) {
+                s[t][0] = __float_as_uint((float)__builtin_bit_cast(_Float16, b0));
+                s[t][1] = __float_as_uint((float)__builtin_bit_cast(_Float16, b1));
+            } else {
+                s[t][0] = (uint32_t)b0 << 16;
+                s[t][1] = (uint32_t)b1 << 16;
+            }
+        }
+        if (sym) {
+            z[t][0] = z[t][1] = __float_as_uint(2.0f);
+        } else {
+            z[t] = __builtin_amdgcn_raw_buffer_load_b64(rz[t], skip + gi * 4, 0, 0);
+        }
     }
 }
 
@@ -213,12 +236,14 @@ __device__ __forceinline__ void compute_group(const GroupLoads<G, K> &d, const f
 
 template <int G, int K>
 __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
-    const uint32_t *__restrict__ codes, const float *__restrict__ scales,
+    const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int64_t n_tokens,
-    float *__restrict__ Y)
+    float *__restrict__ Y, int zero_point, int scale_type)
 {
     constexpr int NW = kLinearThreads / 64;
+    const bool sym = zero_point == kZpSymmetric;
+    const uint32_t sbytes = scale_type == kScaleF32 ? 4 : 2;
     __shared__ f32x4 red[NW][64];
 
     const int lane = threadIdx.x & 63;
@@ -242,11 +267,12 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
 #pragma unroll
     for (int t = 0; t < K; ++t) {
         rc[t] = make_rsrc(codes + t * plane_words + o0 * wpr, rows_here * (uint32_t)wpr * 4);
-        rs[t] = make_rsrc(scales + t * plane_groups + o0 * gpr, rows_here * (uint32_t)gpr * 4);
+        rs[t] = make_rsrc(scales + (t * plane_groups + o0 * gpr) * sbytes,
+                          rows_here * (uint32_t)gpr * sbytes);
         rz[t] = make_rsrc(zeros + t * plane_groups + o0 * gpr, rows_here * (uint32_t)gpr * 4);
     }
     const uint32_t row_word_off = (uint32_t)(r * wpr) * 4;
-    const uint32_t row_group_off = (uint32_t)(r * gpr) * 4;
+    const uint32_t row_group = (uint32_t)(r * gpr);
 
     for (int64_t m0 = 0; m0 < n_tokens; m0 += 16) {
         const uint32_t m_here = (uint32_t)(n_tokens - m0 < 16 ? n_tokens - m0 : 16);
@@ -260,7 +286,7 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
         GroupLoads<G, K> cur, nxt;
         u32x2 s2[K], z2[K];
         load_group<G, K>(cur, g_begin, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
-        load_sz<K>(s2, z2, g_begin, g_end, rs, rz, row_group_off);
+        load_sz<K>(s2, z2, g_begin, g_end, rs, rz, row_group, scale_type, sym);
         for (int64_t g = g_begin; g < g_end; g += 2) {
             float s[K], z[K];
             load_group<G, K>(nxt, g + 1, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
@@ -271,7 +297,7 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
 #pragma unroll
             for (int t = 0; t < K; ++t) { s[t] = __uint_as_float(s2[t][1]); z[t] = __uint_as_float(z2[t][1]); }
             load_group<G, K>(cur, g + 2, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
-            load_sz<K>(s2, z2, g + 2, g_end, rs, rz, row_group_off);
+            load_sz<K>(s2, z2, g + 2, g_end, rs, rz, row_group, scale_type, sym);
             compute_group<G, K>(nxt, s, z, j, acc);
         }
 
@@ -308,33 +334,35 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
 }
 
 template <int G>
-hipError_t launch_linear_g(const uint32_t *codes, const float *scales, const float *zeros,
-                           int64_t rows, int64_t cols, int S, int k, const uint16_t *X,
-                           int64_t n_tokens, float *Y, hipStream_t stream)
+hipError_t launch_linear_g(const uint32_t *codes, const char *scales, const float *zeros,
+                           int64_t rows, int64_t cols, int S, int k, int zp, int sdt,
+                           const uint16_t *X, int64_t n_tokens, float *Y, hipStream_t stream)
 {
     const int64_t plane_words = rows * cols / 16;
     const int64_t plane_groups = rows * cols / G;
     const int grid = (int)((rows + 15) / 16);
     (void)S;
     switch (k) {
-    case 1: return launch(linear_kernel<G, 1>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y);
-    case 2: return launch(linear_kernel<G, 2>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y);
-    case 3: return launch(linear_kernel<G, 3>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y);
-    case 4: return launch(linear_kernel<G, 4>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y);
+    case 1: return launch(linear_kernel<G, 1>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 2: return launch(linear_kernel<G, 2>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 3: return launch(linear_kernel<G, 3>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 4: return launch(linear_kernel<G, 4>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
     default: return hipErrorInvalidValue;
     }
 }
 
 }  // namespace
 
-hipError_t launch_linear(const uint32_t *codes, const float *scales, const float *zeros,
-                         int64_t rows, int64_t cols, int G, int S, int k, const uint16_t *X,
-                         int64_t n_tokens, float *Y, hipStream_t stream)
+hipError_t launch_linear(const uint32_t *codes, const void *scales, const float *zeros,
+                         int64_t rows, int64_t cols, int G, int S, int k, int zero_point,
+                         int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
+                         hipStream_t stream)
 {
+    const char *sc = static_cast<const char *>(scales);
     switch (G) {
-    case 32: return launch_linear_g<32>(codes, scales, zeros, rows, cols, S, k, X, n_tokens, Y, stream);
-    case 64: return launch_linear_g<64>(codes, scales, zeros, rows, cols, S, k, X, n_tokens, Y, stream);
-    case 128: return launch_linear_g<128>(codes, scales, zeros, rows, cols, S, k, X, n_tokens, Y, stream);
+    case 32: return launch_linear_g<32>(codes, sc, zeros, rows, cols, S, k, zero_point, scale_type, X, n_tokens, Y, stream);
+    case 64: return launch_linear_g<64>(codes, sc, zeros, rows, cols, S, k, zero_point, scale_type, X, n_tokens, Y, stream);
+    case 128: return launch_linear_g<128>(codes, sc, zeros, rows, cols, S, k, zero_point, scale_type, X, n_tokens, Y, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -31,8 +31,10 @@ def _declared_enums():
 def test_library_exports_every_declared_function():
     lib = rrq.load_library()
     names = _declared_functions()
-    assert names == ["rrq_construct", "rrq_construct_from_base", "rrq_linear",
-                     "rrq_package_bytes", "rrq_reconstruct", "rrq_status_string"]
+    assert names == ["rrq_construct", "rrq_construct_format", "rrq_construct_from_base",
+                     "rrq_construct_from_base_format", "rrq_linear", "rrq_linear_format",
+                     "rrq_package_bytes", "rrq_reconstruct", "rrq_reconstruct_format",
+                     "rrq_status_string"]
     for name in names:
         assert hasattr(lib, name), name
     out = os.popen(f"nm -D --defined-only {rrq.LIB_PATH}").read()
@@ -153,7 +155,7 @@ def test_reconstruct_rejects(kw, status):
 
 
 def test_status_strings():
-    for st in range(8):
+    for st in range(9):
         s = rrq.rrq_status_string(st)
         assert isinstance(s, str) and s
     assert rrq.rrq_status_string(0) == "success"
@@ -230,3 +232,50 @@ def _linear_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128
 ])
 def test_linear_rejects(kw, status):
     assert _linear_status(**kw) == status
+
+
+def _fmt_status(fn, zp=0, sd=0, scales=FAKE, zeros=FAKE, **kw):
+    lib = rrq.load_library()
+    if fn == "construct":
+        return lib.rrq_construct_format(FAKE, 64, 128, 128, 4, zp, sd, FAKE, scales, zeros, None)
+    if fn == "from_base":
+        return lib.rrq_construct_from_base_format(FAKE, 64, 128, 128, 4, zp, sd, FAKE, scales,
+                                                  zeros, None)
+    if fn == "reconstruct":
+        return lib.rrq_reconstruct_format(FAKE, scales, zeros, 64, 128, 128, 4, zp, sd, 4, FAKE,
+                                          rrq.RRQ_BF16, None)
+    return lib.rrq_linear_format(FAKE, scales, zeros, 64, 128, 128, 4, zp, sd, 4, FAKE, 1, FAKE,
+                                 None)
+
+
+@pytest.mark.parametrize("fn", ["construct", "from_base", "reconstruct", "linear"])
+@pytest.mark.parametrize("kw,status", [
+    (dict(zp=3), rrq.RRQ_ERR_FORMAT),
+    (dict(zp=-1), rrq.RRQ_ERR_FORMAT),
+    (dict(sd=3), rrq.RRQ_ERR_FORMAT),
+    (dict(scales=None), rrq.RRQ_ERR_NULL),
+    (dict(zeros=None), rrq.RRQ_ERR_NULL),                      # zeros required unless symmetric
+    (dict(sd=rrq.RRQ_SCALE_F32, scales=FAKE + 2), rrq.RRQ_ERR_ALIGN),
+    (dict(sd=rrq.RRQ_SCALE_F16, scales=FAKE + 1), rrq.RRQ_ERR_ALIGN),
+    (dict(zp=rrq.RRQ_ZP_REAL, zeros=FAKE + 2), rrq.RRQ_ERR_ALIGN),
+])
+def test_format_calls_reject(fn, kw, status):
+    assert _fmt_status(fn, **kw) == status
+
+
+def test_symmetric_allows_null_zeros_and_16bit_scales_at_2_bytes():
+    """These argument checks pass (the S = 1 base call then enqueues nothing,
+    so no device is needed to see it)."""
+    lib = rrq.load_library()
+    for sd in (rrq.RRQ_SCALE_F16, rrq.RRQ_SCALE_BF16):
+        st = lib.rrq_construct_from_base_format(FAKE, 64, 128, 128, 1, rrq.RRQ_ZP_SYMMETRIC, sd,
+                                                FAKE, FAKE + 2, None, None)
+        assert st == rrq.RRQ_OK
+
+
+def test_format_enums_match_header():
+    text = open(HEADER).read()
+    for name in ("RRQ_ZP_INTEGER", "RRQ_ZP_REAL", "RRQ_ZP_SYMMETRIC", "RRQ_SCALE_F32",
+                 "RRQ_SCALE_F16", "RRQ_SCALE_BF16", "RRQ_ERR_FORMAT"):
+        m = re.search(name + r"\s*=\s*(\d+)", text)
+        assert m and int(m.group(1)) == getattr(rrq, name), name
