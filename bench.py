@@ -10,8 +10,10 @@ Default workload: the 36-layer Qwen3-8B-shaped stack (6.95e9 weights,
 
 After the steps: rrq_construct_from_base (the residual stages on a given base
 checkpoint; here the package's own stage 0) is timed on the same workload,
-rrq_linear decode passes (1 and 16 tokens, prefixes k = 1..4, one call per
-tensor on per-tensor packages) are timed, and a streaming probe with the same read/write mix gives the practical HBM
+construction in other stage formats (symmetric with fp16 scales, real
+zero-points, bf16 scales) is timed, rrq_linear decode passes (1 and 16
+tokens, prefixes k = 1..4, one call per tensor on per-tensor packages) are
+timed, and a streaming probe with the same read/write mix gives the practical HBM
 ceiling (include/hbm_probe.h).
 
 Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
@@ -176,6 +178,52 @@ def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 
     return out
 
 
+def format_bytes(n, G, S, zero_point, scale_type):
+    """Algorithmic HBM bytes of one construct launch in a stage format:
+    bf16 in, codes, scales (4 or 2 bytes) and zeros (none if symmetric)."""
+    sb = 4 if scale_type == "f32" else 2
+    zb = 0 if zero_point == "sym" else 4
+    return 2 * n + S * n // 4 + (sb + zb) * S * (n // G)
+
+
+def time_formats(W, n, G, S, stream, formats=(("sym", "f16"), ("real", "f32"), ("int", "bf16")),
+                 launches=10):
+    """Mean time of rrq_construct_format over the flat workload per format."""
+    import torch
+
+    import paper_2608_04048_amd as rrq
+
+    rows, cols = W.shape
+    codes = torch.empty((S, n // 16), dtype=torch.int32, device="cuda")
+    zeros = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+    out = {}
+    for zp, sd in formats:
+        scales = torch.empty((S, n // G), dtype=torch.float32 if sd == "f32" else torch.int16,
+                             device="cuda")
+
+        def run():
+            rrq.rrq_construct_format(W, rows, cols, G, S, rrq.ZERO_POINTS[zp], rrq.SCALE_TYPES[sd],
+                                     codes, scales, None if zp == "sym" else zeros, stream)
+        run()
+        ms = []
+        for _ in range(launches):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            run()
+            b.record(stream)
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        t = sum(ms) / len(ms)
+        nb = format_bytes(n, G, S, zp, sd)
+        out[f"{zp}_{sd}"] = {"ms": round(t, 4), "gbs_bf16_weights": round(2 * n / (t * 1e-3) / 1e9, 1),
+                             "hbm_gbs": round(nb / (t * 1e-3) / 1e9, 1),
+                             "hbm_frac": round(nb / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             "bytes_per_launch": nb}
+        del scales
+    del codes, zeros
+    return out
+
+
 def stream_probe(src_bytes, flush_buf=None, launches=10):
     """Practical HBM ceiling for construction's read/write mix: a streaming
     kernel reading src_bytes and writing 5/8 of that (include/hbm_probe.h),
@@ -227,6 +275,8 @@ def main():
                          "256 MB MALL (auto: on when the step moves under 4 GB)")
     ap.add_argument("--no-from-base", action="store_true",
                     help="skip timing rrq_construct_from_base (residual stages on a given base)")
+    ap.add_argument("--no-formats", action="store_true",
+                    help="skip timing rrq_construct_format in other stage formats")
     ap.add_argument("--no-linear", action="store_true",
                     help="skip timing rrq_linear (decode passes over every tensor)")
     ap.add_argument("--no-stream-probe", action="store_true",
@@ -399,6 +449,9 @@ def main():
             "bytes_per_launch": fb_bytes,
             "base": "stage 0 of the package built in the steps",
         }
+    if not args.no_formats:
+        print("bench: timing construct in other stage formats", file=sys.stderr, flush=True)
+        result["formats"] = time_formats(W, n, G, S, stream)
     if not args.no_linear:
         print("bench: timing rrq_linear decode passes", file=sys.stderr, flush=True)
         result["linear"] = time_linear(w, W.view(-1), codes, scales, zeros, stream)
