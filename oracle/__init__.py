@@ -61,6 +61,8 @@ def _load():
                                                       ctypes.c_int32, ctypes.c_int32,
                                                       ctypes.c_int32, P]
         lib.rrq_oracle_reconstruct_format.restype = ctypes.c_int
+        lib.rrq_oracle_group_pmr.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P]
+        lib.rrq_oracle_group_pmr.restype = ctypes.c_int
         lib.rrq_oracle_f32_to_f16.argtypes = [P, ctypes.c_int64, P]
         lib.rrq_oracle_f32_to_f16.restype = None
         lib.rrq_oracle_reconstruct.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32,
@@ -202,4 +204,14 @@ def c_f32_to_f16(x: np.ndarray) -> np.ndarray:
     x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
     out = np.empty(x.size, dtype=np.uint16)
     _load().rrq_oracle_f32_to_f16(_ptr(x), x.size, _ptr(out))
+    return out
+
+
+def c_group_pmr(w_bits: np.ndarray, group_size: int) -> np.ndarray:
+    """C oracle per-group peak-to-mean ratio of flat bfloat16 bits."""
+    w = np.ascontiguousarray(w_bits, dtype=np.uint16).reshape(-1)
+    out = np.empty(w.size // group_size, dtype=np.float32)
+    rc = _load().rrq_oracle_group_pmr(_ptr(w), w.size, group_size, _ptr(out))
+    if rc != 0:
+        raise ValueError(f"RRQ oracle: bad arguments (status {rc})")
     return out

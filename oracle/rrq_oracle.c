@@ -336,6 +336,32 @@ int rrq_oracle_reconstruct_format(const uint32_t *codes, const void *scales, con
     return ORACLE_OK;
 }
 
+/*
+ * Peak-to-Mean Ratio of every group of n bfloat16 weights (Sec. 3): K / MAE,
+ * K = max |w|, MAE = fl(S / G) with S accumulated as four partial sums over
+ * j = 0, 1, 2, 3 (mod 4), each in increasing j, combined as
+ * fl(fl(p0 + p1) + fl(p2 + p3)); a group of zeros gives 0.
+ */
+int rrq_oracle_group_pmr(const uint16_t *W, int64_t n, int32_t G, float *pmr)
+{
+    if (!W || !pmr || G <= 0 || G % 4 != 0 || n <= 0 || n % G != 0) return ORACLE_ERR_ARGS;
+    const int64_t n_groups = n / G;
+#pragma omp parallel for schedule(static)
+    for (int64_t g = 0; g < n_groups; ++g) {
+        float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        float K = 0.0f;
+        for (int j = 0; j < G; ++j) {
+            const float a = fabsf(bf16_to_f32(W[g * G + j]));
+            p[j % 4] = p[j % 4] + a;
+            if (a > K) K = a;
+        }
+        const float S = (p[0] + p[1]) + (p[2] + p[3]);
+        const float mae = S / (float)G;
+        pmr[g] = S > 0.0f ? K / mae : 0.0f;
+    }
+    return ORACLE_OK;
+}
+
 /* Conversion helpers exported for the pins: binary32 -> binary16 bits. */
 void rrq_oracle_f32_to_f16(const float *x, int64_t n, uint16_t *out)
 {

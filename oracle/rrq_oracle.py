@@ -19,6 +19,7 @@ What it computes (paper, Sec. 3 "Recurrent Residual Quantization"):
 * the prefix reconstruction of Eq. 8 (restated as Eq. 18-19 in the
   prefill/decode appendix): the effective weight after t stages is the sum of
   the first t dequantized stages;
+* the peak-to-mean ratio of Sec. 3 (``group_pmr``), the outlier diagnostic;
 * the stage-sum product of Eq. 20: a linear layer on the prefix-t weight is the
   sum of the products of the activations with each stage (``linear``,
   evaluated in float64);
@@ -405,6 +406,38 @@ def reconstruct(codes, scales, zeros, group_size: int, k_stages: int,
     if out_dtype == "bf16":
         return f32_to_bf16_bits(acc)
     raise ValueError(out_dtype)
+
+
+# ---------------------------------------------------------------------------
+# Outlier diagnostic: the peak-to-mean ratio of each group (Sec. 3)
+# ---------------------------------------------------------------------------
+
+def group_pmr(x: np.ndarray, group_size: int) -> np.ndarray:
+    """Peak-to-Mean Ratio of every group (Sec. 3): K / MAE with K the largest
+    |x| of the group and MAE the mean |x|.
+
+    Fixed binary32 reading: S = sum |x| is accumulated as four partial sums
+    p_i over the elements j = i (mod 4), each in increasing j from +0, then
+    S = fl(fl(p0 + p1) + fl(p2 + p3)); MAE = fl(S / G); PMR = fl(K / MAE).
+    A group of zeros has PMR 0. Returns float32 [n / G].
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32).reshape(-1, group_size)
+    a = np.abs(x)
+    K = a.max(axis=1)
+    p = [np.zeros(x.shape[0], dtype=np.float32) for _ in range(4)]
+    for j in range(group_size):                       # each partial sum in index order
+        p[j % 4] = p[j % 4] + a[:, j]
+    S = (p[0] + p[1]) + (p[2] + p[3])
+    mae = S / np.float32(group_size)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        pmr = K / mae
+    return np.where(S > 0, pmr, np.float32(0.0)).astype(np.float32)
+
+
+def tensor_pmr_stats(pmr_groups: np.ndarray):
+    """The paper's tensor-level indicators from per-group PMR values of one
+    tensor: its largest group PMR (the tensor-wise maximum)."""
+    return float(np.max(pmr_groups))
 
 
 # ---------------------------------------------------------------------------

@@ -60,6 +60,9 @@ MUTATIONS = {
                                 "        z = np.rint((zero - lo) * inv)"),
     "scale_not_rounded_to_storage": ("    s = round_scale(s, scale_dtype)            # the stored scale is the one used",
                                      "    s = s"),
+    "pmr_single_running_sum": ("        p[j % 4] = p[j % 4] + a[:, j]", "        p[0] = p[0] + a[:, j]"),
+    "pmr_sum_not_averaged": ("    mae = S / np.float32(group_size)", "    mae = S"),
+    "pmr_peak_without_abs": ("    K = a.max(axis=1)", "    K = x.max(axis=1)"),
 }
 
 
@@ -249,6 +252,16 @@ def _battery(o) -> list:
         _, s, z, _ = o.rtn_stage(r, 2, "sym")
         return bool(np.all(z == 2.0))
 
+    def golden_pmr():
+        for case in json.load(open(os.path.join(HERE, "golden", "pmr_cases.json")))["cases"]:
+            x = np.full(32, case["rest"], dtype=np.float32)
+            for i, v in case["entries"]:
+                x[i] = v
+            if f"{int(o.group_pmr(x, 32).view(np.uint32)[0]):08X}" != case["pmr"]:
+                return False
+        return True
+
+    check("golden_pmr", golden_pmr)
     check("golden_variants", golden_variants)
     check("symmetric_zero_point_fixed", symmetric_zero_point_fixed)
     check("golden_linear", golden_linear)
