@@ -171,6 +171,33 @@ int rrq_construct_format(const uint16_t *W, int64_t rows, int64_t cols, int32_t 
                          uint32_t *codes, void *scales, float *zeros, hipStream_t stream);
 
 /*
+ * rrq_construct_stats - rrq_construct_format plus the paper's outlier
+ * diagnostic (Sec. 3) as a side output of the same pass: the Peak-to-Mean
+ * Ratio of every group of W, its largest |w| over its mean |w|.
+ *
+ *   pmr    device, float [rows*cols/G], 4-byte aligned (written); required.
+ *   other arguments as rrq_construct_format.
+ *
+ * Arithmetic (fixed; the paper states the ratio in real terms): K = max |w|;
+ * S = fl(fl(p0 + p1) + fl(p2 + p3)) with p_i the binary32 sum, in index
+ * order, of |w_j| over the group's elements j = i (mod 4); MAE = fl(S / G);
+ * PMR = fl(K / MAE); a group of zeros gives 0. The tensor-level indicators of
+ * the paper are the largest PMR over a tensor's groups and the mean / maximum
+ * of that over tensors.
+ */
+int rrq_construct_stats(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                        int32_t n_stages, int32_t zero_point, int32_t scale_type, uint32_t *codes,
+                        void *scales, float *zeros, float *pmr, hipStream_t stream);
+
+/*
+ * rrq_group_pmr - the per-group Peak-to-Mean Ratio of W only (as in
+ * rrq_construct_stats, without building a package): W as rrq_construct, pmr
+ * device float [rows*cols/G] (written).
+ */
+int rrq_group_pmr(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size, float *pmr,
+                  hipStream_t stream);
+
+/*
  * rrq_construct_from_base - build the residual stages of an RRQ package on
  * an existing base checkpoint (Algorithm 1's first branch: the base stage's
  * codes, scales and zero-points are loaded, not computed; Eq. 4-7; the paper

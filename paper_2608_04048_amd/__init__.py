@@ -3,7 +3,9 @@ reconstruction on AMD Instinct MI355X.
 
 Thin Python binding of librrq.so (include/rrq.h). The functions named like the
 C ABI (``rrq_construct``, ``rrq_construct_from_base``, ``rrq_reconstruct``,
-``rrq_linear``, ``rrq_package_bytes``, ``rrq_status_string``) only marshal arguments: tensors become device pointers,
+``rrq_linear``, their ``*_format`` twins, ``rrq_construct_stats``,
+``rrq_group_pmr``, ``rrq_package_bytes``, ``rrq_status_string``) only marshal
+arguments: tensors become device pointers,
 the stream defaults to torch's current stream, and a nonzero status raises
 ``RRQError``. ``construct``, ``construct_from_base``, ``reconstruct`` and
 ``linear`` additionally allocate the output tensors with torch. Every computation runs in the HIP kernels; there is
@@ -72,6 +74,10 @@ def load_library() -> ctypes.CDLL:
         lib.rrq_reconstruct.restype = ctypes.c_int
         lib.rrq_linear.argtypes = [P, P, P, I64, I64, I32, I32, I32, P, I64, P, P]
         lib.rrq_linear.restype = ctypes.c_int
+        lib.rrq_construct_stats.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P, P, P, P]
+        lib.rrq_construct_stats.restype = ctypes.c_int
+        lib.rrq_group_pmr.argtypes = [P, I64, I64, I32, P, P]
+        lib.rrq_group_pmr.restype = ctypes.c_int
         lib.rrq_construct_format.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P, P, P]
         lib.rrq_construct_format.restype = ctypes.c_int
         lib.rrq_construct_from_base_format.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P,
@@ -177,6 +183,24 @@ def rrq_construct_format(W, rows: int, cols: int, group_size: int, n_stages: int
                                              _ptr(zeros), _stream(stream))
     if st != RRQ_OK:
         raise RRQError(st, "rrq_construct_format")
+
+
+def rrq_construct_stats(W, rows: int, cols: int, group_size: int, n_stages: int,
+                        zero_point: int, scale_type: int, codes, scales, zeros, pmr,
+                        stream=None) -> None:
+    """Enqueue construction plus the per-group peak-to-mean ratios of W."""
+    st = load_library().rrq_construct_stats(_ptr(W), rows, cols, group_size, n_stages,
+                                            zero_point, scale_type, _ptr(codes), _ptr(scales),
+                                            _ptr(zeros), _ptr(pmr), _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_construct_stats")
+
+
+def rrq_group_pmr(W, rows: int, cols: int, group_size: int, pmr, stream=None) -> None:
+    """Enqueue the per-group peak-to-mean ratios of W."""
+    st = load_library().rrq_group_pmr(_ptr(W), rows, cols, group_size, _ptr(pmr), _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_group_pmr")
 
 
 def rrq_construct_from_base_format(W, rows: int, cols: int, group_size: int, n_stages: int,
@@ -329,4 +353,14 @@ def reconstruct_format(codes, scales, zeros, rows: int, cols: int, group_size: i
     rrq_reconstruct_format(codes, scales, zeros, rows, cols, group_size, codes.shape[0],
                            ZERO_POINTS[zero_point], SCALE_TYPES[scale_type], k_stages, out, code,
                            stream)
+    return out
+
+
+def group_pmr(W, group_size: int = 128, stream=None):
+    """Per-group peak-to-mean ratios (float32 [N/G]) of a bfloat16 tensor."""
+    import torch
+    _check_device_tensor(W, "W", torch.bfloat16)
+    rows, cols = (W.shape[0], W.shape[1]) if W.dim() == 2 else (1, W.numel())
+    out = torch.empty(rows * cols // group_size, dtype=torch.float32, device=W.device)
+    rrq_group_pmr(W, rows, cols, group_size, out, stream)
     return out

@@ -78,7 +78,8 @@ int grid_for(int64_t work_items, int per_block, int blocks_per_cu, int *grid)
 // Construction with or without a base stage, in any stage format.
 int construct_common(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
                      int32_t n_stages, int32_t zero_point, int32_t scale_type, uint32_t *codes,
-                     void *scales, float *zeros, bool from_base, hipStream_t stream)
+                     void *scales, float *zeros, bool from_base, hipStream_t stream,
+                     float *pmr = nullptr)
 {
     if (!W || !codes) return RRQ_ERR_NULL;
     int64_t n = 0;
@@ -86,15 +87,15 @@ int construct_common(const uint16_t *W, int64_t rows, int64_t cols, int32_t grou
     if (st != RRQ_OK) return st;
     st = check_format(zero_point, scale_type, scales, zeros);
     if (st != RRQ_OK) return st;
-    if (!aligned(W, 16) || !aligned(codes, 16)) return RRQ_ERR_ALIGN;
+    if (!aligned(W, 16) || !aligned(codes, 16) || (pmr && !aligned(pmr, 4))) return RRQ_ERR_ALIGN;
     if (from_base && n_stages == 1) return RRQ_OK;   // the package is the base alone
     const int64_t n_groups = n / group_size;
     int grid = 0;
     st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
-                                                zeros, from_base, zero_point, scale_type, grid,
-                                                stream);
+                                                zeros, pmr, from_base, zero_point, scale_type,
+                                                grid, stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 
@@ -165,6 +166,32 @@ extern "C" int rrq_construct_format(const uint16_t *W, int64_t rows, int64_t col
 {
     return construct_common(W, rows, cols, group_size, n_stages, zero_point, scale_type, codes,
                             scales, zeros, false, stream);
+}
+
+extern "C" int rrq_construct_stats(const uint16_t *W, int64_t rows, int64_t cols,
+                                   int32_t group_size, int32_t n_stages, int32_t zero_point,
+                                   int32_t scale_type, uint32_t *codes, void *scales,
+                                   float *zeros, float *pmr, hipStream_t stream)
+{
+    if (!pmr) return RRQ_ERR_NULL;
+    return construct_common(W, rows, cols, group_size, n_stages, zero_point, scale_type, codes,
+                            scales, zeros, false, stream, pmr);
+}
+
+extern "C" int rrq_group_pmr(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_size,
+                             float *pmr, hipStream_t stream)
+{
+    if (!W || !pmr) return RRQ_ERR_NULL;
+    int64_t n = 0;
+    int st = check_common(rows, cols, group_size, 1, &n);
+    if (st != RRQ_OK) return st;
+    if (!aligned(W, 16) || !aligned(pmr, 4)) return RRQ_ERR_ALIGN;
+    const int64_t n_groups = n / group_size;
+    int grid = 0;
+    st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
+    if (st != RRQ_OK) return st;
+    hipError_t e = rrq_detail::launch_group_pmr(W, n_groups, group_size, pmr, grid, stream);
+    return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 
 extern "C" int rrq_construct_from_base(const uint16_t *W, int64_t rows, int64_t cols,

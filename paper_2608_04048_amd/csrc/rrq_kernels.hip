@@ -236,6 +236,37 @@ __device__ __forceinline__ void subtract_base_half(float (&r)[G], const uint32_t
     }
 }
 
+// Sum of |x| over the lane's group in the order that defines the peak-to-mean
+// ratio: four partial sums over j = 0, 1, 2, 3 (mod 4), each in increasing j,
+// combined as (p0 + p1) + (p2 + p3).
+template <int G>
+__device__ __forceinline__ float group_abs_sum(const float (&r)[G])
+{
+    float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
+#pragma unroll
+    for (int j = 0; j < G; j += 4) {
+        p0 = p0 + fabsf(r[j]);
+        p1 = p1 + fabsf(r[j + 1]);
+        p2 = p2 + fabsf(r[j + 2]);
+        p3 = p3 + fabsf(r[j + 3]);
+    }
+    return (p0 + p1) + (p2 + p3);
+}
+
+// Peak-to-mean ratio K / fl(S / G) of a group (0 for a group of zeros) from
+// its zero-included range (K = max(|lo|, hi)) and its |x| sum S; stored at
+// the lane's group.
+template <int G>
+__device__ __forceinline__ void store_pmr(float *pmr, int64_t g0, uint32_t groups_here, int lane,
+                                          float lo, float hi, float S)
+{
+    const float K = fmaxf(fabsf(lo), hi);
+    const float mae = S * (1.0f / (float)G);             // exact: G is a power of two
+    const float v = S > 0.0f ? K / mae : 0.0f;
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), make_rsrc(pmr + g0, groups_here * 4),
+                                          lane * 4, 0, 0);
+}
+
 template <int G>
 __device__ __forceinline__ void group_range(const float (&r)[G], float &lo, float &hi)
 {
@@ -436,13 +467,15 @@ __device__ __forceinline__ void load_base(const uint32_t *codes, const char *sca
 // FROM_BASE: plane 0 of codes / scales / zeros holds a base checkpoint on
 // entry (read only); the kernel forms R_0 = W - dequant(base) and writes the
 // residual stages 1 .. n_stages - 1 (n_stages >= 2).
-// ZP: zero-point kind; SC: scale storage type.
-template <int G, bool FROM_BASE, int ZP, int SC>
+// ZP: zero-point kind; SC: scale storage type. pmr (may be NULL): per-group
+// peak-to-mean ratios of W as a side output. STATS_ONLY: only pmr.
+template <int G, bool FROM_BASE, int ZP, int SC, bool STATS_ONLY = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void construct_kernel(const uint4 *__restrict__ W,
                                                        int64_t n_groups, int n_stages,
                                                        uint32_t *__restrict__ codes,
                                                        char *__restrict__ scales,
-                                                       float *__restrict__ zeros)
+                                                       float *__restrict__ zeros,
+                                                       float *__restrict__ pmr)
 {
     if (FROM_BASE && n_stages < 2) return;
     constexpr int CH = G / 8;            // 16-byte chunks (8 bfloat16) per group
@@ -498,6 +531,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             }
         }
 
+        // |x| sum for the peak-to-mean side output (the weights, before any stage)
+        const bool stats = !FROM_BASE && pmr != nullptr;
+        float abs_sum = 0.f;
+        if (stats) abs_sum = group_abs_sum<G>(r);
+
         // Prefetch the next tile while this one is quantized.
         load_tile<CH>(W, n_groups, tile + gridDim.x, lane, v);
 
@@ -513,6 +551,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
         } else {
             group_range<G>(r, lo, hi);
         }
+        if (stats) store_pmr<G>(pmr, g0, groups_here, lane, lo, hi, abs_sum);
+        if constexpr (STATS_ONLY) continue;
         for (int k = FROM_BASE ? 1 : 0; k + 1 < n_stages; ++k) {
             stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
             fill_table(tab, lane, sq, z);
@@ -649,52 +689,68 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
 
 template <bool FROM_BASE, int ZP, int SC>
 hipError_t launch_construct_s(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
-                              char *scales, float *zeros, int grid, hipStream_t stream)
+                              char *scales, float *zeros, float *pmr, int grid, hipStream_t stream)
 {
     switch (G) {
-    case 32: return launch(construct_kernel<32, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
-    case 64: return launch(construct_kernel<64, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
-    case 128: return launch(construct_kernel<128, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros);
+    case 32: return launch(construct_kernel<32, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros, pmr);
+    case 64: return launch(construct_kernel<64, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros, pmr);
+    case 128: return launch(construct_kernel<128, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros, pmr);
     default: return hipErrorInvalidValue;
     }
 }
 
 template <bool FROM_BASE, int ZP>
 hipError_t launch_construct_g(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
-                              char *scales, float *zeros, int scale_type, int grid,
+                              char *scales, float *zeros, float *pmr, int scale_type, int grid,
                               hipStream_t stream)
 {
     switch (scale_type) {
-    case kScaleF32: return launch_construct_s<FROM_BASE, ZP, kScaleF32>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
-    case kScaleF16: return launch_construct_s<FROM_BASE, ZP, kScaleF16>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
-    case kScaleBF16: return launch_construct_s<FROM_BASE, ZP, kScaleBF16>(w4, n_groups, G, S, codes, scales, zeros, grid, stream);
+    case kScaleF32: return launch_construct_s<FROM_BASE, ZP, kScaleF32>(w4, n_groups, G, S, codes, scales, zeros, pmr, grid, stream);
+    case kScaleF16: return launch_construct_s<FROM_BASE, ZP, kScaleF16>(w4, n_groups, G, S, codes, scales, zeros, pmr, grid, stream);
+    case kScaleBF16: return launch_construct_s<FROM_BASE, ZP, kScaleBF16>(w4, n_groups, G, S, codes, scales, zeros, pmr, grid, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
 template <bool FROM_BASE>
 hipError_t launch_construct_b(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
-                              char *scales, float *zeros, int zero_point, int scale_type,
-                              int grid, hipStream_t stream)
+                              char *scales, float *zeros, float *pmr, int zero_point,
+                              int scale_type, int grid, hipStream_t stream)
 {
     switch (zero_point) {
-    case kZpInteger: return launch_construct_g<FROM_BASE, kZpInteger>(w4, n_groups, G, S, codes, scales, zeros, scale_type, grid, stream);
-    case kZpReal: return launch_construct_g<FROM_BASE, kZpReal>(w4, n_groups, G, S, codes, scales, zeros, scale_type, grid, stream);
-    case kZpSymmetric: return launch_construct_g<FROM_BASE, kZpSymmetric>(w4, n_groups, G, S, codes, scales, zeros, scale_type, grid, stream);
+    case kZpInteger: return launch_construct_g<FROM_BASE, kZpInteger>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, grid, stream);
+    case kZpReal: return launch_construct_g<FROM_BASE, kZpReal>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, grid, stream);
+    case kZpSymmetric: return launch_construct_g<FROM_BASE, kZpSymmetric>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, grid, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
-                            uint32_t *codes, void *scales, float *zeros, bool from_base,
-                            int zero_point, int scale_type, int grid, hipStream_t stream)
+                            uint32_t *codes, void *scales, float *zeros, float *pmr,
+                            bool from_base, int zero_point, int scale_type, int grid,
+                            hipStream_t stream)
 {
     const uint4 *w4 = reinterpret_cast<const uint4 *>(W);
     char *sc = static_cast<char *>(scales);
-    return from_base ? launch_construct_b<true>(w4, n_groups, G, S, codes, sc, zeros, zero_point,
-                                                scale_type, grid, stream)
-                     : launch_construct_b<false>(w4, n_groups, G, S, codes, sc, zeros, zero_point,
-                                                 scale_type, grid, stream);
+    return from_base ? launch_construct_b<true>(w4, n_groups, G, S, codes, sc, zeros, nullptr,
+                                                zero_point, scale_type, grid, stream)
+                     : launch_construct_b<false>(w4, n_groups, G, S, codes, sc, zeros, pmr,
+                                                 zero_point, scale_type, grid, stream);
+}
+
+hipError_t launch_group_pmr(const uint16_t *W, int64_t n_groups, int G, float *pmr, int grid,
+                            hipStream_t stream)
+{
+    const uint4 *w4 = reinterpret_cast<const uint4 *>(W);
+    uint32_t *nc = nullptr;
+    char *ns = nullptr;
+    float *nz = nullptr;
+    switch (G) {
+    case 32: return launch(construct_kernel<32, false, kZpInteger, kScaleF32, true>, grid, 64, stream, w4, n_groups, 1, nc, ns, nz, pmr);
+    case 64: return launch(construct_kernel<64, false, kZpInteger, kScaleF32, true>, grid, 64, stream, w4, n_groups, 1, nc, ns, nz, pmr);
+    case 128: return launch(construct_kernel<128, false, kZpInteger, kScaleF32, true>, grid, 64, stream, w4, n_groups, 1, nc, ns, nz, pmr);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 template <int K, bool BF16, bool SC16, bool SYM>

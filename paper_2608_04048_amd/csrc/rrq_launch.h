@@ -13,9 +13,16 @@ namespace rrq_detail {
 // 16-bit patterns; zeros are not written for symmetric stages).
 // from_base: stage 0 of the package is an input (a base checkpoint) and only
 // stages 1 .. S-1 are written.
+// pmr (NULL for none; ignored with from_base): per-group peak-to-mean
+// ratios of W as a side output.
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
-                            uint32_t *codes, void *scales, float *zeros, bool from_base,
-                            int zero_point, int scale_type, int grid, hipStream_t stream);
+                            uint32_t *codes, void *scales, float *zeros, float *pmr,
+                            bool from_base, int zero_point, int scale_type, int grid,
+                            hipStream_t stream);
+
+// Per-group peak-to-mean ratios of W only.
+hipError_t launch_group_pmr(const uint16_t *W, int64_t n_groups, int G, float *pmr, int grid,
+                            hipStream_t stream);
 
 // Prefix-k reconstruction of a package with n_groups groups of G, S stages.
 hipError_t launch_reconstruct(const uint32_t *codes, const void *scales,

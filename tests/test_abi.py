@@ -32,9 +32,9 @@ def test_library_exports_every_declared_function():
     lib = rrq.load_library()
     names = _declared_functions()
     assert names == ["rrq_construct", "rrq_construct_format", "rrq_construct_from_base",
-                     "rrq_construct_from_base_format", "rrq_linear", "rrq_linear_format",
-                     "rrq_package_bytes", "rrq_reconstruct", "rrq_reconstruct_format",
-                     "rrq_status_string"]
+                     "rrq_construct_from_base_format", "rrq_construct_stats", "rrq_group_pmr",
+                     "rrq_linear", "rrq_linear_format", "rrq_package_bytes", "rrq_reconstruct",
+                     "rrq_reconstruct_format", "rrq_status_string"]
     for name in names:
         assert hasattr(lib, name), name
     out = os.popen(f"nm -D --defined-only {rrq.LIB_PATH}").read()
@@ -279,3 +279,24 @@ def test_format_enums_match_header():
                  "RRQ_SCALE_F16", "RRQ_SCALE_BF16", "RRQ_ERR_FORMAT"):
         m = re.search(name + r"\s*=\s*(\d+)", text)
         assert m and int(m.group(1)) == getattr(rrq, name), name
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(W=None), rrq.RRQ_ERR_NULL),
+    (dict(pmr=None), rrq.RRQ_ERR_NULL),
+    (dict(G=16), rrq.RRQ_ERR_GROUP),
+    (dict(cols=100), rrq.RRQ_ERR_SHAPE),
+    (dict(W=FAKE + 8), rrq.RRQ_ERR_ALIGN),
+    (dict(pmr=FAKE + 2), rrq.RRQ_ERR_ALIGN),
+])
+def test_group_pmr_rejects(kw, status):
+    a = dict(W=FAKE, rows=64, cols=128, G=128, pmr=FAKE)
+    a.update(kw)
+    assert rrq.load_library().rrq_group_pmr(a["W"], a["rows"], a["cols"], a["G"], a["pmr"], None) == status
+
+
+def test_construct_stats_requires_pmr():
+    lib = rrq.load_library()
+    assert lib.rrq_construct_stats(FAKE, 64, 128, 128, 4, 0, 0, FAKE, FAKE, FAKE, None, None) == rrq.RRQ_ERR_NULL
+    assert lib.rrq_construct_stats(FAKE, 64, 128, 128, 4, 0, 0, FAKE, FAKE, FAKE, FAKE + 2, None) == rrq.RRQ_ERR_ALIGN
+    assert lib.rrq_construct_stats(FAKE, 64, 128, 128, 4, 5, 0, FAKE, FAKE, FAKE, FAKE, None) == rrq.RRQ_ERR_FORMAT
