@@ -10,6 +10,8 @@ Default workload: the 36-layer Qwen3-8B-shaped stack (6.95e9 weights,
 
 After the steps: rrq_construct_from_base (the residual stages on a given base
 checkpoint; here the package's own stage 0) is timed on the same workload,
+the per-group peak-to-mean ratio (alone, and as a side output of
+construction) is timed and its tensor-level indicators reported,
 construction in other stage formats (symmetric with fp16 scales, real
 zero-points, bf16 scales) is timed, rrq_linear decode passes (1 and 16
 tokens, prefixes k = 1..4, one call per tensor on per-tensor packages) are
@@ -224,6 +226,49 @@ def time_formats(W, n, G, S, stream, formats=(("sym", "f16"), ("real", "f32"), (
     return out
 
 
+def time_pmr(w, W, G, S, stream, launches=10):
+    """rrq_group_pmr over the flat workload (HBM: 2 bytes in, 4/G out per
+    weight), rrq_construct_stats against plain construction, and the paper's
+    tensor-level outlier indicators (mean and maximum over tensors of the
+    largest group PMR of each tensor) for the workload."""
+    import torch
+
+    import paper_2608_04048_amd as rrq
+
+    rows, cols = W.shape
+    n = rows * cols
+    pmr = torch.empty(n // G, dtype=torch.float32, device="cuda")
+    codes = torch.empty((S, n // 16), dtype=torch.int32, device="cuda")
+    scales = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+    zeros = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+
+    def timed(fn):
+        fn()
+        ms = []
+        for _ in range(launches):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        return sum(ms) / len(ms)
+
+    t_pmr = timed(lambda: rrq.rrq_group_pmr(W, rows, cols, G, pmr, stream))
+    t_stats = timed(lambda: rrq.rrq_construct_stats(W, rows, cols, G, S, rrq.RRQ_ZP_INTEGER,
+                                                    rrq.RRQ_SCALE_F32, codes, scales, zeros,
+                                                    pmr, stream))
+    t_plain = timed(lambda: rrq.rrq_construct(W, rows, cols, G, S, codes, scales, zeros, stream))
+    tmax = [float(pmr[t.offset // G:(t.offset + t.numel) // G].max()) for t in w.tensors]
+    pbytes = 2 * n + 4 * (n // G)
+    del codes, scales, zeros, pmr
+    return {"group_pmr_ms": round(t_pmr, 4), "group_pmr_hbm_gbs": round(pbytes / (t_pmr * 1e-3) / 1e9, 1),
+            "group_pmr_hbm_frac": round(pbytes / (t_pmr * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "construct_stats_ms": round(t_stats, 4), "construct_ms_same_run": round(t_plain, 4),
+            "mean_tensor_max_pmr": round(sum(tmax) / len(tmax), 3),
+            "max_tensor_max_pmr": round(max(tmax), 3)}
+
+
 def stream_probe(src_bytes, flush_buf=None, launches=10):
     """Practical HBM ceiling for construction's read/write mix: a streaming
     kernel reading src_bytes and writing 5/8 of that (include/hbm_probe.h),
@@ -275,6 +320,8 @@ def main():
                          "256 MB MALL (auto: on when the step moves under 4 GB)")
     ap.add_argument("--no-from-base", action="store_true",
                     help="skip timing rrq_construct_from_base (residual stages on a given base)")
+    ap.add_argument("--no-pmr", action="store_true",
+                    help="skip timing the peak-to-mean ratio side output")
     ap.add_argument("--no-formats", action="store_true",
                     help="skip timing rrq_construct_format in other stage formats")
     ap.add_argument("--no-linear", action="store_true",
@@ -449,6 +496,9 @@ def main():
             "bytes_per_launch": fb_bytes,
             "base": "stage 0 of the package built in the steps",
         }
+    if not args.no_pmr:
+        print("bench: timing the peak-to-mean side output", file=sys.stderr, flush=True)
+        result["pmr"] = time_pmr(w, W, G, S, stream)
     if not args.no_formats:
         print("bench: timing construct in other stage formats", file=sys.stderr, flush=True)
         result["formats"] = time_formats(W, n, G, S, stream)
