@@ -138,18 +138,19 @@ static int rtn_stage_group(float *r, int G, int bits, int update_residual, int z
     }
     float inv = 1.0f / s;
     float z;
-    if (zp == ZP_INT) z = rintf((0.0f - lo) * inv) + 0.0f;   /* integer, +0 not -0 */
+    /* integer zero-point: RNE of the exact |lo| inv (exact in double); +0 */
+    if (zp == ZP_INT) z = (float)rint((double)(0.0f - lo) * (double)inv) + 0.0f;
     else if (zp == ZP_REAL) z = (0.0f - lo) * inv + 0.0f;
     else z = zsym;
     for (int j = 0; j < G; ++j) {
-        float t = r[j] * inv;
         double q;
         if (zp == ZP_REAL) {
+            float t = r[j] * inv;
             q = (double)rintf(t + z);      /* RNE of the rounded sum */
         } else {
-            /* t + z is exact in double at every place where its rounding to
-             * an integer is decided; rint rounds ties to even. */
-            q = rint((double)t + (double)z);
+            /* r inv + z with the product unrounded: exact in double wherever
+             * its rounding to an integer is decided; rint ties to even. */
+            q = rint((double)r[j] * (double)inv + (double)z);
         }
         if (q < 0.0) q = 0.0;
         if (q > (double)maxq) q = (double)maxq;

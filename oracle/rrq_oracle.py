@@ -35,10 +35,10 @@ The paper leaves the floating-point details open; this oracle fixes them
 * range: lo = min(+0, min r), hi = max(+0, max r) (zero is always on the grid);
 * scale: s = fl(fl(hi - lo) / (2^b - 1)); a group whose s is zero or subnormal
   is degenerate: s = z = 0, all codes 0, residual passed through unchanged;
-* inv = fl(1 / s); zero-point z = RNE(fl((0 - lo) * inv)), an integer stored
-  as binary32;
-* code: t = fl(r * inv), Q = clamp(RNE(t + z), 0, 2^b - 1) where t + z is the
-  exact sum, rounded once, ties to even;
+* inv = fl(1 / s); zero-point z = RNE((0 - lo) * inv) of the exact product,
+  an integer stored as binary32;
+* code: Q = clamp(RNE(r * inv + z), 0, 2^b - 1) of the exact value (the
+  product is not rounded), ties to even;
 * dequantized stage value rhat = fl((Q - z) * s); next residual
   r <- fl(r - rhat);
 * reconstruction after k stages: acc = rhat_0, then acc = fl(acc + rhat_t) for
@@ -51,8 +51,9 @@ Inputs must be finite bfloat16 values whose per-group range hi - lo is finite
 in binary32 (always so when every |x| < 2^127); the oracle raises otherwise.
 
 Every step below is a separate numpy float32 operation (one IEEE rounding per
-operation, no fused multiply-add). Where a step needs an exact value (t + z),
-it is formed in float64, where it is exact; see ``_exact_round_sum``.
+operation, no fused multiply-add). Where a step needs an exact value (r * inv
++ z, |lo| * inv), it is formed in float64, where it is exact; see
+``_exact_round_sum``.
 """
 
 from __future__ import annotations
@@ -97,16 +98,18 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
 # One RTN stage on a batch of groups (Eq. 1-3)
 # ---------------------------------------------------------------------------
 
-def _exact_round_sum(t: np.ndarray, z: np.ndarray) -> np.ndarray:
-    """RNE(t + z) of the exact sum of a binary32 t and a small integer z.
+def _exact_round_sum(r: np.ndarray, inv: np.ndarray, z: np.ndarray) -> np.ndarray:
+    """RNE(r inv + z) of the exact value, for binary32 r and inv and a small
+    integer z (the product is not rounded).
 
-    In float64 the sum is exact whenever |t| >= 1/4 (t then has no bits below
-    2^-25 and |t + z| < 8), and when |t| < 1/4 the sum lies within 1/4 of an
+    In float64 the product r inv (two 24-bit significands) is exact. When
+    |r inv| >= 1/8 its lowest bit is at or above 2^-51 and |r inv + z| < 8, so
+    the sum is exact too; when |r inv| < 1/8 the sum lies within 1/8 of an
     integer, so the float64 rounding cannot move it across a half-integer. In
     both cases rounding the float64 sum to an integer, ties to even, gives the
-    rounding of the exact sum.
+    rounding of the exact value.
     """
-    return np.rint(t.astype(np.float64) + z.astype(np.float64))
+    return np.rint(r.astype(np.float64) * inv.astype(np.float64) + z.astype(np.float64))
 
 
 ZERO_POINTS = ("int", "real", "sym")
@@ -136,9 +139,10 @@ def rtn_stage(r: np.ndarray, bits: int, zero_point: str = "int", scale_dtype: st
     Eq. 1 (q = x/s + z with a scale and zero-point shared by the group),
     Eq. 2 (Q = R(q)) and Eq. 3 (dequantized value (Q - z) s).
 
-    ``zero_point``: "int" (the default reading: z = RNE(fl(-lo inv)), Q the
-    single rounding of the exact t + z); "real" (z = fl(-lo inv) kept real,
-    Q = RNE(fl(t + z))); "sym" (symmetric stage: the range is widened to
+    ``zero_point``: "int" (the default reading: z = RNE(-lo inv) and Q =
+    RNE(r inv + z), each the single rounding of the exact value); "real"
+    (z = fl(-lo inv) kept real, t = fl(r inv), Q = RNE(fl(t + z))); "sym"
+    (symmetric stage: the range is widened to
     [-amax, amax], amax = max(-lo, hi), and z is fixed at 2^(b-1), not
     stored; a degenerate group gets the zero code Q = z).
     ``scale_dtype``: the scale is rounded to its storage type ("f16", "bf16")
@@ -171,7 +175,7 @@ def rtn_stage(r: np.ndarray, bits: int, zero_point: str = "int", scale_dtype: st
     s_safe = np.where(degenerate, F32(1.0), s)
     inv = F32(1.0) / s_safe                    # fl(1 / s)
     if zero_point == "int":
-        z = np.rint((zero - lo) * inv)         # RNE(fl((0 - lo) * inv))
+        z = np.rint((zero - lo).astype(np.float64) * inv)   # RNE(|lo| inv), product exact
     elif zero_point == "real":
         z = (zero - lo) * inv                  # fl((0 - lo) * inv)
     else:
@@ -181,11 +185,11 @@ def rtn_stage(r: np.ndarray, bits: int, zero_point: str = "int", scale_dtype: st
     inv = np.where(degenerate, zero, inv)
     s = np.where(degenerate, zero, s)
 
-    t = r * inv[:, None]                       # fl(r * inv)
     if zero_point == "real":
+        t = r * inv[:, None]                   # fl(r * inv)
         q = np.rint(t + z[:, None])            # RNE(fl(t + z))
     else:
-        q = _exact_round_sum(t, z[:, None])    # RNE(t + z), one rounding
+        q = _exact_round_sum(r, inv[:, None], z[:, None])   # RNE(r inv + z), one rounding
     Q = np.clip(q, 0, maxq)
     Q = np.where(degenerate[:, None], z_deg, Q).astype(np.uint8)
 

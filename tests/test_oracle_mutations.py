@@ -18,13 +18,12 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(os.path.dirname(HERE), "oracle", "rrq_oracle.py")
 
 MUTATIONS = {
-    "zero_point_dropped": ("q = _exact_round_sum(t, z[:, None])", "q = _exact_round_sum(t, 0 * z[:, None])"),
-    "zero_point_sign": ("z = np.rint((zero - lo) * inv)", "z = np.rint((lo - zero) * inv)"),
+    "zero_point_dropped": ('q = _exact_round_sum(r, inv[:, None], z[:, None])', 'q = _exact_round_sum(r, inv[:, None], 0 * z[:, None])'),
+    "zero_point_sign": ('z = np.rint((zero - lo).astype(np.float64) * inv)', 'z = np.rint((lo - zero).astype(np.float64) * inv)'),
     "range_without_zero": ("lo = np.minimum(r.min(axis=1), zero)", "lo = r.min(axis=1)"),
     "range_transposed": ("d = hi - lo ", "d = lo - hi "),
     "steps_off_by_one": ("s = d / F32(maxq)", "s = d / F32(maxq + 1)"),
-    "floor_not_nearest": ("return np.rint(t.astype(np.float64) + z.astype(np.float64))",
-                          "return np.floor(t.astype(np.float64) + z.astype(np.float64))"),
+    "floor_not_nearest": ('return np.rint(r.astype(np.float64) * inv.astype(np.float64) + z.astype(np.float64))', 'return np.floor(r.astype(np.float64) * inv.astype(np.float64) + z.astype(np.float64))'),
     "no_clamp": ("Q = np.clip(q, 0, maxq)", "Q = np.clip(q, -8, 8)"),
     "dequant_without_zero_point": ("qz = Q.astype(np.float32) - z[:, None]", "qz = Q.astype(np.float32)"),
     "residual_not_updated": ("r = r - rhat                           # R_k", "r = r                                  # R_k"),
@@ -60,6 +59,10 @@ MUTATIONS = {
                                 "        z = np.rint((zero - lo) * inv)"),
     "scale_not_rounded_to_storage": ("    s = round_scale(s, scale_dtype)            # the stored scale is the one used",
                                      "    s = s"),
+    "zero_point_of_rounded_product": ("z = np.rint((zero - lo).astype(np.float64) * inv)",
+                                      "z = np.rint(((zero - lo) * inv).astype(np.float64))"),
+    "code_of_rounded_product": ("return np.rint(r.astype(np.float64) * inv.astype(np.float64) + z.astype(np.float64))",
+                                "return np.rint((r * inv).astype(np.float64) + z.astype(np.float64))"),
     "pmr_single_running_sum": ("        p[j % 4] = p[j % 4] + a[:, j]", "        p[0] = p[0] + a[:, j]"),
     "pmr_sum_not_averaged": ("    mae = S / np.float32(group_size)", "    mae = S"),
     "pmr_peak_without_abs": ("    K = a.max(axis=1)", "    K = x.max(axis=1)"),
