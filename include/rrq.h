@@ -23,12 +23,13 @@
  *   lo = min(+0, min r), hi = max(+0, max r) over the group;
  *   s = fl(fl(hi - lo) / 3); if s < 2^-126 (zero or subnormal) the group is
  *     degenerate for that stage: s = z = 0, all codes 0, residual unchanged;
- *   inv = fl(1 / s); z = RNE(fl((0 - lo) * inv)), an integer in {0,1,2,3};
- *   Q = clamp(RNE(fl(r * inv) + z), 0, 3), where fl(r * inv) + z is rounded
- *     once, ties to even;
+ *   inv = fl(1 / s); z = RNE((0 - lo) * inv), an integer in {0,1,2,3};
+ *   Q = clamp(RNE(r * inv + z), 0, 3);
+ *     in both the product is exact (not rounded to binary32) and the value is
+ *     rounded once to the nearest integer, ties to even;
  *   rhat = fl((Q - z) * s); next residual r <- fl(r - rhat);
- *   every operation is one correctly rounded binary32 operation, nearest-even,
- *   with no fused multiply-add.
+ *   every other operation is one correctly rounded binary32 operation,
+ *   nearest-even.
  *   Reconstruction after k stages: acc = rhat_0, acc = fl(acc + rhat_t) for
  *   t = 1..k-1 in stage order; binary32 output, or bfloat16 rounded to
  *   nearest-even.
@@ -101,7 +102,8 @@ enum rrq_dtype {
  * RRQ_ZP_INTEGER and RRQ_SCALE_F32, the arithmetic stated above.
  *
  * Zero-point kind:
- *   RRQ_ZP_INTEGER    z = RNE(fl(|lo| inv)), stored as float (the default).
+ *   RRQ_ZP_INTEGER    z = RNE(|lo| inv) of the exact product, stored as float
+ *                     (the default).
  *   RRQ_ZP_REAL       z = fl(|lo| inv) is kept real and stored; the code is
  *                     Q = clamp(RNE(fl(fl(r inv) + z)), 0, 3) (the sum is
  *                     rounded to binary32 first); dequantized values are

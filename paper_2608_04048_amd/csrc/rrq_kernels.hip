@@ -24,16 +24,18 @@
 //   * per group and stage (once per lane): range lo = min(0, min r),
 //     hi = max(0, max r) (two-chain min3/max3, fused into the previous stage's
 //     residual update), s = fl((hi - lo) / 3), inv = fl(1 / s),
-//     z = RNE(fl(|lo| inv)), and a per-lane LDS table of dequantized pairs;
-//   * per element and stage: t = fl(r inv); u = fl(t + 1.5 * 2^23 + z) is the
-//     single nearest-even rounding of the exact t + z (u lies in [2^23, 2^24),
+//     z = RNE(|lo| inv) (the exact product), and a per-lane LDS table of
+//     dequantized pairs;
+//   * per element and stage: u = fma(r, inv, 1.5 * 2^23 + z) is the single
+//     nearest-even rounding of the exact r inv + z (u lies in [2^23, 2^24),
 //     where binary32 spacing is 1); one clamped FMA turns u into a tiny
 //     binary32 whose bit pattern is 3 - min(Q, 3); exact FMAs on such values
 //     pack the codes and form the LDS address of each element pair's
 //     dequantized values fl((Q - z) s); r = fl(r - rhat). Lanes past the input
 //     compute on zeros and their stores fall outside the buffer resources.
-//   * Clamp: no element can round below code 0 (z comes from the same
-//     fl(|lo| inv) that bounds every fl(r inv) from below); the upper clamp
+//   * Clamp: no element can round below code 0 (z = RNE(|lo| inv) of the same
+//     exact product that bounds every r inv from below, so r inv + z >= -1/2,
+//     and -1/2 rounds to -0, code 0); the upper clamp
 //     is needed in most tiles (a residual range symmetric about zero gives
 //     z = RNE(1.5) = 2 and puts its top element on code 4) and costs nothing
 //     here: it is the clamp modifier of the FMA above.
@@ -53,7 +55,7 @@ namespace {
 constexpr float kMagic = 12582912.0f;          // 1.5 * 2^23
 
 // Stage formats (values of the C ABI's zero-point and scale-type enums).
-constexpr int kZpInteger = 0;    // z = RNE(fl(|lo| inv)), stored
+constexpr int kZpInteger = 0;    // z = RNE(|lo| inv), exact product, stored
 constexpr int kZpReal = 1;       // z = fl(|lo| inv), stored
 constexpr int kZpSymmetric = 2;  // range [-amax, amax], z = 2, not stored
 constexpr int kScaleF32 = 0, kScaleF16 = 1, kScaleBF16 = 2;
@@ -97,12 +99,12 @@ struct DequantTable {
 };
 
 // Code of one element as the tiny binary32 (3 - min(Q, 3)) 2^-149, where
-// Q = RNE(fl(r inv) + z): t = fl(r inv); u = fl(t + 1.5 * 2^23 + z) rounds the
-// exact t + z once to the nearest integer, ties to even (u lies in
+// Q = RNE(r inv + z) of the exact value: u = fma(r, inv, 1.5 * 2^23 + z) rounds
+// the exact r inv + z once to the nearest integer, ties to even (u lies in
 // [2^23, 2^24), where binary32 spacing is 1).
 __device__ __forceinline__ float tiny_code(float r, float inv, float m)
 {
-    const float u = r * inv + m;   // two roundings: no contraction in this build
+    const float u = __builtin_fmaf(r, inv, m);
     return __builtin_amdgcn_fmed3f(__builtin_fmaf(u, kNegTiny, kTopTiny), 0.0f, 1.0f);
 }
 
@@ -409,7 +411,8 @@ __device__ __forceinline__ void stage_params(float lo, float hi, float &inv, flo
     const bool degenerate = !(s >= 0x1p-126f);
     inv = degenerate ? 0.0f : 1.0f / s;
     sq = degenerate ? 0.0f : s;
-    if constexpr (ZP == kZpInteger) z = rintf(fabsf(lo) * inv);
+    // integer zero-point: RNE of the exact |lo| inv, by the same magic addend
+    if constexpr (ZP == kZpInteger) z = __builtin_fmaf(fabsf(lo), inv, kMagic) - kMagic;
     else if constexpr (ZP == kZpReal) z = fabsf(lo) * inv;
     else z = 2.0f;
     m = kMagic + z;
