@@ -21,7 +21,8 @@ import os
 import sys
 from collections import defaultdict
 
-DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "stream_probe_kernel", "copyBuffer"]
+DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "linear_kernel", "stream_probe_kernel",
+                 "copyBuffer"]
 
 
 def _short(name: str) -> str:
@@ -117,6 +118,30 @@ def stats(path: str, match):
     return rows
 
 
+def trace(path: str, match, first: int = 0):
+    """Per-kernel durations from a rocprofv3 kernel-trace csv, in dispatch
+    order: (kernel, calls, average, min, max, average of the first `first`
+    dispatches) in microseconds. The first dispatches of a kernel are the
+    ones of the leg that runs first in the profiled program."""
+    per = defaultdict(list)
+    with open(path, newline="") as fh:
+        for row in csv.DictReader(fh):
+            name = row.get("Kernel_Name", "")
+            if not any(m in name for m in match):
+                continue
+            per[_short(name)].append((int(row["Start_Timestamp"]),
+                                      (int(row["End_Timestamp"]) - int(row["Start_Timestamp"])) / 1e3))
+    out = []
+    for k, v in per.items():
+        v.sort()
+        d = [x for _, x in v]
+        head = d[:first] if first > 0 else []
+        out.append((k, len(d), sum(d) / len(d), min(d), max(d),
+                    sum(head) / len(head) if head else float("nan")))
+    out.sort(key=lambda r: -r[1] * r[2])
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -126,6 +151,10 @@ def main(argv=None):
     b = sub.add_parser("stats")
     b.add_argument("path")
     b.add_argument("--match", nargs="*", default=DEFAULT_MATCH)
+    tr = sub.add_parser("trace")
+    tr.add_argument("path")
+    tr.add_argument("--match", nargs="*", default=DEFAULT_MATCH)
+    tr.add_argument("--first", type=int, default=0)
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
@@ -153,6 +182,12 @@ def main(argv=None):
         print(f"| HBM bytes read per launch | {r['read_bytes']:.6e} |")
         print(f"| HBM bytes written per launch | {r['written_bytes']:.6e} |")
         print(f"| dispatches profiled (fetch, write) | {r['dispatches']} |")
+        return 0
+    if args.cmd == "trace":
+        print(f"| kernel | calls | average (us) | min (us) | max (us) | average of the first {args.first} (us) |")
+        print("|---|---:|---:|---:|---:|---:|")
+        for k, n, avg, mn, mx, hd in trace(args.path, args.match, args.first):
+            print(f"| {k} | {n} | {avg:.1f} | {mn:.1f} | {mx:.1f} | {hd:.1f} |")
         return 0
     if args.cmd == "counters":
         print("| kernel | counter | mean per dispatch | dispatches | mean duration (us) |")
