@@ -14,8 +14,9 @@ the per-group peak-to-mean ratio (alone, and as a side output of
 construction) is timed and its tensor-level indicators reported,
 construction in other stage formats (symmetric with fp16 scales, real
 zero-points, bf16 scales) is timed, rrq_linear decode passes (1 and 16
-tokens, prefixes k = 1..4, one call per tensor on per-tensor packages) are
-timed, and a streaming probe with the same read/write mix gives the practical HBM
+tokens, prefixes k = 1..4, one call per tensor on per-tensor packages, the
+pass replayed as a HIP graph and also launched call by call) are timed, and a
+streaming probe with the same read/write mix gives the practical HBM
 ceiling (include/hbm_probe.h).
 
 Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
@@ -135,8 +136,12 @@ def linear_bytes(w, k, M):
 def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 2, 3, 4),
                 launches=10):
     """Decode-style passes of rrq_linear over every tensor of w (one call per
-    tensor, each tensor its own package), timed with HIP events around the
-    whole pass. Builds the per-tensor packages first (untimed)."""
+    tensor, each tensor its own package). A pass is captured once in a HIP
+    graph and replayed, as a serving loop would run it, and timed with HIP
+    events around each replay ("ms"); the same pass launched call by call
+    from Python is timed too ("ms_eager": at a few microseconds per call it
+    is bound by the host's launch rate for the small tensors). Builds the
+    per-tensor packages first (untimed)."""
     import torch
 
     import paper_2608_04048_amd as rrq
@@ -157,24 +162,42 @@ def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 
     xs = {c: torch.randn((max_m, c), generator=g, device="cuda").to(torch.bfloat16)
           for c in sorted({t.cols for t in w.tensors})}
     y = torch.empty(max_m * max(t.rows for t in w.tensors), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        fn()
+        ms = []
+        for _ in range(launches):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        return sum(ms) / len(ms)
+
     out = {}
+    cs = torch.cuda.Stream()
     for M in tokens:
         for k in ks:
-            def run():
+            def run(st, M=M, k=k):
                 for t, c, sc, zz in pk:
-                    rrq.rrq_linear(c, sc, zz, t.rows, t.cols, G, S, k, xs[t.cols], M, y, stream)
-            run()
-            ms = []
-            for _ in range(launches):
-                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                a.record(stream)
-                run()
-                b.record(stream)
-                b.synchronize()
-                ms.append(a.elapsed_time(b))
-            t_ms = sum(ms) / len(ms)
+                    rrq.rrq_linear(c, sc, zz, t.rows, t.cols, G, S, k, xs[t.cols], M, y, st)
+            t_eager = timed(lambda: run(stream))
+            cs.wait_stream(stream)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=cs):
+                run(cs)
+            stream.wait_stream(cs)
+
+            def replay():
+                with torch.cuda.stream(stream):
+                    graph.replay()
+            t_ms = timed(replay)
+            del graph
             nbytes = linear_bytes(w, k, M)
-            out[f"M{M}_k{k}"] = {"ms": round(t_ms, 4), "bytes": nbytes,
+            out[f"M{M}_k{k}"] = {"ms": round(t_ms, 4), "ms_eager": round(t_eager, 4),
+                                 "bytes": nbytes,
                                  "hbm_gbs": round(nbytes / (t_ms * 1e-3) / 1e9, 1),
                                  "hbm_frac": round(nbytes / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     return out
@@ -505,7 +528,8 @@ def main():
     if not args.no_linear:
         print("bench: timing rrq_linear decode passes", file=sys.stderr, flush=True)
         result["linear"] = time_linear(w, W.view(-1), codes, scales, zeros, stream)
-        result["linear"]["calls"] = f"one rrq_linear call per tensor ({len(w.tensors)} per pass)"
+        result["linear"]["calls"] = (f"one rrq_linear call per tensor ({len(w.tensors)} per pass), "
+                                     "the pass replayed as one HIP graph")
     if not args.no_stream_probe:
         result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
         result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)

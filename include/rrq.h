@@ -290,20 +290,22 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *
  *   codes, scales, zeros  device, a package (as rrq_reconstruct reads it).
  *   rows, cols, group_size, n_stages  the package's shape; same rules as
- *              rrq_construct, and rows, cols < 2^26.
+ *              rrq_construct, and rows, cols < 2^26, k_stages * rows * cols
+ *              / 4 < 2^32 (the code planes read span less than 4 GiB).
  *   k_stages   1..n_stages (2 k_stages effective bits).
  *   X          device, bfloat16 bit patterns [n_tokens][cols], 16-byte
  *              aligned (read only).
- *   n_tokens   >= 1; tokens are processed 16 at a time (the package is read
- *              once per 16 tokens), so decode (1..16 tokens) reads it once.
+ *   n_tokens   >= 1; tokens are processed 4 at a time (the package is read
+ *              once per 4 tokens: single-token decode reads it once).
  *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
  *   stream     HIP stream the work is enqueued on.
  *
  * Arithmetic: every product X * (1 + Q/4), X * 1 is exact in the matrix
  * cores; fp32 rounding enters in the accumulations only, in a fixed order
  * (results are deterministic). With u = 2^-24, A = sum_{t, g} |s_t,g|
- * (11 + |z_t,g|) sum_{i in g} |X[m][i]| and n = k_stages * (ceil(groups
- * per row / 8) + 1), |Y[m][o] - exact| <= 1.05 u A (group_size + 2 n + 24).
+ * (11 + |z_t,g|) sum_{i in g} |X[m][i]|, p = groups per row and
+ * n = k_stages * (min(p, 4 ceil(p / 16)) + 1),
+ * |Y[m][o] - exact| <= 1.05 u A (group_size + 2 n + 24).
  *
  * Returns RRQ_OK, or RRQ_ERR_NULL / _ALIGN / _SHAPE / _GROUP / _STAGES with
  * nothing enqueued, or RRQ_ERR_HIP if the kernel launch failed.

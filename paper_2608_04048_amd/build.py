@@ -35,6 +35,10 @@ DEVICE_FLAGS = [
     "-Wall",
 ]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra"]
+# Per-source device flags: the linear kernel keeps its MFMA results in
+# ordinary VGPRs (its accumulations are VALU work, so accumulator registers
+# would only add copies).
+SOURCE_FLAGS = {"rrq_linear": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:
@@ -63,7 +67,7 @@ def build(keep_asm: bool = False) -> str:
     kern_objs = []
     for name in ("rrq_kernels", "rrq_linear"):
         obj = os.path.join(BUILD_DIR, name + ".o")
-        cmd = [cc, *DEVICE_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+        cmd = [cc, *DEVICE_FLAGS, *SOURCE_FLAGS.get(name, []), f"-I{INCLUDE}", f"-I{CSRC}", "-c",
                os.path.join(CSRC, name + ".hip"), "-o", obj]
         if keep_asm:
             cmd += ["-save-temps=obj"]

@@ -141,6 +141,8 @@ int linear_common(const uint32_t *codes, const void *scales, const float *zeros,
     if (k_stages < 1 || k_stages > n_stages) return RRQ_ERR_STAGES;
     if (n_tokens < 1 || rows >= rrq_detail::kLinearMaxDim || cols >= rrq_detail::kLinearMaxDim)
         return RRQ_ERR_SHAPE;
+    // the k stage planes the kernel reads span less than 4 GiB of codes
+    if ((uint64_t)k_stages * (uint64_t)(n / 4) >= (uint64_t(1) << 32)) return RRQ_ERR_SHAPE;
     if (!aligned(codes, 16) || !aligned(X, 16) || !aligned(Y, 4)) return RRQ_ERR_ALIGN;
     if (current_cu_count() <= 0) return RRQ_ERR_HIP;
     hipError_t e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,

@@ -6,12 +6,12 @@
 // Per group g of G inputs and stage t the sum over the group factors as
 //   s_t (sum_i x_i Q_i - z_t sum_i x_i),
 // and both inner sums run on v_mfma_f32_16x16x32_bf16 with fp32 accumulation:
-//   * A operand: 16 tokens x 32 inputs of X (bfloat16, exact);
+//   * A operand: 16 token rows x 32 inputs of X (bfloat16, exact);
 //   * B operand: 32 inputs x 16 output rows of codes, each code Q encoded as
 //     the bfloat16 1 + Q/4 (bits 0x3F80 | Q << 5: the code lands in the top
-//     two mantissa bits with one shift, one AND and one OR per pair of
-//     codes), so the MFMA yields P = sum x (1 + Q/4) and
-//     sum x Q = 4 P - 4 Sx exactly in real arithmetic;
+//     two mantissa bits with one shift and one AND-OR per pair of codes), so
+//     the MFMA yields P = sum x (1 + Q/4) and sum x Q = 4 P - 4 Sx exactly in
+//     real arithmetic;
 //   * Sx = sum x over the group comes from the same MFMA with a B operand of
 //     bfloat16 ones.
 // The group's contribution s (4 P - (4 + z) Sx) is added to the lane's fp32
@@ -19,14 +19,25 @@
 // exact; fp32 rounding enters only in the accumulations (error bound in the
 // tests).
 //
-// Work split: a workgroup of 8 waves owns 16 output rows; the groups of a
-// row are split into 8 contiguous ranges, one per wave, each wave keeping
-// the loads of two groups in flight; the partial results are summed through
-// LDS in wave order (deterministic). Tokens are processed 16 at a time. The
-// loads are shaped for the vector-memory address path, which bounds this
-// kernel before HBM does: no lane loads a code word another lane of its row
-// loads (G = 128, 64), activations come in 16-byte loads and only for live
-// tokens, scales and zero-points for two groups per load.
+// Work split: a workgroup of 4 waves owns 16 output rows; the groups of a
+// row are split into 4 contiguous ranges, one per wave, and each wave walks
+// its range in chunks of groups. The partial results are summed through
+// LDS in wave order (deterministic). Up to 4 tokens are served by one pass
+// over the package (chunks of 4 groups); more tokens go 16 at a time
+// (chunks of 2 groups, so that a chunk's activations fit the same LDS).
+//
+// Memory path: everything a chunk needs (codes of 16 rows per stage, scales
+// and zero-points, activations of the tile's tokens) goes
+// from memory straight into LDS with LDS-DMA buffer loads, the code loads
+// covering whole 128-byte runs of a row (8 rows per instruction for
+// G = 128), and is read back in the MFMA operand layout. Every wave
+// double-buffers its chunks, so the next chunk is in flight while the
+// current one is computed. The DMA instructions are issued from inline
+// assembly, a fixed number per chunk, and the wave waits for exactly the
+// chunk it is about to read (s_waitcnt vmcnt(n) with n = one chunk's
+// instructions); no other vector-memory loads are issued in the loop. LDS
+// slots are XOR-swizzled so that the reads of 16 rows (or 4 tokens) fall in
+// distinct banks.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -36,20 +47,141 @@
 namespace rrq_detail {
 namespace {
 
-using rsrc_t = __amdgpu_buffer_rsrc_t;
-constexpr int kRsrcWord3 = 0x00020000;
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
+constexpr uint32_t kRsrcWord3 = 0x00020000u;
 constexpr uint32_t kOnePair = 0x3F803F80u;    // two bfloat16 1.0
 constexpr uint32_t kCodeMask = 0x00600060u;   // top two mantissa bits of both halves
+// Offset added to an activation load that must not touch memory: past the
+// activation buffer's size (below 2^30 bytes), so it reads zeros.
+constexpr uint32_t kSkip = 0x80000000u;
 
-__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes)
+constexpr int kWaves = kLinearThreads / 64;
+
+// Package stage format (values of the C ABI's enums).
+constexpr int kZpSymmetric = 2;
+constexpr int kScaleF32 = 0, kScaleF16 = 1;
+
+// A pass over the package serves a tile of TT tokens: TT = 4 (decode, up to
+// 4 tokens) walks the groups in chunks of 4, TT = 16 in chunks of 2, so that
+// a chunk's activations fit the same LDS budget.
+//
+// LDS image of one chunk (per wave and buffer), in 16-byte slots:
+//   codes   K stages x 16 rows x RB bytes (CG groups of G / 4 bytes; a stage
+//           takes at least the 1 KiB one DMA instruction writes),
+//   scales  K stages x 16 rows x CG groups, one dword each (a stage takes
+//           the 256 bytes one dword DMA writes),
+//   zeros   the same,
+//   X       TT tokens x CG G inputs x 2 bytes (whole KiB: the DMA
+//           lanes past the last token read zeros into the padding).
+// Groups per chunk.
+constexpr int chunk_groups(int G, int K, int TT)
 {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
-                                             kRsrcWord3);
+    return (void)G, (void)K, TT == 4 ? 4 : 2;
+}
+
+template <int G, int K, int TT>
+struct Chunk {
+    static constexpr int CG = chunk_groups(G, K, TT);
+    static constexpr int RB = CG * G / 4;                         // code bytes per row
+    static constexpr int SLOTS = RB / 16;                         // code slots per row
+    static constexpr int CODE_BYTES = 16 * RB > 1024 ? 16 * RB : 1024;
+    static constexpr int CODE_DMA = CODE_BYTES / 1024;            // per stage
+    static constexpr int PARAM_BYTES = 256;
+    static constexpr int SCALES = K * CODE_BYTES;
+    static constexpr int ZEROS = SCALES + K * PARAM_BYTES;
+    static constexpr int XOFF = ZEROS + K * PARAM_BYTES;
+    static constexpr int X_ROW = CG * G * 2;                      // one token
+    static constexpr int X_SLOTS = X_ROW / 16;
+    static constexpr int X_DMA = (TT * X_ROW + 1023) / 1024;     // whole KiB (padding reads zeros)
+    static constexpr int BYTES = XOFF + X_DMA * 1024;
+    // DMA instructions per chunk: what one wait leaves in flight
+    static constexpr int DMA = K * (CODE_DMA + 2) + X_DMA;
+    static_assert(DMA <= 31, "two chunks in flight must fit the vmcnt counter");
+    static_assert(16 * CG * 4 <= PARAM_BYTES, "chunk shape");
+
+    // Slot k of code row r holds the row's piece k ^ code_swizzle(r): rows
+    // that share LDS banks (256 / RB rows apart) get different slots.
+    static __device__ __forceinline__ int code_swizzle(int r)
+    {
+        return SLOTS > 1 ? (r * RB / 256) & (SLOTS - 1) : 0;
+    }
+    // Slot p of token row tk holds piece p ^ x_swizzle(tk): token rows that
+    // share banks get different slots (4 tokens: rows are a multiple of 256
+    // bytes long; 16 tokens: 16 distinct patterns where the row has them).
+    static __device__ __forceinline__ int x_swizzle(int tk)
+    {
+        return (TT == 4 ? 4 * tk : tk) & (X_SLOTS - 1);
+    }
+};
+
+// Raw buffer descriptor (gfx9 family): accesses beyond bytes read zero.
+__device__ __forceinline__ u32x4 make_desc(const void *base, uint32_t bytes)
+{
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    u32x4 d;
+    d[0] = (uint32_t)a;
+    d[1] = (uint32_t)(a >> 32) & 0xFFFFu;
+    d[2] = bytes;
+    d[3] = kRsrcWord3;
+    return d;
+}
+
+// LDS-DMA loads: every lane reads from the buffer at byte offset
+// soff + voff (both range-checked against the descriptor's size) and the
+// wave writes LDS at lds + lane * 16 (dwordx4) or lds + lane * 4 (dword,
+// ushort). lds is a wave-uniform LDS byte address. m0, which
+// carries it, is restored. The wait states the compiler cannot see inside
+// the block are explicit: 5 before the load reads SGPRs that a VALU
+// instruction may have just written (spill reloads), 1 after writing m0.
+__device__ __forceinline__ void dma_x4(const u32x4 &desc, uint32_t soff, uint32_t lds,
+                                       uint32_t voff)
+{
+    uint32_t m0;
+    asm volatile("s_nop 4\n\t"
+                 "s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "buffer_load_dwordx4 %1, %3, %4 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(m0) : "v"(voff), "s"(lds), "s"(desc), "s"(soff) : "memory");
+}
+
+__device__ __forceinline__ void dma_dword(const u32x4 &desc, uint32_t soff, uint32_t lds,
+                                       uint32_t voff)
+{
+    uint32_t m0;
+    asm volatile("s_nop 4\n\t"
+                 "s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "buffer_load_dword %1, %3, %4 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(m0) : "v"(voff), "s"(lds), "s"(desc), "s"(soff) : "memory");
+}
+
+__device__ __forceinline__ void dma_ushort(const u32x4 &desc, uint32_t soff, uint32_t lds,
+                                       uint32_t voff)
+{
+    uint32_t m0;
+    asm volatile("s_nop 4\n\t"
+                 "s_mov_b32 %0, m0\n\t"
+                 "s_mov_b32 m0, %2\n\t"
+                 "s_nop 0\n\t"
+                 "buffer_load_ushort %1, %3, %4 offen lds\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(m0) : "v"(voff), "s"(lds), "s"(desc), "s"(soff) : "memory");
+}
+
+// Wait until at most N of the wave's vector-memory instructions are in
+// flight.
+template <int N>
+__device__ __forceinline__ void wait_vm()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
 __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x4 &c)
@@ -60,13 +192,15 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x
 
 // B operand of one block: codes q = 0..3 of the (pre-shifted) word w sit at
 // bits 2q and 16 + 2q; register q gets codes q and q + 8 as 1 + code / 4.
-__device__ __forceinline__ u32x4 code_operand(uint32_t w)
+// mask and one hold kCodeMask and kOnePair in registers, so that each
+// register costs a shift and one AND-OR.
+__device__ __forceinline__ u32x4 code_operand(uint32_t w, uint32_t mask, uint32_t one)
 {
     u32x4 b;
-    b[0] = ((w << 5) & kCodeMask) | kOnePair;
-    b[1] = ((w << 3) & kCodeMask) | kOnePair;
-    b[2] = ((w << 1) & kCodeMask) | kOnePair;
-    b[3] = ((w >> 1) & kCodeMask) | kOnePair;
+    b[0] = ((w << 5) & mask) | one;
+    b[1] = ((w << 3) & mask) | one;
+    b[2] = ((w << 1) & mask) | one;
+    b[3] = ((w >> 1) & mask) | one;
     return b;
 }
 
@@ -83,241 +217,291 @@ __device__ __forceinline__ u32x4 act_operand(const u32x2 &run1, const u32x2 &run
     return a;
 }
 
-// Lane layout of one group (G inputs of 16 output rows, nb = G / 32 MFMA
-// blocks of 32 inputs). Lane l: row / token r = l % 16, slice j = l / 16.
-//   G = 128: lane j owns code words 2j, 2j + 1 of the row's group (one 8-byte
-//            load per stage) and the activations of their 32 inputs; block b
-//            takes word 2j + b / 2, element pairs of half b % 2.
-//   G = 64:  lane j owns word j; block b takes its half b.
+// Buffers of one row tile and token tile: one descriptor per package
+// array, from the row tile in stage 0 to its end in stage K - 1, and the
+// byte stride between stage planes (the loads' scalar offset). Rows past
+// the last row read the next plane's data (never used) or, in the last
+// plane, zeros.
+struct Sources {
+    u32x4 codes, scales, zeros;
+    uint32_t code_plane, scale_plane, zero_plane;
+    u32x4 x;
+    uint32_t row_bytes;   // code bytes per row: cols / 4
+    uint32_t gpr;         // groups per row
+    uint32_t x_row;       // activation bytes per token: cols * 2
+    uint32_t m_here;      // live tokens of the tile
+    int scale_type;
+    bool sym;
+};
+
+// Issue the DMA of the chunk whose first group is g0 into the LDS buffer
+// at byte address lds: Chunk<G, K, TT>::DMA instructions, whatever the format
+// (zero-points of symmetric stages and tokens past the tile read zeros
+// without touching memory). Code rows past the tile and inputs past the row
+// read zeros or the next row's data: those groups are never computed.
+template <int G, int K, int TT>
+__device__ __forceinline__ void load_chunk(uint32_t lds, const Sources &src, uint32_t g0,
+                                           int lane)
+{
+    using C = Chunk<G, K, TT>;
+    // the reads of the previous chunk in this buffer have completed
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    const uint32_t cbase = g0 * (G / 4);
+#pragma unroll
+    for (int t = 0; t < K; ++t) {
+#pragma unroll
+        for (int i = 0; i < C::CODE_DMA; ++i) {
+            const int sl = i * 64 + lane;
+            const int rho = sl / C::SLOTS;
+            const int k = sl % C::SLOTS;
+            // lanes past row 15 fill the stage's padding (with row 0's data)
+            const uint32_t off = rho < 16 ? (uint32_t)rho * src.row_bytes + cbase +
+                                                16u * (uint32_t)(k ^ C::code_swizzle(rho))
+                                          : 0u;
+            dma_x4(src.codes, t * src.code_plane, lds + t * C::CODE_BYTES + i * 1024, off);
+        }
+    }
+    // scales and zero-points: lane l -> row l / CG, group g0 + l % CG (lanes
+    // past row 15 fill the padding with group 0)
+    const int prow = lane / C::CG;
+    const uint32_t gi = prow < 16 ? (uint32_t)prow * src.gpr + g0 + (uint32_t)(lane % C::CG) : 0u;
+#pragma unroll
+    for (int t = 0; t < K; ++t) {
+        if (src.scale_type == kScaleF32)
+            dma_dword(src.scales, t * src.scale_plane, lds + C::SCALES + t * C::PARAM_BYTES, gi * 4);
+        else
+            dma_ushort(src.scales, t * src.scale_plane, lds + C::SCALES + t * C::PARAM_BYTES, gi * 2);
+        // symmetric stages: a zero-sized descriptor, the loads read zeros
+        dma_dword(src.zeros, t * src.zero_plane, lds + C::ZEROS + t * C::PARAM_BYTES, gi * 4);
+    }
+    const uint32_t xbase = g0 * (G * 2);
+#pragma unroll
+    for (int i = 0; i < C::X_DMA; ++i) {
+        const int sl = i * 64 + lane;
+        const int tk = sl / C::X_SLOTS;
+        const int pc = sl % C::X_SLOTS;
+        const uint32_t off = ((uint32_t)tk < src.m_here ? 0u : kSkip) + (uint32_t)tk * src.x_row +
+                             xbase + 16u * (uint32_t)(pc ^ C::x_swizzle(tk));
+        dma_x4(src.x, 0u, lds + C::XOFF + i * 1024, off);
+    }
+}
+
+// Lane layout (lane l: A row / B column r = l % 16, k-slice j = l / 16).
+// A group's 128 / 64 / 32 inputs form 4 / 2 / 1 MFMA blocks:
+//   G = 128: lane j takes code words 2j, 2j + 1 of the group; block b takes
+//            word 2j + b / 2, half b % 2.
+//   G = 64:  lane j takes word j; block b takes its half b.
 //   G = 32:  lanes j = 2w, 2w + 1 share word w; block 0 takes half j % 2.
 // Half h of a word holds the element pairs (p, p + 8), p = 4h .. 4h + 3.
-template <int G>
-struct LaneMap {
-    static constexpr int NB = G / 32;
-    static constexpr int WL = G == 128 ? 2 : 1;        // words loaded per lane
-    static constexpr int XD = G == 32 ? 4 : 8 * WL;    // activation dwords per lane
-};
-
-template <int G, int K>
-struct GroupLoads {
-    uint32_t w[K][LaneMap<G>::WL];        // code words, per stage
-    uint32_t x[LaneMap<G>::XD];           // activations (bfloat16 pairs)
-};
-
-// A group at or past g_end (the next wave's, or past the row) is not fetched:
-// its offsets are moved 2^31 bytes up, past every resource's size (all are
-// below 2^28 bytes), so the loads return zeros without touching memory.
-// Token lanes past the tile's last token skip their activation loads.
-template <int G, int K>
-__device__ __forceinline__ void load_group(GroupLoads<G, K> &d, int64_t g, int64_t g_end,
-                                           rsrc_t rx, uint32_t tok_off, bool tok_live,
-                                           const rsrc_t (&rc)[K], uint32_t row_word_off,
-                                           int j)
+//
+// Adds the first n_groups groups (1..CG, wave-uniform) of the chunk in the
+// LDS buffer lds to acc; the lane's A row is token tk of the tile.
+template <int G, int K, int TT>
+__device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int r, int j, int tk,
+                                              int scale_type, bool sym, uint32_t mask,
+                                              uint32_t one, f32x4 &acc)
 {
-    constexpr int WPG = G / 16;
-    const uint32_t skip = g < g_end ? 0u : 0x80000000u;
-    // first word of this lane within the group, and its first input
-    const int w0 = G == 128 ? 2 * j : G == 64 ? j : (j >> 1);
-    const uint32_t word_off = skip + row_word_off + (uint32_t)(g * WPG + w0) * 4;
-#pragma unroll
-    for (int t = 0; t < K; ++t) {
-        if constexpr (G == 128) {
-            const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rc[t], word_off, 0, 0);
-            d.w[t][0] = v[0];
-            d.w[t][1] = v[1];
-        } else {
-            d.w[t][0] = __builtin_amdgcn_raw_buffer_load_b32(rc[t], word_off, 0, 0);
-        }
-    }
-    const uint32_t in0 = (uint32_t)(g * G) + 16 * w0;
-    const uint32_t xoff = skip + tok_off + in0 * 2;
-#pragma unroll
-    for (int i = 0; i < LaneMap<G>::XD; ++i) d.x[i] = 0u;
-    if (tok_live) {
-        if constexpr (G == 32) {
-            // only this lane's half: inputs 4h .. 4h + 3 and 8 + 4h .. 8 + 4h + 3
-            const uint32_t h = (uint32_t)(j & 1);
-            const u32x2 a = __builtin_amdgcn_raw_buffer_load_b64(rx, xoff + 8 * h, 0, 0);
-            const u32x2 b = __builtin_amdgcn_raw_buffer_load_b64(rx, xoff + 16 + 8 * h, 0, 0);
-            d.x[0] = a[0]; d.x[1] = a[1]; d.x[2] = b[0]; d.x[3] = b[1];
-        } else {
-#pragma unroll
-            for (int q = 0; q < LaneMap<G>::XD / 4; ++q) {
-                const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff + 16 * q, 0, 0);
-                d.x[4 * q] = v[0]; d.x[4 * q + 1] = v[1]; d.x[4 * q + 2] = v[2]; d.x[4 * q + 3] = v[3];
-            }
-        }
-    }
-}
-
-// Package stage format (values of the C ABI's enums).
-constexpr int kZpSymmetric = 2;
-constexpr int kScaleF32 = 0, kScaleF16 = 1;
-
-// Scales and zero-points of groups g, g + 1, as binary32 (one load each per
-// stage): 16-bit scales are widened, symmetric stages have z = 2. gi is the
-// group's index within the row tile's plane segment.
-template <int K>
-__device__ __forceinline__ void load_sz(u32x2 (&s)[K], u32x2 (&z)[K], int64_t g, int64_t g_end,
-                                        const rsrc_t (&rs)[K], const rsrc_t (&rz)[K],
-                                        uint32_t row_group, int scale_type, bool sym)
-{
-    const uint32_t skip = g < g_end ? 0u : 0x80000000u;
-    const uint32_t gi = row_group + (uint32_t)g;     // group index within the row tile
-#pragma unroll
-    for (int t = 0; t < K; ++t) {
-        if (scale_type == kScaleF32) {
-            s[t] = __builtin_amdgcn_raw_buffer_load_b64(rs[t], skip + gi * 4, 0, 0);
-        } else {
-            // two 16-bit scales (2-byte aligned: a row may start at an odd group)
-            const uint16_t b0 = __builtin_amdgcn_raw_buffer_load_b16(rs[t], skip + gi * 2, 0, 0);
-            const uint16_t b1 = __builtin_amdgcn_raw_buffer_load_b16(rs[t], skip + gi * 2 + 2, 0, 0);
-            if (scale_type == kScaleF16) {
-                s[t][0] = __float_as_uint((float)__builtin_bit_cast(_Float16, b0));
-                s[t][1] = __float_as_uint((float)__builtin_bit_cast(_Float16, b1));
-            } else {
-                s[t][0] = (uint32_t)b0 << 16;
-                s[t][1] = (uint32_t)b1 << 16;
-            }
-        }
-        if (sym) {
-            z[t][0] = z[t][1] = __float_as_uint(2.0f);
-        } else {
-            z[t] = __builtin_amdgcn_raw_buffer_load_b64(rz[t], skip + gi * 4, 0, 0);
-        }
-    }
-}
-
-// One group's contribution to the lane's 4 outputs: Sx, then per stage P and
-// acc += 4 s P - s (4 + z) Sx.
-template <int G, int K>
-__device__ __forceinline__ void compute_group(const GroupLoads<G, K> &d, const float (&s)[K],
-                                              const float (&z)[K], int j, f32x4 &acc)
-{
+    using C = Chunk<G, K, TT>;
+    constexpr int CG = C::CG;
     constexpr int NB = G / 32;
-    const u32x4 ones = {kOnePair, kOnePair, kOnePair, kOnePair};
-    u32x4 a[NB];
-    if constexpr (G == 32) {
-        a[0] = act_operand((u32x2){d.x[0], d.x[1]}, (u32x2){d.x[2], d.x[3]});
-    } else {
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            // word b / 2 of the lane (G = 128) or its only word (G = 64), half b % 2
-            const int base = (G == 128 ? 8 * (b >> 1) : 0) + 2 * (b & 1);
-            a[b] = act_operand((u32x2){d.x[base], d.x[base + 1]},
-                               (u32x2){d.x[base + 4], d.x[base + 5]});
-        }
-    }
-    f32x4 sx = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int b = 0; b < NB; ++b) sx = mfma(a[b], ones, sx);
+    const u32x4 ones = {one, one, one, one};
+    // scales and zero-points of the lane's row, widened to binary32
+    float sc[K][CG], zc[K][CG];
 #pragma unroll
     for (int t = 0; t < K; ++t) {
-        f32x4 p = {0.f, 0.f, 0.f, 0.f};
+        uint32_t sv[CG], zv[CG];
+        if constexpr (CG == 4) {
+            const u32x4 a = *reinterpret_cast<const u32x4 *>(lds + C::SCALES + t * C::PARAM_BYTES + 16 * r);
+            const u32x4 b = *reinterpret_cast<const u32x4 *>(lds + C::ZEROS + t * C::PARAM_BYTES + 16 * r);
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            uint32_t word;
-            int h;
-            if constexpr (G == 128) { word = d.w[t][b >> 1]; h = b & 1; }
-            else if constexpr (G == 64) { word = d.w[t][0]; h = b; }
-            else { word = d.w[t][0]; h = j & 1; }
-            p = mfma(a[b], code_operand(h ? word >> 8 : word), p);
+            for (int q = 0; q < CG; ++q) { sv[q] = a[q]; zv[q] = b[q]; }
+        } else {
+            const u32x2 a = *reinterpret_cast<const u32x2 *>(lds + C::SCALES + t * C::PARAM_BYTES + 8 * r);
+            const u32x2 b = *reinterpret_cast<const u32x2 *>(lds + C::ZEROS + t * C::PARAM_BYTES + 8 * r);
+#pragma unroll
+            for (int q = 0; q < CG; ++q) { sv[q] = a[q]; zv[q] = b[q]; }
         }
-        // s (sum x Q - z Sx) = 4 s P - s (4 + z) Sx
-        const float s4 = 4.0f * s[t];
-        const float scz = s[t] * (4.0f + z[t]);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
-            acc[i] = __builtin_fmaf(-scz, sx[i], acc[i]);
+        for (int q = 0; q < CG; ++q) {
+            sc[t][q] = scale_type == kScaleF32 ? __uint_as_float(sv[q])
+                       : scale_type == kScaleF16
+                           ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sv[q] & 0xFFFFu))
+                           : __uint_as_float(sv[q] << 16);
+            zc[t][q] = sym ? 2.0f : __uint_as_float(zv[q]);
+        }
+    }
+    const char *xl = lds + C::XOFF + tk * C::X_ROW;
+    const int xs = C::x_swizzle(tk);
+    const int cs = C::code_swizzle(r);
+#pragma unroll
+    for (int q = 0; q < CG; ++q) {
+        if (q >= n_groups) break;
+        // activations of the lane's token and k-slice
+        u32x4 a[NB];
+        if constexpr (G == 128) {
+            uint32_t x[16];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const u32x4 d = *reinterpret_cast<const u32x4 *>(xl + 16 * ((q * 16 + 4 * j + v) ^ xs));
+                x[4 * v] = d[0]; x[4 * v + 1] = d[1]; x[4 * v + 2] = d[2]; x[4 * v + 3] = d[3];
+            }
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int base = 8 * (b >> 1) + 2 * (b & 1);
+                a[b] = act_operand((u32x2){x[base], x[base + 1]}, (u32x2){x[base + 4], x[base + 5]});
+            }
+        } else if constexpr (G == 64) {
+            uint32_t x[8];
+#pragma unroll
+            for (int v = 0; v < 2; ++v) {
+                const u32x4 d = *reinterpret_cast<const u32x4 *>(xl + 16 * ((q * 8 + 2 * j + v) ^ xs));
+                x[4 * v] = d[0]; x[4 * v + 1] = d[1]; x[4 * v + 2] = d[2]; x[4 * v + 3] = d[3];
+            }
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+                a[b] = act_operand((u32x2){x[2 * b], x[2 * b + 1]}, (u32x2){x[2 * b + 4], x[2 * b + 5]});
+        } else {
+            // inputs 16 w + 4h .. + 3 and 16 w + 8 + 4h .. + 3 of the group,
+            // w = j / 2, h = j % 2: 8 bytes at 8h in pieces 2w and 2w + 1
+            const int piece = q * 4 + 2 * (j >> 1);
+            const int h8 = 8 * (j & 1);
+            const u32x2 lo = *reinterpret_cast<const u32x2 *>(xl + 16 * (piece ^ xs) + h8);
+            const u32x2 hi = *reinterpret_cast<const u32x2 *>(xl + 16 * ((piece + 1) ^ xs) + h8);
+            a[0] = act_operand(lo, hi);
+        }
+        f32x4 sx = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int b = 0; b < NB; ++b) sx = mfma(a[b], ones, sx);
+#pragma unroll
+        for (int t = 0; t < K; ++t) {
+            const char *row = lds + t * C::CODE_BYTES + r * C::RB;
+            f32x4 pq = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (G == 128) {
+                const u32x2 w = *reinterpret_cast<const u32x2 *>(
+                    row + 16 * ((2 * q + (j >> 1)) ^ cs) + 8 * (j & 1));
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    const uint32_t word = w[b >> 1];
+                    pq = mfma(a[b], code_operand((b & 1) ? word >> 8 : word, mask, one), pq);
+                }
+            } else if constexpr (G == 64) {
+                const uint32_t word = *reinterpret_cast<const uint32_t *>(row + 16 * (q ^ cs) + 4 * j);
+#pragma unroll
+                for (int b = 0; b < NB; ++b)
+                    pq = mfma(a[b], code_operand(b ? word >> 8 : word, mask, one), pq);
+            } else {
+                const uint32_t word = *reinterpret_cast<const uint32_t *>(
+                    row + 16 * ((q >> 1) ^ cs) + 8 * (q & 1) + 4 * (j >> 1));
+                pq = mfma(a[0], code_operand((j & 1) ? word >> 8 : word, mask, one), pq);
+            }
+            // s (sum x Q - z Sx) = 4 s P - s (4 + z) Sx
+            const float s4 = 4.0f * sc[t][q];
+            const float scz = sc[t][q] * (4.0f + zc[t][q]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc[i] = __builtin_fmaf(s4, pq[i], acc[i]);
+                acc[i] = __builtin_fmaf(-scz, sx[i], acc[i]);
+            }
         }
     }
 }
 
-template <int G, int K>
+template <int G, int K, int TT>
 __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int64_t n_tokens,
     float *__restrict__ Y, int zero_point, int scale_type)
 {
-    constexpr int NW = kLinearThreads / 64;
-    const bool sym = zero_point == kZpSymmetric;
-    const uint32_t sbytes = scale_type == kScaleF32 ? 4 : 2;
-    __shared__ f32x4 red[NW][64];
+    using C = Chunk<G, K, TT>;
+    constexpr int CG = C::CG;
+    // two chunk buffers per wave
+    __shared__ __attribute__((aligned(16))) char buf[2][kWaves][C::BYTES];
+    __shared__ f32x4 red[kWaves][64];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15;            // B column (output row) and A row (token)
-    const int j = lane >> 4;            // input slice
+    const int j = lane >> 4;            // k-slice
+    const int tk = r < TT ? r : TT - 1; // A rows past the tile repeat its last token
+    // the code operand's constants in registers (opaque to constant folding,
+    // so that the AND and OR fuse)
+    uint32_t mask, one;
+    asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
+    asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
 
     const int64_t o0 = (int64_t)blockIdx.x * 16;
     const uint32_t rows_here = (uint32_t)(rows - o0 < 16 ? rows - o0 : 16);
     const int64_t gpr = cols / G;       // groups per row
     const int64_t wpr = cols / 16;      // code words per row
-    // This wave's contiguous range of groups (an even count, so that scales
-    // and zero-points come in pairs of groups).
-    const int64_t per_wave = ((gpr + NW - 1) / NW + 1) & ~int64_t(1);
+    // This wave's contiguous range of groups, a whole number of chunks.
+    const int64_t per_wave = ((gpr + kWaves - 1) / kWaves + CG - 1) / CG * CG;
     const int64_t g_begin = per_wave * wave < gpr ? per_wave * wave : gpr;
     const int64_t g_end = g_begin + per_wave < gpr ? g_begin + per_wave : gpr;
+    const int n_chunks = (int)((g_end - g_begin + CG - 1) / CG);
 
-    // Package resources of this row tile, one per stage (rows past the end
-    // read zero codes and zero scales).
-    rsrc_t rc[K], rs[K], rz[K];
-#pragma unroll
-    for (int t = 0; t < K; ++t) {
-        rc[t] = make_rsrc(codes + t * plane_words + o0 * wpr, rows_here * (uint32_t)wpr * 4);
-        rs[t] = make_rsrc(scales + (t * plane_groups + o0 * gpr) * sbytes,
-                          rows_here * (uint32_t)gpr * sbytes);
-        rz[t] = make_rsrc(zeros + t * plane_groups + o0 * gpr, rows_here * (uint32_t)gpr * 4);
-    }
-    const uint32_t row_word_off = (uint32_t)(r * wpr) * 4;
-    const uint32_t row_group = (uint32_t)(r * gpr);
+    // Package buffers of this row tile (rows past the end read zero).
+    Sources src;
+    const uint32_t sbytes = scale_type == kScaleF32 ? 4 : 2;
+    src.code_plane = (uint32_t)plane_words * 4;
+    src.scale_plane = (uint32_t)plane_groups * sbytes;
+    src.zero_plane = (uint32_t)plane_groups * 4;
+    src.codes = make_desc(codes + o0 * wpr,
+                          (K - 1) * src.code_plane + rows_here * (uint32_t)wpr * 4);
+    src.scales = make_desc(scales + o0 * gpr * sbytes,
+                           (K - 1) * src.scale_plane + rows_here * (uint32_t)gpr * sbytes);
+    src.sym = zero_point == kZpSymmetric;
+    src.zeros = make_desc(src.sym ? nullptr : zeros + o0 * gpr,
+                          src.sym ? 0u : (K - 1) * src.zero_plane + rows_here * (uint32_t)gpr * 4);
+    src.row_bytes = (uint32_t)wpr * 4;
+    src.gpr = (uint32_t)gpr;
+    src.x_row = (uint32_t)cols * 2;
+    src.scale_type = scale_type;
+    const uint32_t lds_a = (uint32_t)reinterpret_cast<uintptr_t>(
+        (__attribute__((address_space(3))) char *)&buf[0][wave][0]);
+    const uint32_t lds_b = (uint32_t)reinterpret_cast<uintptr_t>(
+        (__attribute__((address_space(3))) char *)&buf[1][wave][0]);
+    const char *la = &buf[0][wave][0];
+    const char *lb = &buf[1][wave][0];
 
-    for (int64_t m0 = 0; m0 < n_tokens; m0 += 16) {
-        const uint32_t m_here = (uint32_t)(n_tokens - m0 < 16 ? n_tokens - m0 : 16);
-        const rsrc_t rx = make_rsrc(X + m0 * cols, m_here * (uint32_t)cols * 2);
-        const uint32_t tok_off = (uint32_t)(r * cols) * 2;
-        const bool tok_live = (uint32_t)r < m_here;
+    for (int64_t m0 = 0; m0 < n_tokens; m0 += TT) {
+        src.m_here = (uint32_t)(n_tokens - m0 < TT ? n_tokens - m0 : TT);
+        src.x = make_desc(X + m0 * cols, src.m_here * src.x_row);
 
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        // Groups in pairs; the loads of the next group are issued before the
-        // current one is computed.
-        GroupLoads<G, K> cur, nxt;
-        u32x2 s2[K], z2[K];
-        load_group<G, K>(cur, g_begin, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
-        load_sz<K>(s2, z2, g_begin, g_end, rs, rz, row_group, scale_type, sym);
-        for (int64_t g = g_begin; g < g_end; g += 2) {
-            float s[K], z[K];
-            load_group<G, K>(nxt, g + 1, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
-#pragma unroll
-            for (int t = 0; t < K; ++t) { s[t] = __uint_as_float(s2[t][0]); z[t] = __uint_as_float(z2[t][0]); }
-            compute_group<G, K>(cur, s, z, j, acc);
-            if (g + 1 >= g_end) break;
-#pragma unroll
-            for (int t = 0; t < K; ++t) { s[t] = __uint_as_float(s2[t][1]); z[t] = __uint_as_float(z2[t][1]); }
-            load_group<G, K>(cur, g + 2, g_end, rx, tok_off, tok_live, rc, row_word_off, j);
-            load_sz<K>(s2, z2, g + 2, g_end, rs, rz, row_group, scale_type, sym);
-            compute_group<G, K>(nxt, s, z, j, acc);
+        const uint32_t g0 = (uint32_t)g_begin;
+        if (n_chunks > 0) load_chunk<G, K, TT>(lds_a, src, g0, lane);
+        if (n_chunks > 1) load_chunk<G, K, TT>(lds_b, src, g0 + CG, lane);
+        for (int c = 0; c < n_chunks; c += 2) {
+            const uint32_t ga = g0 + (uint32_t)c * CG;
+            const int na = (int)(g_end - ga < CG ? g_end - ga : CG);
+            // chunk c is in buffer a; chunk c + 1, if any, may stay in flight
+            if (c + 1 < n_chunks) wait_vm<C::DMA>(); else wait_vm<0>();
+            compute_chunk<G, K, TT>(la, na, r, j, tk, scale_type, src.sym, mask, one, acc);
+            if (c + 2 < n_chunks) load_chunk<G, K, TT>(lds_a, src, ga + 2 * CG, lane);
+            if (c + 1 >= n_chunks) break;
+            const uint32_t gb = ga + CG;
+            const int nb = (int)(g_end - gb < CG ? g_end - gb : CG);
+            if (c + 2 < n_chunks) wait_vm<C::DMA>(); else wait_vm<0>();
+            compute_chunk<G, K, TT>(lb, nb, r, j, tk, scale_type, src.sym, mask, one, acc);
+            if (c + 3 < n_chunks) load_chunk<G, K, TT>(lds_b, src, gb + 2 * CG, lane);
         }
 
         // Sum the waves' partial results in wave order and store: lane l
         // holds tokens m0 + 4 j + i of output row o0 + r.
         red[wave][lane] = acc;
         __syncthreads();
-        if (wave == 0) {
+        if (wave == 0 && 4 * j < TT) {
             f32x4 y = red[0][lane];
 #pragma unroll
-            for (int v = 1; v < NW; ++v) {
+            for (int v = 1; v < kWaves; ++v) {
                 const f32x4 q = red[v][lane];
                 y[0] += q[0]; y[1] += q[1]; y[2] += q[2]; y[3] += q[3];
             }
             if ((uint32_t)r < rows_here) {
-                const rsrc_t ry = make_rsrc(Y + m0 * rows, m_here * (uint32_t)rows * 4);
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    __builtin_amdgcn_raw_buffer_store_b32(
-                        __float_as_uint(y[i]), ry, (uint32_t)((4 * j + i) * rows + o0 + r) * 4, 0, 0);
+                    if ((uint32_t)(4 * j + i) < src.m_here) Y[(m0 + 4 * j + i) * rows + o0 + r] = y[i];
             }
         }
         __syncthreads();   // red is reused by the next token tile
@@ -333,22 +517,32 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-template <int G>
-hipError_t launch_linear_g(const uint32_t *codes, const char *scales, const float *zeros,
-                           int64_t rows, int64_t cols, int S, int k, int zp, int sdt,
-                           const uint16_t *X, int64_t n_tokens, float *Y, hipStream_t stream)
+template <int G, int TT>
+hipError_t launch_linear_gt(const uint32_t *codes, const char *scales, const float *zeros,
+                            int64_t rows, int64_t cols, int k, int zp, int sdt, const uint16_t *X,
+                            int64_t n_tokens, float *Y, hipStream_t stream)
 {
     const int64_t plane_words = rows * cols / 16;
     const int64_t plane_groups = rows * cols / G;
     const int grid = (int)((rows + 15) / 16);
-    (void)S;
     switch (k) {
-    case 1: return launch(linear_kernel<G, 1>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
-    case 2: return launch(linear_kernel<G, 2>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
-    case 3: return launch(linear_kernel<G, 3>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
-    case 4: return launch(linear_kernel<G, 4>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 1: return launch(linear_kernel<G, 1, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 2: return launch(linear_kernel<G, 2, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 3: return launch(linear_kernel<G, 3, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 4: return launch(linear_kernel<G, 4, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
     default: return hipErrorInvalidValue;
     }
+}
+
+// Up to 4 tokens: one pass with 4-token tiles; more: 16-token tiles.
+template <int G>
+hipError_t launch_linear_g(const uint32_t *codes, const char *scales, const float *zeros,
+                           int64_t rows, int64_t cols, int k, int zp, int sdt, const uint16_t *X,
+                           int64_t n_tokens, float *Y, hipStream_t stream)
+{
+    if (n_tokens <= 4)
+        return launch_linear_gt<G, 4>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
+    return launch_linear_gt<G, 16>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
 }
 
 }  // namespace
@@ -359,10 +553,11 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
                          hipStream_t stream)
 {
     const char *sc = static_cast<const char *>(scales);
+    (void)S;
     switch (G) {
-    case 32: return launch_linear_g<32>(codes, sc, zeros, rows, cols, S, k, zero_point, scale_type, X, n_tokens, Y, stream);
-    case 64: return launch_linear_g<64>(codes, sc, zeros, rows, cols, S, k, zero_point, scale_type, X, n_tokens, Y, stream);
-    case 128: return launch_linear_g<128>(codes, sc, zeros, rows, cols, S, k, zero_point, scale_type, X, n_tokens, Y, stream);
+    case 32: return launch_linear_g<32>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, n_tokens, Y, stream);
+    case 64: return launch_linear_g<64>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, n_tokens, Y, stream);
+    case 128: return launch_linear_g<128>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, n_tokens, Y, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -226,6 +226,8 @@ def _linear_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128
     (dict(M=0), rrq.RRQ_ERR_SHAPE),
     (dict(rows=1 << 26), rrq.RRQ_ERR_SHAPE),
     (dict(cols=1 << 27), rrq.RRQ_ERR_SHAPE),
+    # 4 stage planes of (2^17 x 2^17) / 4 bytes = 4 GiB of codes
+    (dict(rows=1 << 17, cols=1 << 17, k=4), rrq.RRQ_ERR_SHAPE),
     (dict(X=FAKE + 8), rrq.RRQ_ERR_ALIGN),
     (dict(codes=FAKE + 4), rrq.RRQ_ERR_ALIGN),
     (dict(Y=FAKE + 2), rrq.RRQ_ERR_ALIGN),

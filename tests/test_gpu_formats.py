@@ -143,7 +143,8 @@ def test_linear_in_format(gpu, zp, sd):
         ref = npo.linear(oc, sv, oz, rows, cols, G, k, xb)
         A = sum(T @ (np.abs(sv[t].astype(np.float64)) * (11 + np.abs(oz[t].astype(np.float64)))).reshape(rows, cols // G).T
                 for t in range(k))
-        n = k * (math.ceil((cols // G) / 8) + 1)
+        p = cols // G
+        n = k * (min(p, 4 * math.ceil(p / 16)) + 1)
         tol = 1.05 * U * A * (G + 2 * n + 24) + 1e-300
         err = np.abs(Y.cpu().numpy().astype(np.float64) - ref)
         assert np.all(err <= tol), f"k={k}: {np.max(err / tol)}"

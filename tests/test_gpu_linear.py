@@ -38,7 +38,8 @@ def _bound(codes, s, z, rows, cols, G, k, x_bits):
     for t in range(k):
         w = (np.abs(s[t].astype(np.float64)) * (11 + np.abs(z[t].astype(np.float64)))).reshape(rows, cols // G)
         A += T @ w.T
-    n = k * (math.ceil((cols // G) / 8) + 1)
+    p = cols // G
+    n = k * (min(p, 4 * math.ceil(p / 16)) + 1)
     return 1.05 * U * A * (G + 2 * n + 24) + 1e-300
 
 
@@ -160,3 +161,36 @@ def test_qwen3_layer_every_projection(gpu):
         _log(f"{t.name}: ok")
     del Wf
     torch.cuda.empty_cache()
+
+
+def test_graph_replay_matches_eager(gpu):
+    """rrq_linear captured in a HIP graph: every replay (with eager work and
+    synchronisations between them) gives the eager result bit for bit."""
+    import torch
+    rows, cols, G, S = 80, 512, 128, 4
+    codes, s, z = _realistic(rows, cols, G, S, 77)
+    rng = np.random.default_rng(5)
+    xb = npo.f32_to_bf16_bits(rng.standard_normal((3, cols)).astype(np.float32))
+    c_d = torch.from_numpy(codes.view(np.int32).copy()).cuda()
+    s_d = torch.from_numpy(s.copy()).cuda()
+    z_d = torch.from_numpy(z.copy()).cuda()
+    X = torch.from_numpy(xb.view(np.int16).reshape(3, cols).copy()).cuda()
+    Y_eager = torch.empty((3, rows), dtype=torch.float32, device="cuda")
+    gpu.rrq_linear(c_d, s_d, z_d, rows, cols, G, S, 3, X, 3, Y_eager)
+    torch.cuda.synchronize()
+    Y = torch.full((3, rows), float("nan"), dtype=torch.float32, device="cuda")
+    cs = torch.cuda.Stream()
+    cs.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=cs):
+        gpu.rrq_linear(c_d, s_d, z_d, rows, cols, G, S, 3, X, 3, Y, cs)
+    torch.cuda.current_stream().wait_stream(cs)
+    for i in range(3):
+        Y.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y, Y_eager), i
+        # eager work between replays
+        gpu.rrq_linear(c_d, s_d, z_d, rows, cols, G, S, 1 + i % 3, X, 2, Y_eager[:2])
+        gpu.rrq_linear(c_d, s_d, z_d, rows, cols, G, S, 3, X, 3, Y_eager)
+        torch.cuda.synchronize()
