@@ -36,8 +36,6 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
                          int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
                          hipStream_t stream);
 
-// Linear layer: threads per workgroup (4 waves sharing 16 output rows).
-constexpr int kLinearThreads = 256;
 // rows and cols of the linear kernel stay below this bound, so its 32-bit
 // buffer sizes and offsets (at most 16 * rows * 4 bytes) cannot wrap.
 constexpr int64_t kLinearMaxDim = int64_t(1) << 26;

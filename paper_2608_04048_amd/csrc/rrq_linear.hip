@@ -10,34 +10,33 @@
 //   * B operand: 32 inputs x 16 output rows of codes, each code Q encoded as
 //     the bfloat16 1 + Q/4 (bits 0x3F80 | Q << 5: the code lands in the top
 //     two mantissa bits with one shift and one AND-OR per pair of codes), so
-//     the MFMA yields P = sum x (1 + Q/4) and sum x Q = 4 P - 4 Sx exactly in
-//     real arithmetic;
+//     the MFMA yields P_t = sum x (1 + Q/4) and sum x Q = 4 P_t - 4 Sx
+//     exactly in real arithmetic;
 //   * Sx = sum x over the group comes from the same MFMA with a B operand of
 //     bfloat16 ones.
-// The group's contribution s (4 P - (4 + z) Sx) is added to the lane's fp32
-// accumulators with two fused multiply-adds. Every product of the MFMAs is
-// exact; fp32 rounding enters only in the accumulations (error bound in the
-// tests).
+// The group's contribution sum_t s_t (4 P_t - (4 + z_t) Sx) is added to the
+// lane's fp32 accumulators as sum_t (4 s_t) P_t (one fused multiply-add per
+// output and stage) minus c Sx with c = sum_t s_t (4 + z_t) (one per output
+// and group). Every product of the MFMAs is exact; fp32 rounding enters only
+// in the accumulations (error bound in the tests).
 //
-// Work split: a workgroup of 4 waves owns 16 output rows; the groups of a
-// row are split into 4 contiguous ranges, one per wave, and each wave walks
-// its range in chunks of groups. The partial results are summed through
+// Work split: a workgroup of NW waves owns 16 output rows; the groups of a
+// row are split into NW contiguous ranges, one per wave, and each wave walks
+// its range in chunks of 2 groups. The partial results are summed through
 // LDS in wave order (deterministic). Up to 4 tokens are served by one pass
-// over the package (chunks of 4 groups); more tokens go 16 at a time
-// (chunks of 2 groups, so that a chunk's activations fit the same LDS).
+// over the package with 8 waves per workgroup; more tokens go 16 at a time
+// with 4 waves (a chunk's activations take 4 times the LDS).
 //
 // Memory path: everything a chunk needs (codes of 16 rows per stage, scales
-// and zero-points, activations of the tile's tokens) goes
-// from memory straight into LDS with LDS-DMA buffer loads, the code loads
-// covering whole 128-byte runs of a row (8 rows per instruction for
-// G = 128), and is read back in the MFMA operand layout. Every wave
-// double-buffers its chunks, so the next chunk is in flight while the
-// current one is computed. The DMA instructions are issued from inline
-// assembly, a fixed number per chunk, and the wave waits for exactly the
-// chunk it is about to read (s_waitcnt vmcnt(n) with n = one chunk's
-// instructions); no other vector-memory loads are issued in the loop. LDS
-// slots are XOR-swizzled so that the reads of 16 rows (or 4 tokens) fall in
-// distinct banks.
+// and zero-points, activations of the tile's tokens) goes from memory
+// straight into LDS with LDS-DMA buffer loads and is read back in the MFMA
+// operand layout. Every wave double-buffers its chunks, so the next chunk is
+// in flight while the current one is computed. The DMA instructions are
+// issued from inline assembly, a fixed number per chunk, and the wave waits
+// for exactly the chunk it is about to read (s_waitcnt vmcnt(n) with n = one
+// chunk's instructions); no other vector-memory loads are issued in the
+// loop. LDS slots are XOR-swizzled so that the reads of 16 rows (or of the
+// tile's tokens) fall in distinct banks.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -59,33 +58,26 @@ constexpr uint32_t kCodeMask = 0x00600060u;   // top two mantissa bits of both h
 // activation buffer's size (below 2^30 bytes), so it reads zeros.
 constexpr uint32_t kSkip = 0x80000000u;
 
-constexpr int kWaves = kLinearThreads / 64;
-
 // Package stage format (values of the C ABI's enums).
 constexpr int kZpSymmetric = 2;
 constexpr int kScaleF32 = 0, kScaleF16 = 1;
 
-// A pass over the package serves a tile of TT tokens: TT = 4 (decode, up to
-// 4 tokens) walks the groups in chunks of 4, TT = 16 in chunks of 2, so that
-// a chunk's activations fit the same LDS budget.
-//
-// LDS image of one chunk (per wave and buffer), in 16-byte slots:
-//   codes   K stages x 16 rows x RB bytes (CG groups of G / 4 bytes; a stage
-//           takes at least the 1 KiB one DMA instruction writes),
-//   scales  K stages x 16 rows x CG groups, one dword each (a stage takes
+// Waves per workgroup for a token tile of TT.
+constexpr int tile_waves(int TT) { return TT == 4 ? 8 : 4; }
+
+// LDS image of one chunk of 2 groups (per wave and buffer), in 16-byte
+// slots:
+//   codes   K stages x 16 rows x RB = G / 2 bytes (a stage takes at least
+//           the 1 KiB one DMA instruction writes),
+//   scales  K stages x 16 rows x 2 groups, one dword each (a stage takes
 //           the 256 bytes one dword DMA writes),
 //   zeros   the same,
-//   X       TT tokens x CG G inputs x 2 bytes (whole KiB: the DMA
-//           lanes past the last token read zeros into the padding).
-// Groups per chunk.
-constexpr int chunk_groups(int G, int K, int TT)
-{
-    return (void)G, (void)K, TT == 4 ? 4 : 2;
-}
-
+//   X       TT tokens x 2 G inputs x 2 bytes (whole KiB: the DMA lanes past
+//           the last token read zeros into the padding).
 template <int G, int K, int TT>
 struct Chunk {
-    static constexpr int CG = chunk_groups(G, K, TT);
+    static constexpr int NW = tile_waves(TT);
+    static constexpr int CG = 2;                                  // groups per chunk
     static constexpr int RB = CG * G / 4;                         // code bytes per row
     static constexpr int SLOTS = RB / 16;                         // code slots per row
     static constexpr int CODE_BYTES = 16 * RB > 1024 ? 16 * RB : 1024;
@@ -96,7 +88,7 @@ struct Chunk {
     static constexpr int XOFF = ZEROS + K * PARAM_BYTES;
     static constexpr int X_ROW = CG * G * 2;                      // one token
     static constexpr int X_SLOTS = X_ROW / 16;
-    static constexpr int X_DMA = (TT * X_ROW + 1023) / 1024;     // whole KiB (padding reads zeros)
+    static constexpr int X_DMA = (TT * X_ROW + 1023) / 1024;
     static constexpr int BYTES = XOFF + X_DMA * 1024;
     // DMA instructions per chunk: what one wait leaves in flight
     static constexpr int DMA = K * (CODE_DMA + 2) + X_DMA;
@@ -110,15 +102,14 @@ struct Chunk {
         return SLOTS > 1 ? (r * RB / 256) & (SLOTS - 1) : 0;
     }
     // Slot p of token row tk holds piece p ^ x_swizzle(tk): token rows that
-    // share banks get different slots (4 tokens: rows are a multiple of 256
-    // bytes long; 16 tokens: 16 distinct patterns where the row has them).
+    // share banks get different slots where the row has enough of them.
     static __device__ __forceinline__ int x_swizzle(int tk)
     {
         return (TT == 4 ? 4 * tk : tk) & (X_SLOTS - 1);
     }
 };
 
-// Raw buffer descriptor (gfx9 family): accesses beyond bytes read zero.
+// Raw buffer descriptor (gfx9 family): accesses at or beyond bytes read zero.
 __device__ __forceinline__ u32x4 make_desc(const void *base, uint32_t bytes)
 {
     const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -133,10 +124,10 @@ __device__ __forceinline__ u32x4 make_desc(const void *base, uint32_t bytes)
 // LDS-DMA loads: every lane reads from the buffer at byte offset
 // soff + voff (both range-checked against the descriptor's size) and the
 // wave writes LDS at lds + lane * 16 (dwordx4) or lds + lane * 4 (dword,
-// ushort). lds is a wave-uniform LDS byte address. m0, which
-// carries it, is restored. The wait states the compiler cannot see inside
-// the block are explicit: 5 before the load reads SGPRs that a VALU
-// instruction may have just written (spill reloads), 1 after writing m0.
+// ushort). lds is a wave-uniform LDS byte address. m0, which carries it, is
+// restored. The wait states the compiler cannot see inside the block are
+// explicit: 5 before the load reads SGPRs that a VALU instruction may have
+// just written, 1 after writing m0.
 __device__ __forceinline__ void dma_x4(const u32x4 &desc, uint32_t soff, uint32_t lds,
                                        uint32_t voff)
 {
@@ -151,7 +142,7 @@ __device__ __forceinline__ void dma_x4(const u32x4 &desc, uint32_t soff, uint32_
 }
 
 __device__ __forceinline__ void dma_dword(const u32x4 &desc, uint32_t soff, uint32_t lds,
-                                       uint32_t voff)
+                                          uint32_t voff)
 {
     uint32_t m0;
     asm volatile("s_nop 4\n\t"
@@ -164,7 +155,7 @@ __device__ __forceinline__ void dma_dword(const u32x4 &desc, uint32_t soff, uint
 }
 
 __device__ __forceinline__ void dma_ushort(const u32x4 &desc, uint32_t soff, uint32_t lds,
-                                       uint32_t voff)
+                                           uint32_t voff)
 {
     uint32_t m0;
     asm volatile("s_nop 4\n\t"
@@ -204,6 +195,21 @@ __device__ __forceinline__ u32x4 code_operand(uint32_t w, uint32_t mask, uint32_
     return b;
 }
 
+// The same for both halves of two words at once (G = 128: the lane's two
+// words of a group), with 64-bit shifts: the bits one word's shift carries
+// into the other land outside the mask. b[h][v] is word v, half h.
+__device__ __forceinline__ void code_operands2(uint32_t w0, uint32_t w1, uint32_t mask,
+                                               uint32_t one, u32x4 (&b)[2][2])
+{
+    const uint64_t w = ((uint64_t)w1 << 32) | w0;
+    const uint64_t s[8] = {w << 5, w << 3, w << 1, w >> 1, w >> 3, w >> 5, w >> 7, w >> 9};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        b[q >> 2][0][q & 3] = ((uint32_t)s[q] & mask) | one;
+        b[q >> 2][1][q & 3] = ((uint32_t)(s[q] >> 32) & mask) | one;
+    }
+}
+
 // A operand of one block from two runs of 4 activations (inputs p0 .. p0 + 3
 // and p0 + 8 .. p0 + 11 of a 16-input word): register q = (x[p0 + q],
 // x[p0 + 8 + q]).
@@ -231,14 +237,14 @@ struct Sources {
     uint32_t x_row;       // activation bytes per token: cols * 2
     uint32_t m_here;      // live tokens of the tile
     int scale_type;
-    bool sym;
 };
 
 // Issue the DMA of the chunk whose first group is g0 into the LDS buffer
-// at byte address lds: Chunk<G, K, TT>::DMA instructions, whatever the format
-// (zero-points of symmetric stages and tokens past the tile read zeros
-// without touching memory). Code rows past the tile and inputs past the row
-// read zeros or the next row's data: those groups are never computed.
+// at byte address lds: Chunk<G, K, TT>::DMA instructions, whatever the
+// format (symmetric stages read zeros through a zero-sized descriptor,
+// tokens past the tile read zeros without touching memory). Code rows past
+// the tile and inputs past the row read zeros or other rows' data: those
+// groups are never computed.
 template <int G, int K, int TT>
 __device__ __forceinline__ void load_chunk(uint32_t lds, const Sources &src, uint32_t g0,
                                            int lane)
@@ -271,7 +277,6 @@ __device__ __forceinline__ void load_chunk(uint32_t lds, const Sources &src, uin
             dma_dword(src.scales, t * src.scale_plane, lds + C::SCALES + t * C::PARAM_BYTES, gi * 4);
         else
             dma_ushort(src.scales, t * src.scale_plane, lds + C::SCALES + t * C::PARAM_BYTES, gi * 2);
-        // symmetric stages: a zero-sized descriptor, the loads read zeros
         dma_dword(src.zeros, t * src.zero_plane, lds + C::ZEROS + t * C::PARAM_BYTES, gi * 4);
     }
     const uint32_t xbase = g0 * (G * 2);
@@ -295,8 +300,10 @@ __device__ __forceinline__ void load_chunk(uint32_t lds, const Sources &src, uin
 // Half h of a word holds the element pairs (p, p + 8), p = 4h .. 4h + 3.
 //
 // Adds the first n_groups groups (1..CG, wave-uniform) of the chunk in the
-// LDS buffer lds to acc; the lane's A row is token tk of the tile.
-template <int G, int K, int TT>
+// LDS buffer lds to acc; the lane's A row is token tk of the tile. DEF: the
+// default stage format (binary32 scales, stored zero-points), with no format
+// branches; otherwise scale_type and sym are read at run time.
+template <int G, int K, int TT, bool DEF>
 __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int r, int j, int tk,
                                               int scale_type, bool sym, uint32_t mask,
                                               uint32_t one, f32x4 &acc)
@@ -305,29 +312,29 @@ __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int
     constexpr int CG = C::CG;
     constexpr int NB = G / 32;
     const u32x4 ones = {one, one, one, one};
-    // scales and zero-points of the lane's row, widened to binary32
-    float sc[K][CG], zc[K][CG];
+    // 4 s_t and c = sum_t s_t (4 + z_t) per group of the lane's row
+    float s4[K][CG], c[CG];
+#pragma unroll
+    for (int q = 0; q < CG; ++q) c[q] = 0.0f;
 #pragma unroll
     for (int t = 0; t < K; ++t) {
-        uint32_t sv[CG], zv[CG];
-        if constexpr (CG == 4) {
-            const u32x4 a = *reinterpret_cast<const u32x4 *>(lds + C::SCALES + t * C::PARAM_BYTES + 16 * r);
-            const u32x4 b = *reinterpret_cast<const u32x4 *>(lds + C::ZEROS + t * C::PARAM_BYTES + 16 * r);
-#pragma unroll
-            for (int q = 0; q < CG; ++q) { sv[q] = a[q]; zv[q] = b[q]; }
-        } else {
-            const u32x2 a = *reinterpret_cast<const u32x2 *>(lds + C::SCALES + t * C::PARAM_BYTES + 8 * r);
-            const u32x2 b = *reinterpret_cast<const u32x2 *>(lds + C::ZEROS + t * C::PARAM_BYTES + 8 * r);
-#pragma unroll
-            for (int q = 0; q < CG; ++q) { sv[q] = a[q]; zv[q] = b[q]; }
-        }
+        const u32x2 sv = *reinterpret_cast<const u32x2 *>(lds + C::SCALES + t * C::PARAM_BYTES + 8 * r);
+        const u32x2 zv = *reinterpret_cast<const u32x2 *>(lds + C::ZEROS + t * C::PARAM_BYTES + 8 * r);
 #pragma unroll
         for (int q = 0; q < CG; ++q) {
-            sc[t][q] = scale_type == kScaleF32 ? __uint_as_float(sv[q])
-                       : scale_type == kScaleF16
-                           ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sv[q] & 0xFFFFu))
-                           : __uint_as_float(sv[q] << 16);
-            zc[t][q] = sym ? 2.0f : __uint_as_float(zv[q]);
+            float s, z;
+            if constexpr (DEF) {
+                s = __uint_as_float(sv[q]);
+                z = __uint_as_float(zv[q]);
+            } else {
+                s = scale_type == kScaleF32 ? __uint_as_float(sv[q])
+                    : scale_type == kScaleF16
+                        ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sv[q] & 0xFFFFu))
+                        : __uint_as_float(sv[q] << 16);
+                z = sym ? 2.0f : __uint_as_float(zv[q]);
+            }
+            s4[t][q] = 4.0f * s;
+            c[q] = __builtin_fmaf(s, 4.0f + z, c[q]);
         }
     }
     const char *xl = lds + C::XOFF + tk * C::X_ROW;
@@ -379,11 +386,10 @@ __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int
             if constexpr (G == 128) {
                 const u32x2 w = *reinterpret_cast<const u32x2 *>(
                     row + 16 * ((2 * q + (j >> 1)) ^ cs) + 8 * (j & 1));
+                u32x4 bop[2][2];
+                code_operands2(w[0], w[1], mask, one, bop);
 #pragma unroll
-                for (int b = 0; b < NB; ++b) {
-                    const uint32_t word = w[b >> 1];
-                    pq = mfma(a[b], code_operand((b & 1) ? word >> 8 : word, mask, one), pq);
-                }
+                for (int b = 0; b < NB; ++b) pq = mfma(a[b], bop[b & 1][b >> 1], pq);
             } else if constexpr (G == 64) {
                 const uint32_t word = *reinterpret_cast<const uint32_t *>(row + 16 * (q ^ cs) + 4 * j);
 #pragma unroll
@@ -394,20 +400,17 @@ __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int
                     row + 16 * ((q >> 1) ^ cs) + 8 * (q & 1) + 4 * (j >> 1));
                 pq = mfma(a[0], code_operand((j & 1) ? word >> 8 : word, mask, one), pq);
             }
-            // s (sum x Q - z Sx) = 4 s P - s (4 + z) Sx
-            const float s4 = 4.0f * sc[t][q];
-            const float scz = sc[t][q] * (4.0f + zc[t][q]);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                acc[i] = __builtin_fmaf(s4, pq[i], acc[i]);
-                acc[i] = __builtin_fmaf(-scz, sx[i], acc[i]);
-            }
+            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s4[t][q], pq[i], acc[i]);
         }
+        // - c Sx, c = sum_t s_t (4 + z_t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c[q], sx[i], acc[i]);
     }
 }
 
-template <int G, int K, int TT>
-__global__ __launch_bounds__(kLinearThreads) void linear_kernel(
+template <int G, int K, int TT, bool DEF>
+__global__ __launch_bounds__(64 * tile_waves(TT)) void linear_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int64_t n_tokens,
@@ -415,15 +418,17 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
 {
     using C = Chunk<G, K, TT>;
     constexpr int CG = C::CG;
+    constexpr int NW = C::NW;
     // two chunk buffers per wave
-    __shared__ __attribute__((aligned(16))) char buf[2][kWaves][C::BYTES];
-    __shared__ f32x4 red[kWaves][64];
+    __shared__ __attribute__((aligned(16))) char buf[2][NW][C::BYTES];
+    __shared__ f32x4 red[NW][64];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r = lane & 15;            // B column (output row) and A row (token)
     const int j = lane >> 4;            // k-slice
     const int tk = r < TT ? r : TT - 1; // A rows past the tile repeat its last token
+    const bool sym = zero_point == kZpSymmetric;
     // the code operand's constants in registers (opaque to constant folding,
     // so that the AND and OR fuse)
     uint32_t mask, one;
@@ -435,7 +440,7 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
     const int64_t gpr = cols / G;       // groups per row
     const int64_t wpr = cols / 16;      // code words per row
     // This wave's contiguous range of groups, a whole number of chunks.
-    const int64_t per_wave = ((gpr + kWaves - 1) / kWaves + CG - 1) / CG * CG;
+    const int64_t per_wave = ((gpr + NW - 1) / NW + CG - 1) / CG * CG;
     const int64_t g_begin = per_wave * wave < gpr ? per_wave * wave : gpr;
     const int64_t g_end = g_begin + per_wave < gpr ? g_begin + per_wave : gpr;
     const int n_chunks = (int)((g_end - g_begin + CG - 1) / CG);
@@ -450,9 +455,8 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
                           (K - 1) * src.code_plane + rows_here * (uint32_t)wpr * 4);
     src.scales = make_desc(scales + o0 * gpr * sbytes,
                            (K - 1) * src.scale_plane + rows_here * (uint32_t)gpr * sbytes);
-    src.sym = zero_point == kZpSymmetric;
-    src.zeros = make_desc(src.sym ? nullptr : zeros + o0 * gpr,
-                          src.sym ? 0u : (K - 1) * src.zero_plane + rows_here * (uint32_t)gpr * 4);
+    src.zeros = make_desc(sym ? nullptr : zeros + o0 * gpr,
+                          sym ? 0u : (K - 1) * src.zero_plane + rows_here * (uint32_t)gpr * 4);
     src.row_bytes = (uint32_t)wpr * 4;
     src.gpr = (uint32_t)gpr;
     src.x_row = (uint32_t)cols * 2;
@@ -477,13 +481,13 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
             const int na = (int)(g_end - ga < CG ? g_end - ga : CG);
             // chunk c is in buffer a; chunk c + 1, if any, may stay in flight
             if (c + 1 < n_chunks) wait_vm<C::DMA>(); else wait_vm<0>();
-            compute_chunk<G, K, TT>(la, na, r, j, tk, scale_type, src.sym, mask, one, acc);
+            compute_chunk<G, K, TT, DEF>(la, na, r, j, tk, scale_type, sym, mask, one, acc);
             if (c + 2 < n_chunks) load_chunk<G, K, TT>(lds_a, src, ga + 2 * CG, lane);
             if (c + 1 >= n_chunks) break;
             const uint32_t gb = ga + CG;
             const int nb = (int)(g_end - gb < CG ? g_end - gb : CG);
             if (c + 2 < n_chunks) wait_vm<C::DMA>(); else wait_vm<0>();
-            compute_chunk<G, K, TT>(lb, nb, r, j, tk, scale_type, src.sym, mask, one, acc);
+            compute_chunk<G, K, TT, DEF>(lb, nb, r, j, tk, scale_type, sym, mask, one, acc);
             if (c + 3 < n_chunks) load_chunk<G, K, TT>(lds_b, src, gb + 2 * CG, lane);
         }
 
@@ -494,7 +498,7 @@ __global__ __launch_bounds__(kLinearThreads) void linear_kernel(
         if (wave == 0 && 4 * j < TT) {
             f32x4 y = red[0][lane];
 #pragma unroll
-            for (int v = 1; v < kWaves; ++v) {
+            for (int v = 1; v < NW; ++v) {
                 const f32x4 q = red[v][lane];
                 y[0] += q[0]; y[1] += q[1]; y[2] += q[2]; y[3] += q[3];
             }
@@ -517,32 +521,37 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-template <int G, int TT>
-hipError_t launch_linear_gt(const uint32_t *codes, const char *scales, const float *zeros,
-                            int64_t rows, int64_t cols, int k, int zp, int sdt, const uint16_t *X,
-                            int64_t n_tokens, float *Y, hipStream_t stream)
+template <int G, int TT, bool DEF>
+hipError_t launch_linear_gtd(const uint32_t *codes, const char *scales, const float *zeros,
+                             int64_t rows, int64_t cols, int k, int zp, int sdt, const uint16_t *X,
+                             int64_t n_tokens, float *Y, hipStream_t stream)
 {
     const int64_t plane_words = rows * cols / 16;
     const int64_t plane_groups = rows * cols / G;
     const int grid = (int)((rows + 15) / 16);
+    const int block = 64 * tile_waves(TT);
     switch (k) {
-    case 1: return launch(linear_kernel<G, 1, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
-    case 2: return launch(linear_kernel<G, 2, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
-    case 3: return launch(linear_kernel<G, 3, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
-    case 4: return launch(linear_kernel<G, 4, TT>, grid, kLinearThreads, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 1: return launch(linear_kernel<G, 1, TT, DEF>, grid, block, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 2: return launch(linear_kernel<G, 2, TT, DEF>, grid, block, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 3: return launch(linear_kernel<G, 3, TT, DEF>, grid, block, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
+    case 4: return launch(linear_kernel<G, 4, TT, DEF>, grid, block, stream, codes, scales, zeros, rows, cols, plane_words, plane_groups, X, n_tokens, Y, zp, sdt);
     default: return hipErrorInvalidValue;
     }
 }
 
-// Up to 4 tokens: one pass with 4-token tiles; more: 16-token tiles.
+// Up to 4 tokens: one pass with 4-token tiles; more: 16-token tiles. The
+// default format (binary32 scales, stored zero-points) has its own kernels.
 template <int G>
 hipError_t launch_linear_g(const uint32_t *codes, const char *scales, const float *zeros,
                            int64_t rows, int64_t cols, int k, int zp, int sdt, const uint16_t *X,
                            int64_t n_tokens, float *Y, hipStream_t stream)
 {
+    const bool def = sdt == kScaleF32 && zp != kZpSymmetric;
     if (n_tokens <= 4)
-        return launch_linear_gt<G, 4>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
-    return launch_linear_gt<G, 16>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
+        return def ? launch_linear_gtd<G, 4, true>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream)
+                   : launch_linear_gtd<G, 4, false>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
+    return def ? launch_linear_gtd<G, 16, true>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream)
+               : launch_linear_gtd<G, 16, false>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
 }
 
 }  // namespace
