@@ -14,9 +14,9 @@ the per-group peak-to-mean ratio (alone, and as a side output of
 construction) is timed and its tensor-level indicators reported,
 construction in other stage formats (symmetric with fp16 scales, real
 zero-points, bf16 scales) is timed, rrq_linear decode passes (1 and 16
-tokens, prefixes k = 1..4, one call per tensor on per-tensor packages, the
-pass replayed as a HIP graph and also launched call by call) are timed, and a
-streaming probe with the same read/write mix gives the practical HBM
+tokens, prefixes k = 1..4, one call per tensor on per-tensor packages, and
+with q/k/v and gate/up fused into one call each; the pass replayed as a HIP
+graph and also launched call by call) are timed, and a streaming probe with the same read/write mix gives the practical HBM
 ceiling (include/hbm_probe.h).
 
 Prints one JSON line. ``value`` is construction throughput in GB/s of bf16
@@ -123,46 +123,56 @@ def time_from_base(calls, G, S, stream, flush_buf=None, launches=20):
     return sum(ms) / len(ms), min(ms)
 
 
-def linear_bytes(w, k, M):
-    """Algorithmic HBM bytes of one decode pass of rrq_linear over every
-    tensor of w: k code planes + k (s, z) per group, X in, Y out."""
-    G = w.group_size
-    total = 0
+def decode_calls(w, fused):
+    """The rrq_linear calls of one decode pass over w: one per tensor, or
+    with the projections that read the same input (q/k/v, gate/up: adjacent
+    in the flat buffer, same input width) fused into one call on their
+    row-concatenated weight. Returns (name, rows, cols, offset) tuples."""
+    calls = []
     for t in w.tensors:
-        total += k * t.numel // 4 + 8 * k * (t.numel // G) + 2 * M * t.cols + 4 * M * t.rows
+        short = t.name.split(".")[-1]
+        if fused and calls and short in ("k_proj", "v_proj", "up_proj"):
+            name, rows, cols, off = calls[-1]
+            assert cols == t.cols and off + rows * cols == t.offset
+            calls[-1] = (name + "+" + short, rows + t.rows, cols, off)
+        else:
+            calls.append((short, t.rows, t.cols, t.offset))
+    return calls
+
+
+def linear_bytes(calls, G, k, M):
+    """Algorithmic HBM bytes of one decode pass of rrq_linear calls: k code
+    planes + k (s, z) per group, X in, Y out."""
+    total = 0
+    for _, rows, cols, _ in calls:
+        n = rows * cols
+        total += k * n // 4 + 8 * k * (n // G) + 2 * M * cols + 4 * M * rows
     return total
 
 
 def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 2, 3, 4),
                 launches=10):
-    """Decode-style passes of rrq_linear over every tensor of w (one call per
-    tensor, each tensor its own package). A pass is captured once in a HIP
-    graph and replayed, as a serving loop would run it, and timed with HIP
-    events around each replay ("ms"); the same pass launched call by call
-    from Python is timed too ("ms_eager": at a few microseconds per call it
-    is bound by the host's launch rate for the small tensors). Builds the
-    per-tensor packages first (untimed)."""
+    """Decode-style passes of rrq_linear over every tensor of w, each call on
+    its own package: one call per tensor ("per_tensor"), and with q/k/v and
+    gate/up fused into one call each on their row-concatenated weight
+    ("fused": the same groups, so the same package bytes). A pass is
+    captured once in a HIP graph and replayed, as a serving loop would run
+    it, and timed with HIP events around each replay ("ms"); the same pass
+    launched call by call from Python is timed too ("ms_eager"). Builds the
+    packages first (untimed)."""
     import torch
 
     import paper_2608_04048_amd as rrq
 
     G, S = w.group_size, w.n_stages
     cflat, sflat, zflat = codes.view(-1), scales.view(-1), zeros.view(-1)
-    pk = []
-    for t in w.tensors:
-        c = cflat[S * t.offset // 16:S * (t.offset + t.numel) // 16].view(S, t.numel // 16)
-        sc = sflat[S * t.offset // G:S * (t.offset + t.numel) // G].view(S, t.numel // G)
-        zz = zflat[S * t.offset // G:S * (t.offset + t.numel) // G].view(S, t.numel // G)
-        rrq.rrq_construct(W_flat[t.offset:t.offset + t.numel], t.rows, t.cols, G, S, c, sc, zz,
-                          stream)
-        pk.append((t, c, sc, zz))
     g = torch.Generator(device="cuda")
     g.manual_seed(2608)
     max_m = max(tokens)
     xs = {c: torch.randn((max_m, c), generator=g, device="cuda").to(torch.bfloat16)
           for c in sorted({t.cols for t in w.tensors})}
-    y = torch.empty(max_m * max(t.rows for t in w.tensors), dtype=torch.float32, device="cuda")
-    torch.cuda.synchronize()
+    y = torch.empty(max_m * 2 * max(t.rows for t in w.tensors), dtype=torch.float32,
+                    device="cuda")
 
     def timed(fn):
         fn()
@@ -178,28 +188,43 @@ def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 
 
     out = {}
     cs = torch.cuda.Stream()
-    for M in tokens:
-        for k in ks:
-            def run(st, M=M, k=k):
-                for t, c, sc, zz in pk:
-                    rrq.rrq_linear(c, sc, zz, t.rows, t.cols, G, S, k, xs[t.cols], M, y, st)
-            t_eager = timed(lambda: run(stream))
-            cs.wait_stream(stream)
-            graph = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(graph, stream=cs):
-                run(cs)
-            stream.wait_stream(cs)
+    for mode in ("per_tensor", "fused"):
+        calls = decode_calls(w, mode == "fused")
+        pk = []
+        for name, rows, cols, off in calls:
+            n = rows * cols
+            c = cflat[S * off // 16:S * (off + n) // 16].view(S, n // 16)
+            sc = sflat[S * off // G:S * (off + n) // G].view(S, n // G)
+            zz = zflat[S * off // G:S * (off + n) // G].view(S, n // G)
+            rrq.rrq_construct(W_flat[off:off + n], rows, cols, G, S, c, sc, zz, stream)
+            pk.append((rows, cols, c, sc, zz))
+        torch.cuda.synchronize()
+        res = {}
+        for M in tokens:
+            for k in ks:
+                def run(st, M=M, k=k):
+                    for rows, cols, c, sc, zz in pk:
+                        rrq.rrq_linear(c, sc, zz, rows, cols, G, S, k, xs[cols], M, y, st)
+                t_eager = timed(lambda: run(stream))
+                cs.wait_stream(stream)
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(graph, stream=cs):
+                    run(cs)
+                stream.wait_stream(cs)
 
-            def replay():
-                with torch.cuda.stream(stream):
-                    graph.replay()
-            t_ms = timed(replay)
-            del graph
-            nbytes = linear_bytes(w, k, M)
-            out[f"M{M}_k{k}"] = {"ms": round(t_ms, 4), "ms_eager": round(t_eager, 4),
-                                 "bytes": nbytes,
-                                 "hbm_gbs": round(nbytes / (t_ms * 1e-3) / 1e9, 1),
-                                 "hbm_frac": round(nbytes / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+                def replay():
+                    with torch.cuda.stream(stream):
+                        graph.replay()
+                t_ms = timed(replay)
+                del graph
+                nbytes = linear_bytes(calls, G, k, M)
+                res[f"M{M}_k{k}"] = {"ms": round(t_ms, 4), "ms_eager": round(t_eager, 4),
+                                     "bytes": nbytes,
+                                     "hbm_gbs": round(nbytes / (t_ms * 1e-3) / 1e9, 1),
+                                     "hbm_frac": round(nbytes / (t_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        res["calls"] = (f"{len(calls)} rrq_linear calls per pass "
+                        f"({', '.join(sorted({c[0] for c in calls}))}), replayed as one HIP graph")
+        out[mode] = res
     return out
 
 
@@ -528,8 +553,6 @@ def main():
     if not args.no_linear:
         print("bench: timing rrq_linear decode passes", file=sys.stderr, flush=True)
         result["linear"] = time_linear(w, W.view(-1), codes, scales, zeros, stream)
-        result["linear"]["calls"] = (f"one rrq_linear call per tensor ({len(w.tensors)} per pass), "
-                                     "the pass replayed as one HIP graph")
     if not args.no_stream_probe:
         result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
         result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)
