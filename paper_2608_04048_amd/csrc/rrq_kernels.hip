@@ -91,12 +91,21 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes)
 // Per-lane dequantization tables in LDS, one per wave. Entry idx = k[e] +
 // 4 k[e + 1] (k = 3 - code) of lane l holds the pair of dequantized values
 // {fl((Q[e] - z) s), fl((Q[e + 1] - z) s)} of the lane's group for the current
-// stage, at byte offset idx * 512 + l * 8: a wave's 64 lookups of one pair
-// of elements read 512 bytes that cover all banks once per half wave.
+// stage, the first at byte offset idx * 512 + l * 4 and the second 256 bytes
+// further: one two-address LDS read fetches a pair, a wave's 64 lookups of one
+// pair of elements touch every bank once per value, and the lane's whole
+// table is written from a single address register.
 struct DequantTable {
-    float *base;      // this wave's 16 x 64 x 2 floats
-    float lane_off;   // binary32 whose bit pattern is l * 8
+    float *base;      // this wave's 16 x 2 x 64 floats
+    float lane_off;   // binary32 whose bit pattern is l * 4
 };
+
+// The pair of dequantized values at byte offset off of the table.
+__device__ __forceinline__ f32x2 table_pair(const char *tbase, uint32_t off)
+{
+    const float *p = reinterpret_cast<const float *>(tbase + off);
+    return (f32x2){p[0], p[64]};
+}
 
 // Code of one element as the tiny binary32 (3 - min(Q, 3)) 2^-149, where
 // Q = RNE(r inv + z) of the exact value: u = fma(r, inv, 1.5 * 2^23 + z) rounds
@@ -143,7 +152,7 @@ __device__ __forceinline__ void stage_elements(float (&r)[G], float inv, float m
                 x[p] = __builtin_fmaf(tiny_code(r[j + 1], inv, m), 4.0f, tiny_code(r[j], inv, m));
             if (UPDATE) {
                 const uint32_t off = __float_as_uint(__builtin_fmaf(x[p], 512.0f, tab.lane_off));
-                rhw[p] = *reinterpret_cast<const f32x2 *>(tbase + off);
+                rhw[p] = table_pair(tbase, off);
             }
         }
         float q[4];
@@ -198,7 +207,7 @@ __device__ __forceinline__ void subtract_base_half(float (&r)[G], const uint32_t
                                                    float &h0, float &h1)
 {
     const char *tbase = reinterpret_cast<const char *>(tab.base);
-    const uint32_t lane_off = __float_as_uint(tab.lane_off);   // lane * 8 < 512
+    const uint32_t lane_off = __float_as_uint(tab.lane_off);   // lane * 4 < 256
     f32x2 rh[2][4];   // lookups of two consecutive 8-element pieces in flight
     constexpr int H0 = HALF * (G / 16), H1 = H0 + G / 16;    // 8-element pieces
 
@@ -210,7 +219,7 @@ __device__ __forceinline__ void subtract_base_half(float (&r)[G], const uint32_t
             // nibble p of kw, times 512
             const uint32_t nib = (4 * p <= 9) ? (kw << (9 - 4 * p)) & 0x1E00u
                                               : (kw >> (4 * p - 9)) & 0x1E00u;
-            rhh[i] = *reinterpret_cast<const f32x2 *>(tbase + (nib | lane_off));
+            rhh[i] = table_pair(tbase, nib | lane_off);
         }
     };
     auto apply = [&](int h, const f32x2 (&rhh)[4]) {
@@ -346,7 +355,7 @@ struct TileOut {
     char *scales;        // binary32, or 16-bit patterns (the kernel's SC)
     float *zeros;
     int64_t words_per_stage, n_groups;
-    uint32_t code_bytes, groups_here;
+    uint32_t groups_here;
 };
 
 // Scale storage SC (kScaleF32, kScaleF16, kScaleBF16): the binary32 value of
@@ -365,29 +374,52 @@ __device__ __forceinline__ float round_scale(float s)
     }
 }
 
+// Stores one stage of a tile. With active false the same store instructions
+// go to zero-sized resources and are dropped: every tile then issues the same
+// sequence of vector-memory operations whatever the stage count, which lets
+// the wait for the prefetched tile at the top of the tile loop count past
+// the previous tile's stores instead of draining them (loads and stores share
+// one in-order counter on this architecture).
 template <int G, int ZP, int SC>
 __device__ __forceinline__ void store_stage(const TileOut &o, int k, int lane,
-                                            const uint32_t (&words)[G / 16], float s, float z)
+                                            const uint32_t (&words)[G / 16], float s, float z,
+                                            bool active = true)
 {
     // Lanes past the last group fall outside the resources; their stores
     // are dropped.
-    store_words<G>(make_rsrc(o.codes + k * o.words_per_stage, o.code_bytes),
+    // (read back as a wave-uniform value: the resource must stay scalar)
+    const uint32_t groups = __builtin_amdgcn_readfirstlane(active ? o.groups_here : 0u);
+    store_words<G>(make_rsrc(o.codes + k * o.words_per_stage, groups * (G / 16) * 4),
                    lane * (G / 16) * 4, words);
     if constexpr (SC == kScaleF32) {
         __builtin_amdgcn_raw_buffer_store_b32(
-            __float_as_uint(s), make_rsrc(o.scales + k * o.n_groups * 4, o.groups_here * 4),
+            __float_as_uint(s), make_rsrc(o.scales + k * o.n_groups * 4, groups * 4),
             lane * 4, 0, 0);
     } else {
         // s already holds a value of the 16-bit type: the conversion is exact
         const uint16_t b = SC == kScaleF16 ? __builtin_bit_cast(uint16_t, (_Float16)s)
                                            : (uint16_t)(__float_as_uint(s) >> 16);
         __builtin_amdgcn_raw_buffer_store_b16(
-            b, make_rsrc(o.scales + k * o.n_groups * 2, o.groups_here * 2), lane * 2, 0, 0);
+            b, make_rsrc(o.scales + k * o.n_groups * 2, groups * 2), lane * 2, 0, 0);
     }
     if constexpr (ZP != kZpSymmetric)
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z),
-                                              make_rsrc(o.zeros + k * o.n_groups, o.groups_here * 4),
+                                              make_rsrc(o.zeros + k * o.n_groups, groups * 4),
                                               lane * 4, 0, 0);
+}
+
+// fl(d / 3) for every finite d >= 0 in five fewer dependent steps than the
+// IEEE division sequence: q = fl(d fl(1/3)) is within an ulp of d / 3, the
+// first FMA gives the remainder d - 3q exactly, and the second rounds the
+// corrected quotient q + (d - 3q) fl(1/3) once. It equals IEEE d / 3 on every
+// non-negative finite binary32 (an exhaustive check of the same arithmetic
+// runs with the CPU tests).
+__device__ __forceinline__ float div3(float d)
+{
+    constexpr float kThird = 0x1.555556p-2f;   // fl(1/3)
+    const float q = d * kThird;
+    const float rem = __builtin_fmaf(-3.0f, q, d);
+    return __builtin_fmaf(rem, kThird, q);
 }
 
 // Scale, reciprocal, zero-point and magic addend of one stage from the
@@ -407,7 +439,7 @@ __device__ __forceinline__ void stage_params(float lo, float hi, float &inv, flo
     } else {
         d = hi - lo;
     }
-    const float s = round_scale<SC>(d / 3.0f);
+    const float s = round_scale<SC>(div3(d));
     const bool degenerate = !(s >= 0x1p-126f);
     inv = degenerate ? 0.0f : 1.0f / s;
     sq = degenerate ? 0.0f : s;
@@ -418,6 +450,26 @@ __device__ __forceinline__ void stage_params(float lo, float hi, float &inv, flo
     m = kMagic + z;
 }
 
+// Two 32-bit LDS writes at addr + O0 * 256 and addr + O1 * 256 bytes, from two
+// independent registers (a 64-bit write would need them in adjacent
+// registers, i.e. copies).
+template <int O0, int O1>
+__device__ __forceinline__ void lds_write2st64(uint32_t addr, float a, float b)
+{
+    asm volatile("ds_write2st64_b32 %0, %1, %2 offset0:%3 offset1:%4"
+                 :: "v"(addr), "v"(a), "v"(b), "i"(O0), "i"(O1) : "memory");
+}
+
+template <int I = 0>
+__device__ __forceinline__ void write_table_entries(uint32_t addr, const float (&t)[4])
+{
+    if constexpr (I < 16) {
+        // entry I: its two values at I * 512 and I * 512 + 256 bytes
+        lds_write2st64<2 * I, 2 * I + 1>(addr, t[I & 3], t[I >> 2]);
+        write_table_entries<I + 1>(addr, t);
+    }
+}
+
 // Fills this lane's dequantization table for the stage: entry k0 + 4 k1 is
 // {fl((3 - k0 - z) s), fl((3 - k1 - z) s)}.
 __device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, float sq, float z)
@@ -425,19 +477,21 @@ __device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, fl
     float t[4];   // t[k] = fl((Q - z) s) for Q = 3 - k
 #pragma unroll
     for (int k = 0; k < 4; ++k) t[k] = ((float)(3 - k) - z) * sq;
-    f32x2 *row = reinterpret_cast<f32x2 *>(tab.base) + lane;
-#pragma unroll
-    for (int idx = 0; idx < 16; ++idx) row[idx * 64] = (f32x2){t[idx & 3], t[idx >> 2]};
+    typedef __attribute__((address_space(3))) float lds_float;
+    write_table_entries((uint32_t)(uintptr_t)(lds_float *)(tab.base + lane), t);
 }
 
-// Loads one lane's base stage (plane 0 of the package): its group's code
-// words, scale and zero-point. Lanes past the input read zeros.
+// Loads one lane's base stage (plane 0 of the package) for tile `tile`: its
+// group's code words, scale and zero-point. Lanes past the input, and a tile
+// past the end, read zeros.
 template <int G, int ZP, int SC>
 __device__ __forceinline__ void load_base(const uint32_t *codes, const char *scales,
-                                          const float *zeros, int64_t g0,
-                                          uint32_t groups_here, int lane, uint32_t (&bw)[G / 16],
-                                          float &s0, float &z0)
+                                          const float *zeros, int64_t n_groups, int64_t tile,
+                                          int lane, uint32_t (&bw)[G / 16], float &s0, float &z0)
 {
+    const int64_t left = n_groups - tile * 64;
+    const int64_t g0 = left <= 0 ? 0 : tile * 64;
+    const uint32_t groups_here = left <= 0 ? 0u : (uint32_t)(left < 64 ? left : 64);
     const rsrc_t rc = make_rsrc(codes + g0 * (G / 16), groups_here * (G / 16) * 4);
     if constexpr (G / 16 >= 4) {
 #pragma unroll
@@ -501,19 +555,34 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     uint4 *const wr_base = tile_lds + (lane / CH) * ROW + (lane % HC);
     const uint4 *const rd_base = tile_lds + lane * ROW;
     const DequantTable tab = {reinterpret_cast<float *>(table_lds),
-                              __uint_as_float((uint32_t)lane * 8)};
+                              __uint_as_float((uint32_t)lane * 4)};
 
     int64_t tile = blockIdx.x;
     uint4 v[CH];
-    if (tile < n_tiles) load_tile<CH>(W, n_groups, tile, lane, v);
+    uint32_t bw[WPG];            // base stage of the tile in v (with a base)
+    float bs = 0.f, bz = 0.f;
+    if (tile < n_tiles) {
+        load_tile<CH>(W, n_groups, tile, lane, v);
+        if constexpr (FROM_BASE)
+            load_base<G, ZP, SC>(codes, scales, zeros, n_groups, tile, lane, bw, bs, bz);
+    }
+    // The stores of one tile, dropped (see store_stage): the loop is entered
+    // with the same operations outstanding as after each tile.
+    {
+        // (distinct planes, so that no store looks overwritten by the next)
+        const TileOut none = {codes, scales, zeros, 1, 1, 0u};
+        const uint32_t zw[WPG] = {};
+        store_pmr<G>(pmr, 0, 0u, lane, 0.f, 0.f, 0.f);
+        if constexpr (!STATS_ONLY) {
+#pragma unroll
+            for (int k = 0; k < kMaxStages; ++k)
+                store_stage<G, ZP, SC>(none, k, lane, zw, 0.f, 0.f, false);
+        }
+    }
 
     for (; tile < n_tiles; tile += gridDim.x) {
         const int64_t g0 = tile * 64;
         const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
-        uint32_t bw[WPG];
-        float bs = 0.f, bz = 0.f;
-        if constexpr (FROM_BASE)
-            load_base<G, ZP, SC>(codes, scales, zeros, g0, groups_here, lane, bw, bs, bz);
 
         float r[G];
         float bl0 = 0.f, bl1 = 0.f, bh0 = 0.f, bh1 = 0.f;   // range of R_0 (with a base)
@@ -544,24 +613,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
 
         constexpr int64_t scale_bytes = SC == kScaleF32 ? 4 : 2;
         const TileOut out = {codes + g0 * WPG, scales + g0 * scale_bytes, zeros + g0,
-                             n_groups * WPG, n_groups, groups_here * WPG * 4, groups_here};
+                             n_groups * WPG, n_groups, groups_here};
 
-        float lo, hi, inv, sq, z, m;
-        uint32_t words[WPG];
+        float lo, hi, inv = 0.f, sq = 0.f, z = 0.f, m = 0.f;
+        uint32_t words[WPG] = {};
         if constexpr (FROM_BASE) {
             lo = fminf(bl0, bl1);
             hi = fmaxf(bh0, bh1);
         } else {
             group_range<G>(r, lo, hi);
         }
-        if (stats) store_pmr<G>(pmr, g0, groups_here, lane, lo, hi, abs_sum);
+        store_pmr<G>(pmr, g0, stats ? groups_here : 0u, lane, lo, hi, abs_sum);
         if constexpr (STATS_ONLY) continue;
-        for (int k = FROM_BASE ? 1 : 0; k + 1 < n_stages; ++k) {
-            stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
-            fill_table(tab, lane, sq, z);
-            stage_elements<G, true, ZP>(r, inv, m, z, tab, words, lo, hi);
-            store_stage<G, ZP, SC>(out, k, lane, words, sq, z);
+        // Stage slots 0 .. kMaxStages - 2 hold the stages that update the
+        // residual; a slot outside 1 + FROM_BASE .. n_stages - 1 computes
+        // nothing and drops its stores.
+#pragma unroll
+        for (int k = 0; k + 1 < kMaxStages; ++k) {
+            const bool active = k >= (FROM_BASE ? 1 : 0) && k + 1 < n_stages;
+            if (active) {
+                stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
+                fill_table(tab, lane, sq, z);
+                stage_elements<G, true, ZP>(r, inv, m, z, tab, words, lo, hi);
+            }
+            store_stage<G, ZP, SC>(out, k, lane, words, sq, z, active);
         }
+        // The next tile's base stage, loaded where the last stage leaves
+        // registers free; only this stage's stores are issued after it.
+        if constexpr (FROM_BASE)
+            load_base<G, ZP, SC>(codes, scales, zeros, n_groups, tile + gridDim.x, lane, bw, bs,
+                                 bz);
         stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
         stage_elements<G, false, ZP>(r, inv, m, z, tab, words, lo, hi);
         store_stage<G, ZP, SC>(out, n_stages - 1, lane, words, sq, z);

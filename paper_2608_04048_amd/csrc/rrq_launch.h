@@ -40,6 +40,9 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
 // buffer sizes and offsets (at most 16 * rows * 4 bytes) cannot wrap.
 constexpr int64_t kLinearMaxDim = int64_t(1) << 26;
 
+// Stages a package holds at most (RRQ_MAX_STAGES of rrq.h).
+constexpr int kMaxStages = 4;
+
 // Workgroups the construct kernel keeps resident per compute unit.
 constexpr int kConstructBlocksPerCU = 8;
 // Reconstruct: threads per workgroup (4 waves), 16-byte output chunks per
