@@ -320,7 +320,8 @@ def time_pmr(w, W, G, S, stream, launches=10):
 def stream_probe(src_bytes, flush_buf=None, launches=10):
     """Practical HBM ceiling for construction's read/write mix: a streaming
     kernel reading src_bytes and writing 5/8 of that (include/hbm_probe.h),
-    mean of `launches` HIP-event-timed launches on the current stream."""
+    mean of `launches` HIP-event-timed launches on the current stream; and the
+    read-only and write-only probes on the same byte counts."""
     import torch
 
     from paper_2608_04048_amd import probe
@@ -344,9 +345,40 @@ def stream_probe(src_bytes, flush_buf=None, launches=10):
     t = sum(ms) / len(ms)
     moved = src_bytes + src_bytes // 8 * 5
     gbs = moved / (t * 1e-3) / 1e9
+
+    # Each direction alone: the read-only probe on src, the write-only probe
+    # on dst (the same byte counts). "serial" is the rate of reading and then
+    # writing those bytes one after the other at these rates.
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def timed(fn):
+        fn()
+        vals = []
+        for _ in range(launches):
+            if flush_buf is not None:
+                flush_buf.fill_(1.0)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            vals.append(a.elapsed_time(b))
+        return sum(vals) / len(vals)
+
+    t_read = timed(lambda: probe.hbm_probe_read(src, src_bytes, out, stream))
+    t_write = timed(lambda: probe.hbm_probe_write(dst, src_bytes // 8 * 5, 0, stream))
     del src, dst
+    read_gbs = src_bytes / (t_read * 1e-3) / 1e9
+    write_gbs = src_bytes // 8 * 5 / (t_write * 1e-3) / 1e9
+    serial_gbs = moved / ((t_read + t_write) * 1e-3) / 1e9
     return {"read_bytes": src_bytes, "written_bytes": src_bytes // 8 * 5, "ms": round(t, 4),
-            "gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+            "gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "read_only": {"ms": round(t_read, 4), "gbs": round(read_gbs, 1),
+                          "frac": round(read_gbs / HBM_PEAK_GBS, 4)},
+            "write_only": {"ms": round(t_write, 4), "gbs": round(write_gbs, 1),
+                           "frac": round(write_gbs / HBM_PEAK_GBS, 4)},
+            "serial": {"ms": round(t_read + t_write, 4), "gbs": round(serial_gbs, 1),
+                       "frac": round(serial_gbs / HBM_PEAK_GBS, 4)}}
 
 
 def main():

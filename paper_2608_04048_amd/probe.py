@@ -1,6 +1,7 @@
-"""Binding of libhbm_probe.so (include/hbm_probe.h): a streaming kernel with
-package construction's read/write ratio (reads B bytes, writes 5B/8), used by
-the benchmark as the practical HBM ceiling for that mix."""
+"""Binding of libhbm_probe.so (include/hbm_probe.h): streaming kernels used by
+the benchmark as practical HBM ceilings: one with package construction's
+read/write ratio (reads B bytes, writes 5B/8), a read-only and a write-only
+one."""
 
 from __future__ import annotations
 
@@ -21,6 +22,12 @@ def load_library() -> ctypes.CDLL:
         lib.hbm_probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                          ctypes.c_void_p]
         lib.hbm_probe_stream.restype = ctypes.c_int
+        lib.hbm_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+        lib.hbm_probe_read.restype = ctypes.c_int
+        lib.hbm_probe_write.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32,
+                                        ctypes.c_void_p]
+        lib.hbm_probe_write.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -35,3 +42,29 @@ def hbm_probe_stream(src, src_bytes: int, dst, stream=None) -> None:
     st = load_library().hbm_probe_stream(ptr(src), int(src_bytes), ptr(dst), sp)
     if st != 0:
         raise RuntimeError(f"hbm_probe_stream failed with status {st}")
+
+
+def _sp(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def _ptr(x):
+    return x if isinstance(x, int) else x.data_ptr()
+
+
+def hbm_probe_read(src, src_bytes: int, out, stream=None) -> None:
+    """Enqueue one read-only pass over src; XORs the XOR of its words into out[0]."""
+    st = load_library().hbm_probe_read(_ptr(src), int(src_bytes), _ptr(out), _sp(stream))
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_read failed with status {st}")
+
+
+def hbm_probe_write(dst, dst_bytes: int, value: int, stream=None) -> None:
+    """Enqueue one write-only pass filling dst with the 32-bit value."""
+    st = load_library().hbm_probe_write(_ptr(dst), int(dst_bytes), int(value) & 0xFFFFFFFF,
+                                        _sp(stream))
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_write failed with status {st}")

@@ -187,7 +187,7 @@ def test_probe_library_exports_declared_function():
     from paper_2608_04048_amd import probe
     text = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
     names = sorted(set(re.findall(r"\b(hbm_probe_\w+)\s*\(", text)))
-    assert names == ["hbm_probe_stream"]
+    assert names == ["hbm_probe_read", "hbm_probe_stream", "hbm_probe_write"]
     lib = probe.load_library()
     out = os.popen(f"nm -D --defined-only {probe.LIB_PATH}").read()
     for name in names:
@@ -206,6 +206,27 @@ def test_probe_library_exports_declared_function():
 def test_probe_rejects(src, nbytes, dst, status):
     from paper_2608_04048_amd import probe
     assert probe.load_library().hbm_probe_stream(src, nbytes, dst, None) == status
+
+
+@pytest.mark.parametrize("src,nbytes,out,status", [
+    (0, 1024, FAKE, 1),
+    (FAKE, 1024, 0, 1),
+    (FAKE + 8, 1024, FAKE, 2),
+    (FAKE, 1024, FAKE + 2, 2),
+    (FAKE, 0, FAKE, 3),
+    (FAKE, 1000, FAKE, 3),
+])
+def test_read_probe_rejects(src, nbytes, out, status):
+    from paper_2608_04048_amd import probe
+    assert probe.load_library().hbm_probe_read(src, nbytes, out, None) == status
+
+
+@pytest.mark.parametrize("dst,nbytes,status", [
+    (0, 1024, 1), (FAKE + 8, 1024, 2), (FAKE, 0, 3), (FAKE, 1000, 3),
+])
+def test_write_probe_rejects(dst, nbytes, status):
+    from paper_2608_04048_amd import probe
+    assert probe.load_library().hbm_probe_write(dst, nbytes, 0, None) == status
 
 
 def _linear_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128, S=4, k=4,
