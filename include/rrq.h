@@ -295,14 +295,17 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *   k_stages   1..n_stages (2 k_stages effective bits).
  *   X          device, bfloat16 bit patterns [n_tokens][cols], 16-byte
  *              aligned (read only).
- *   n_tokens   >= 1; tokens are processed 4 at a time (the package is read
- *              once per 4 tokens: single-token decode reads it once).
+ *   n_tokens   >= 1; up to 4 tokens are served by one pass over the
+ *              package (single-token decode reads it once), more tokens 16
+ *              per pass.
  *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
  *   stream     HIP stream the work is enqueued on.
  *
  * Arithmetic: every product X * (1 + Q/4), X * 1 is exact in the matrix
- * cores; fp32 rounding enters in the accumulations only, in a fixed order
- * (results are deterministic). With u = 2^-24, A = sum_{t, g} |s_t,g|
+ * cores; fp32 rounding enters in the accumulations only, in an order fixed
+ * by rows, cols, group_size, k_stages and n_tokens (results are
+ * deterministic; the same token may round differently in calls with another
+ * n_tokens). With u = 2^-24, A = sum_{t, g} |s_t,g|
  * (11 + |z_t,g|) sum_{i in g} |X[m][i]|, p = groups per row and
  * n = k_stages * (min(p, 4 ceil(p / 16)) + 1),
  * |Y[m][o] - exact| <= 1.05 u A (group_size + 2 n + 24).

@@ -144,10 +144,15 @@ int linear_common(const uint32_t *codes, const void *scales, const float *zeros,
     // the k stage planes the kernel reads span less than 4 GiB of codes
     if ((uint64_t)k_stages * (uint64_t)(n / 4) >= (uint64_t(1) << 32)) return RRQ_ERR_SHAPE;
     if (!aligned(codes, 16) || !aligned(X, 16) || !aligned(Y, 4)) return RRQ_ERR_ALIGN;
-    if (current_cu_count() <= 0) return RRQ_ERR_HIP;
-    hipError_t e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,
-                                             n_stages, k_stages, zero_point, scale_type, X,
-                                             n_tokens, Y, stream);
+    const int cus = current_cu_count();
+    if (cus <= 0) return RRQ_ERR_HIP;
+    hipError_t e = rrq_detail::linear_decode_fits(rows, cols, group_size, k_stages, n_tokens)
+                       ? rrq_detail::launch_linear_decode(codes, scales, zeros, rows, cols, k_stages,
+                                                          zero_point, scale_type, X, n_tokens, Y,
+                                                          cus, stream)
+                       : rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,
+                                                   n_stages, k_stages, zero_point, scale_type, X,
+                                                   n_tokens, Y, stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 

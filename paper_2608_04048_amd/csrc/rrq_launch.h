@@ -2,6 +2,7 @@
 // HIP kernels (rrq_kernels.hip). Arguments are already validated.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include <hip/hip_runtime_api.h>
@@ -35,6 +36,16 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
                          int64_t rows, int64_t cols, int G, int S, int k, int zero_point,
                          int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
                          hipStream_t stream);
+
+// The decode form of the linear layer (up to 4 tokens, groups of 128, at
+// least 2 stages and 6144 rows, cols a multiple of 4096 up to 4096
+// kDecodeMaxSetsPerWave); launch_linear covers every other case.
+constexpr int kDecodeMaxSetsPerWave = 4;
+bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens);
+hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const float *zeros,
+                                int64_t rows, int64_t cols, int k, int zero_point, int scale_type,
+                                const uint16_t *X, int64_t n_tokens, float *Y, int cus,
+                                hipStream_t stream);
 
 // rows and cols of the linear kernel stay below this bound, so its 32-bit
 // buffer sizes and offsets (at most 16 * rows * 4 bytes) cannot wrap.

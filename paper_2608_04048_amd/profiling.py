@@ -21,7 +21,8 @@ import os
 import sys
 from collections import defaultdict
 
-DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "linear_kernel", "stream_probe_kernel",
+DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "linear_kernel", "decode_kernel",
+                 "stream_probe_kernel", "read_probe_kernel", "write_probe_kernel",
                  "copyBuffer"]
 
 
