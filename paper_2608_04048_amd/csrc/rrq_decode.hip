@@ -8,11 +8,8 @@
 // n = l % 16, k-slice j = l / 16):
 //   * B columns are 4 output rows x 4 consecutive groups (n = 4 r + g'); lane
 //     j owns inputs 32 j .. 32 j + 31 of its group, i.e. 8 contiguous bytes
-//     of codes per stage. One load instruction of a wave reads 4 rows x 128
-//     contiguous bytes with consecutive lanes on consecutive 8-byte pieces,
-//     and a cross-lane permutation (ds_bpermute) hands each piece to its
-//     MFMA lane. Codes become the bfloat16 1 + Q/4 (one shift and one AND-OR
-//     per pair of codes, codes q and q + 8 of a word per register);
+//     of codes per stage. Codes become the bfloat16 1 + Q/4 (one shift and
+//     one AND-OR per pair of codes, codes q and q + 8 of a word per register);
 //   * A rows are 4 tokens x the same 4 groups (m = 4 t + g), so C[m][n] is a
 //     group's dot product only on the diagonal g = g': lane l keeps all four
 //     of its C rows (tokens j, groups 0..3) and uses row g' = n % 4 at the end;
@@ -29,13 +26,24 @@
 // Work: the 8 waves of a workgroup split every 4-row tile's columns, so at
 // any moment a workgroup reads whole rows and neighbouring workgroups read
 // neighbouring rows; a workgroup takes batches of consecutive tiles in turn.
-// Each wave walks its (tile, set) items as one sequence and keeps the loads
-// of the next D - 1 items in flight in registers (codes, scales and
-// zero-points of the K stages).
+// Each wave walks its (tile, set) items as one sequence.
+//
+// Memory path: an item's codes (4 rows x 128 contiguous bytes per stage),
+// scales and zero-points go from HBM straight into a ring of D LDS slots per
+// wave by LDS-DMA loads: one 1 KiB load per two stages of codes, one load
+// for the scales and one for the zero-points of all stages, a fixed count
+// per item. The wave keeps the next D - 1 items in flight and waits for
+// exactly the item it is about to read (s_waitcnt vmcnt with the later
+// items' load count); with no register destinations there is nothing for
+// the compiler to drain at the loop's back edge. Each lane then reads its 8
+// code bytes per stage and its scales and zero-points from the slot: the 64
+// lanes' code reads cover the stage's 512 bytes once, so they are free of
+// bank conflicts.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rrq_dma.h"
 #include "rrq_launch.h"
 
 namespace rrq_detail {
@@ -45,19 +53,12 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-using rsrc_t = __amdgpu_buffer_rsrc_t;
 
 constexpr int kWaves = 8;                      // waves per workgroup
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
 constexpr uint32_t kCodeMask = 0x00600060u;    // top two mantissa bits of both halves
 constexpr int kZpSymmetric = 2;
 constexpr int kScaleF32 = 0, kScaleF16 = 1;
-
-__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
-                                             0x00020000);
-}
 
 __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x4 &c)
 {
@@ -81,22 +82,44 @@ __device__ __forceinline__ void word_operands(uint32_t w, uint32_t mask, uint32_
     b1[3] = ((w >> 9) & mask) | one;
 }
 
-// The loads of one item (a 4-row tile and a set of 4 groups) for all K
-// stages: this lane's 8 code bytes, scale and zero-point per stage.
+// One item's LDS slot (a 4-row tile and a set of 4 groups, all K stages):
+// codes of stage t at 1024 (t / 2) + 512 (t % 2), row-major 4 x 128 bytes;
+// scales and zero-points as 32-bit words, stage t of pair n = 4 row + group
+// at 4 (16 t + n) of their block.
 template <int K>
-struct Item {
-    u32x2 c[K];
-    uint32_t s[K], z[K];
+struct ItemSlot {
+    static constexpr int CODE_DMA = (K + 1) / 2;   // 1 KiB loads, two stages each
+    static constexpr int SCALES = CODE_DMA * 1024;
+    static constexpr int ZEROS = SCALES + 256;
+    static constexpr int BYTES = ZEROS + 256;
+    static constexpr int DMA = CODE_DMA + 2;       // vector-memory loads per item
 };
 
-// A operands of one set of 4 groups for the lane (token t, group g, k-slice
-// j): its 32 inputs 32 j .. 32 j + 31 of group g, block b = 16-input run
-// 2 j + b / 2, half b % 2, register v = (x[v'], x[v' + 8]) of the run's half.
-__device__ __forceinline__ void act_operands(const rsrc_t &xs, uint32_t off, u32x4 (&a)[4])
+// Workgroups per CU: two where a wave needs at most 128 VGPRs (up to 2 sets
+// of 4 groups per wave: 16 waves per CU give the slow-issue integer work of
+// the code operands more waves to pair with), one otherwise. The rings share
+// the CU's 160 KiB of LDS with the reduction buffers accordingly.
+constexpr int wgs_per_cu(int spw) { return spw <= 2 ? 2 : 1; }
+constexpr int ring_bytes(int spw) { return wgs_per_cu(spw) == 2 ? 64 * 1024 : 120 * 1024; }
+
+// Ring depth: as deep as the 6-bit vmcnt counter (all in-flight items'
+// loads) and the LDS for the 8 waves' rings allow, at most 16.
+template <int K, int SPW>
+constexpr int depth_for()
 {
-    u32x4 run[4];   // x[32 j .. +7], [+8 .. +15], [+16 .. +23], [+24 .. +31]
-#pragma unroll
-    for (int i = 0; i < 4; ++i) run[i] = __builtin_amdgcn_raw_buffer_load_b128(xs, off + 16 * i, 0, 0);
+    constexpr int by_count = 63 / ItemSlot<K>::DMA;
+    constexpr int by_lds = ring_bytes(SPW) / (kWaves * ItemSlot<K>::BYTES);
+    constexpr int d = by_count < by_lds ? by_count : by_lds;
+    return d < 16 ? d : 16;
+}
+
+// A operands of one set of 4 groups for the lane (token t, group g, k-slice
+// j) from its 32 inputs 32 j .. 32 j + 31 of group g, as four runs of 8
+// (x[32 j .. +7], [+8 .. +15], [+16 .. +23], [+24 .. +31]): block b = 16-input
+// run 2 j + b / 2, half b % 2, register v = (x[v'], x[v' + 8]) of the run's
+// half.
+__device__ __forceinline__ void act_operands(const u32x4 (&run)[4], u32x4 (&a)[4])
+{
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
         const u32x4 &lo = run[2 * (b >> 1)], &hi = run[2 * (b >> 1) + 1];
@@ -108,6 +131,39 @@ __device__ __forceinline__ void act_operands(const rsrc_t &xs, uint32_t off, u32
     }
 }
 
+// Activation run loaded behind the compiler's back: the loads are issued
+// before the ring's first DMA loads and waited for explicitly, so that the
+// wait does not also drain the ring (a compiler-visible load would be
+// followed by a full drain, as the compiler does not count the DMA loads).
+// The value is only read after wait_runs.
+__device__ __forceinline__ u32x4 load_run(const u32x4 &desc, uint32_t voff)
+{
+    u32x4 v;
+    asm volatile("buffer_load_dwordx4 %0, %1, %2, 0 offen" : "=v"(v) : "v"(voff), "s"(desc));
+    return v;
+}
+
+// Wait until at most N vector-memory loads are in flight, with the runs as
+// operands, so that no use of them can move above the wait.
+template <int N, int SPW>
+__device__ __forceinline__ void wait_runs(u32x4 (&run)[SPW][4])
+{
+    if constexpr (SPW == 1) {
+        asm volatile("s_waitcnt vmcnt(%4)"
+                     : "+v"(run[0][0]), "+v"(run[0][1]), "+v"(run[0][2]), "+v"(run[0][3])
+                     : "n"(N) : "memory");
+    } else {
+        asm volatile("s_waitcnt vmcnt(%4)"
+                     : "+v"(run[0][0]), "+v"(run[0][1]), "+v"(run[0][2]), "+v"(run[0][3])
+                     : "n"(N) : "memory");
+#pragma unroll
+        for (int s = 1; s < SPW; ++s)
+            asm volatile(""
+                         : "+v"(run[s][0]), "+v"(run[s][1]), "+v"(run[s][2]), "+v"(run[s][3])
+                         :: "memory");
+    }
+}
+
 // Workgroup: 8 waves share each 4-row tile, wave w taking sets
 // w SPW .. w SPW + SPW - 1 of its 8 SPW sets of 4 groups (so the waves of a
 // workgroup read whole rows together); a batch of up to 8 consecutive tiles
@@ -115,12 +171,15 @@ __device__ __forceinline__ void act_operands(const rsrc_t &xs, uint32_t off, u32
 constexpr int kBatch = 8;
 
 template <int K, int D, int SPW, bool DEF>
-__global__ __launch_bounds__(64 * kWaves) void decode_kernel(
+__global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int n_tokens, float *__restrict__ Y,
     int zero_point, int scale_type, int batch)
 {
+    using L = ItemSlot<K>;
+    // the waves' item rings
+    __shared__ __attribute__((aligned(16))) char ring[kWaves][D][L::BYTES];
     // partial row sums: [buffer][wave][tile of the batch][token][row]
     __shared__ float red[2][kWaves][kBatch][16];
     const int lane = threadIdx.x & 63;
@@ -139,70 +198,90 @@ __global__ __launch_bounds__(64 * kWaves) void decode_kernel(
     const uint32_t row_bytes = (uint32_t)(cols / 4);
     const uint32_t plane_bytes = (uint32_t)plane_words * 4;
     const uint32_t sbytes = scale_type == kScaleF32 ? 4 : 2;
-    const rsrc_t rc = make_rsrc(codes, (uint32_t)K * plane_bytes);
-    const rsrc_t rs = make_rsrc(scales, (uint32_t)K * (uint32_t)plane_groups * sbytes);
-    const rsrc_t rz = make_rsrc(sym ? nullptr : zeros, sym ? 0u : (uint32_t)K * (uint32_t)plane_groups * 4);
-    const rsrc_t rnone = make_rsrc(codes, 0u);
+    const u32x4 dc = make_desc(codes, (uint32_t)K * plane_bytes);
+    const u32x4 ds = make_desc(scales, (uint32_t)K * (uint32_t)plane_groups * sbytes);
+    const u32x4 dz = make_desc(sym ? nullptr : zeros,
+                               sym ? 0u : (uint32_t)K * (uint32_t)plane_groups * 4);
+    const u32x4 dnone = make_desc(codes, 0u);
     const uint32_t set0 = (uint32_t)wave * SPW;
-    // Codes are loaded coalesced: lane l takes bytes 8 (l % 16) of row l / 16
-    // of the set's 4 rows x 128 bytes, and a cross-lane permutation moves
-    // each 8-byte piece to the lane that uses it (row r, group gb, slice j),
-    // i.e. from lane 16 r + 4 gb + j.
-    const uint32_t lane_code = (uint32_t)j * row_bytes + set0 * 128 + 8 * (uint32_t)n;
-    const int perm_src = 4 * (int)(16 * r + 4 * gb + (uint32_t)j);   // ds_bpermute byte address
-    const uint32_t lane_grp = r * gpr + set0 * 4 + gb;
+
+    // DMA lane offsets within an item. Codes: lane l fills bytes 16 l of a
+    // 1 KiB load, i.e. stage 2 i + l / 32, row (l % 32) / 8, bytes
+    // 16 (l % 8) .. + 15 of the set's 128-byte run of the row (a stage past
+    // K - 1 reads past the descriptor, or other data that is never read).
+    const uint32_t dma_code = (uint32_t)((lane & 31) >> 3) * row_bytes +
+                              (uint32_t)(lane & 7) * 16 + (uint32_t)(lane >> 5) * plane_bytes;
+    // Scales and zero-points: lane l -> stage l / 16, row (l % 16) / 4, group
+    // l % 4 of the set; lanes of stages past K - 1 read nothing.
+    const uint32_t pst = (uint32_t)lane >> 4;
+    const uint32_t pgrp = ((uint32_t)(lane & 15) >> 2) * gpr + (uint32_t)(lane & 3) +
+                          pst * (uint32_t)plane_groups;
+    const uint32_t dma_scale = pst < (uint32_t)K ? pgrp * sbytes : kSkip;
+    const uint32_t dma_zero = pst < (uint32_t)K ? pgrp * 4 : kSkip;
+
+    const uint32_t lds_ring = lds_address(&ring[wave][0][0]);
+    const char *my_ring = &ring[wave][0][0];
 
     const int64_t n_tiles = (rows + 3) / 4;
     const int64_t n_batches = (n_tiles + batch - 1) / batch;
     const int my_batches = blockIdx.x < n_batches
                                ? (int)((n_batches - 1 - blockIdx.x) / gridDim.x + 1) : 0;
-    const int per_batch = batch * SPW;                 // items per batch
-    const int total = my_batches * per_batch;
+    const int my_tiles = my_batches * batch;
+    const int total = my_tiles * SPW;                  // items
 
-    // Loads of item it: batch it / per_batch, tile (it % per_batch) / SPW of
-    // it, set it % SPW of this wave's. Items past the end, and tiles past the
-    // last row, load from an empty resource (no memory access).
-    auto issue = [&](int it, Item<K> &dst) {
-        const int bi = it / per_batch, rest = it % per_batch;
-        const int64_t tile = ((int64_t)blockIdx.x + (int64_t)bi * gridDim.x) * batch + rest / SPW;
-        const uint32_t set = (uint32_t)(rest % SPW);
+    // DMA of item it (tile it / SPW of this workgroup's sequence, set
+    // it % SPW of this wave's) into slot it % D. Items past the end, and
+    // tiles past the last row, read through an empty descriptor (no memory
+    // access, zeros in the slot): every item issues the same loads.
+    auto issue = [&](int it) {
+        const int ti = it / SPW;
+        const int64_t tile = ((int64_t)blockIdx.x + (int64_t)(ti / batch) * gridDim.x) * batch +
+                             ti % batch;
+        const uint32_t set = set0 + (uint32_t)(it % SPW);
         const bool live = it < total && tile < n_tiles;
-        const uint32_t code_off = live ? (uint32_t)(tile * 4) * row_bytes + set * 128 + lane_code : 0u;
-        const uint32_t grp = live ? (uint32_t)(tile * 4) * gpr + set * 4 + lane_grp : 0u;
-        const rsrc_t c_src = live ? rc : rnone, s_src = live ? rs : rnone, z_src = live ? rz : rnone;
+        const uint32_t code_base = live ? (uint32_t)(tile * 4) * row_bytes + set * 128 : 0u;
+        const uint32_t grp_base = live ? (uint32_t)(tile * 4) * gpr + set * 4 : 0u;
+        const uint32_t lds = lds_ring + (uint32_t)(it % D) * L::BYTES;
+        const u32x4 c_src = live ? dc : dnone, s_src = live ? ds : dnone,
+                    z_src = live ? dz : dnone;
+        // the reads of the item that used this slot have completed
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int st = 0; st < K; ++st) {
-            dst.c[st] = __builtin_amdgcn_raw_buffer_load_b64(c_src, code_off, st * plane_bytes, 0);
-            if (DEF || scale_type == kScaleF32)
-                dst.s[st] = __builtin_amdgcn_raw_buffer_load_b32(
-                    s_src, grp * 4, st * (uint32_t)plane_groups * 4, 0);
-            else
-                dst.s[st] = __builtin_amdgcn_raw_buffer_load_b16(
-                    s_src, grp * 2, st * (uint32_t)plane_groups * 2, 0);
-            dst.z[st] = __builtin_amdgcn_raw_buffer_load_b32(
-                z_src, grp * 4, st * (uint32_t)plane_groups * 4, 0);
-        }
+        for (int i = 0; i < L::CODE_DMA; ++i)
+            dma_x4(c_src, code_base + 2u * i * plane_bytes, lds + 1024u * i, dma_code);
+        if (DEF || scale_type == kScaleF32)
+            dma_dword(s_src, grp_base * 4, lds + L::SCALES, dma_scale);
+        else
+            dma_ushort(s_src, grp_base * 2, lds + L::SCALES, dma_scale);
+        dma_dword(z_src, grp_base * 4, lds + L::ZEROS, dma_zero);
     };
 
-    Item<K> ring[D];
-#pragma unroll
-    for (int d = 0; d < D; ++d) issue(d, ring[d]);
-
-    // A operands and group sums of this wave's sets (fixed for the whole
-    // kernel, loaded once the first items' loads are in flight): lane as A
-    // row = token ta (tokens past n_tokens repeat the last one), group ga of
-    // the set.
+    // Activations first (the lane as A row: token ta, tokens past n_tokens
+    // repeating the last one, group ga of each of its sets), then the ring.
     const uint32_t ta = (uint32_t)((n >> 2) < n_tokens ? (n >> 2) : n_tokens - 1);
     const uint32_t ga = n & 3;
-    u32x4 a[SPW][4];
-    f32x4 sx[SPW];
+    u32x4 run[SPW][4];
     {
-        const rsrc_t xs = make_rsrc(X, (uint32_t)n_tokens * (uint32_t)cols * 2);
-        const u32x4 ones = {one, one, one, one};
+        const u32x4 xs = make_desc(X, (uint32_t)n_tokens * (uint32_t)cols * 2);
 #pragma unroll
         for (int s = 0; s < SPW; ++s) {
             const uint32_t gi = ((uint32_t)wave * SPW + s) * 4 + ga;
-            act_operands(xs, ta * (uint32_t)cols * 2 + gi * 256 + 64 * (uint32_t)j, a[s]);
+            const uint32_t off = ta * (uint32_t)cols * 2 + gi * 256 + 64 * (uint32_t)j;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) run[s][i] = load_run(xs, off + 16 * i);
+        }
+    }
+#pragma unroll
+    for (int d = 0; d < D; ++d) issue(d);
+    wait_runs<D * L::DMA>(run);
+
+    u32x4 a[SPW][4];
+    f32x4 sx[SPW];
+    {
+        const u32x4 ones = {one, one, one, one};
+#pragma unroll
+        for (int s = 0; s < SPW; ++s) {
+            act_operands(run[s], a[s]);
             // Sx: C rows 4 j + i = token j, group i of the set
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -211,94 +290,80 @@ __global__ __launch_bounds__(64 * kWaves) void decode_kernel(
         }
     }
 
-
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     int n_red = 0;
-    for (int base = 0; base < total; base += D) {
+    for (int ti = 0; ti < my_tiles; ++ti) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int d = 0; d < D; ++d) {
-            const int it = base + d;
-            if (it >= total) break;
-            const int rest = it % per_batch;
-            const int set = rest % SPW;
-            const Item<K> &cur = ring[d];
+        for (int set = 0; set < SPW; ++set) {
+            const int it = ti * SPW + set;
+            // this item's loads have landed; the next D - 1 items' may not
+            wait_vm<(D - 1) * L::DMA>();
+            const char *slot = my_ring + (it % D) * L::BYTES;
             float c = 0.0f;
 #pragma unroll
             for (int st = 0; st < K; ++st) {
-                const uint32_t w0 = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_src, (int)cur.c[st][0]);
-                const uint32_t w1 = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_src, (int)cur.c[st][1]);
+                const u32x2 w = *reinterpret_cast<const u32x2 *>(
+                    slot + 1024 * (st >> 1) + 512 * (st & 1) + r * 128 + gb * 32 + j * 8);
                 u32x4 b[4];
-                word_operands(w0, mask, one, b[0], b[1]);
-                word_operands(w1, mask, one, b[2], b[3]);
+                word_operands(w[0], mask, one, b[0], b[1]);
+                word_operands(w[1], mask, one, b[2], b[3]);
                 f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    // the set index is wave-uniform and SPW is small: select
-                    // the A operand without indexing registers dynamically
-                    u32x4 aq = a[0][q];
-#pragma unroll
-                    for (int s2 = 1; s2 < SPW; ++s2)
-                        if (set == s2) aq = a[s2][q];
-                    p = mfma(aq, b[q], p);
-                }
+                for (int q = 0; q < 4; ++q) p = mfma(a[set][q], b[q], p);
+                const uint32_t sw = *reinterpret_cast<const uint32_t *>(slot + L::SCALES + 4 * (16 * st + n));
+                const uint32_t zw = *reinterpret_cast<const uint32_t *>(slot + L::ZEROS + 4 * (16 * st + n));
                 float s, z;
                 if constexpr (DEF) {
-                    s = __uint_as_float(cur.s[st]);
-                    z = __uint_as_float(cur.z[st]);
+                    s = __uint_as_float(sw);
+                    z = __uint_as_float(zw);
                 } else {
-                    s = scale_type == kScaleF32 ? __uint_as_float(cur.s[st])
+                    s = scale_type == kScaleF32 ? __uint_as_float(sw)
                         : scale_type == kScaleF16
-                            ? (float)__builtin_bit_cast(_Float16, (uint16_t)(cur.s[st] & 0xFFFFu))
-                            : __uint_as_float(cur.s[st] << 16);
-                    z = sym ? 2.0f : __uint_as_float(cur.z[st]);
+                            ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
+                            : __uint_as_float(sw << 16);
+                    z = sym ? 2.0f : __uint_as_float(zw);
                 }
                 const float s4 = 4.0f * s;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
                 c = __builtin_fmaf(s, 4.0f + z, c);
             }
-            f32x4 sxs = sx[0];
 #pragma unroll
-            for (int s2 = 1; s2 < SPW; ++s2)
-                if (set == s2) sxs = sx[s2];
+            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sx[set][i], acc[i]);
+            // the slot is free: refill it with the item D ahead
+            issue(it + D);
+        }
+        // end of this wave's share of the tile: its diagonal entry (token j,
+        // row r, group gb) summed over the 4 groups of the lanes
+        // n = 4 r .. 4 r + 3, kept for the batch reduction
+        float y = gb == 0 ? acc[0] : gb == 1 ? acc[1] : gb == 2 ? acc[2] : acc[3];
+        y += __shfl_xor(y, 1, 64);
+        y += __shfl_xor(y, 2, 64);
+        const int tt = ti % batch;
+        if (gb == 0) red[n_red & 1][wave][tt][4 * j + r] = y;
+        if (tt == batch - 1) {
+            // end of the batch: sum the waves' partial sums in wave order
+            // and store. The buffer written here is next written two batches
+            // later, after a barrier that the summing threads reach only once
+            // they have read it.
+            __syncthreads();
+            const int tid = threadIdx.x;
+            if (tid < batch * 16) {
+                const int tb = tid / 16, e = tid % 16;   // e = 4 token + row
+                float out = red[n_red & 1][0][tb][e];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sxs[i], acc[i]);
-            // reuse the slot for the item D ahead
-            issue(it + D, ring[d]);
-
-            if (set == SPW - 1) {
-                // end of this wave's share of a tile: its diagonal entry
-                // (token j, row r, group gb) summed over the 4 groups of the
-                // lanes n = 4 r .. 4 r + 3, kept for the batch reduction
-                float y = gb == 0 ? acc[0] : gb == 1 ? acc[1] : gb == 2 ? acc[2] : acc[3];
-                y += __shfl_xor(y, 1, 64);
-                y += __shfl_xor(y, 2, 64);
-                const int ti = rest / SPW;
-                if (gb == 0) red[n_red & 1][wave][ti][4 * j + r] = y;
-                acc = (f32x4){0.f, 0.f, 0.f, 0.f};
-                if (rest == per_batch - 1) {
-                    // end of the batch: sum the waves' partial sums in wave
-                    // order and store. The buffer written here is next
-                    // written two batches later, after a barrier that the
-                    // summing threads reach only once they have read it.
-                    __syncthreads();
-                    const int tid = threadIdx.x;
-                    if (tid < batch * 16) {
-                        const int tt = tid / 16, e = tid % 16;   // e = 4 token + row
-                        float out = red[n_red & 1][0][tt][e];
-#pragma unroll
-                        for (int w = 1; w < kWaves; ++w) out += red[n_red & 1][w][tt][e];
-                        const int bi = it / per_batch;
-                        const int64_t tile = ((int64_t)blockIdx.x + (int64_t)bi * gridDim.x) * batch + tt;
-                        const int64_t o = tile * 4 + (e & 3);
-                        const int tok = e >> 2;
-                        if (tok < n_tokens && o < rows) Y[(int64_t)tok * rows + o] = out;
-                    }
-                    ++n_red;
-                }
+                for (int w = 1; w < kWaves; ++w) out += red[n_red & 1][w][tb][e];
+                const int64_t tile =
+                    ((int64_t)blockIdx.x + (int64_t)(ti / batch) * gridDim.x) * batch + tb;
+                const int64_t o = tile * 4 + (e & 3);
+                const int tok = e >> 2;
+                if (tok < n_tokens && o < rows) Y[(int64_t)tok * rows + o] = out;
             }
+            ++n_red;
         }
     }
+    // no DMA load may still write this workgroup's LDS once it ends
+    wait_vm<0>();
 }
 
 template <typename... Args>
@@ -309,16 +374,12 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-// Items in flight per wave: as many as keep all their loads (3 K per item)
-// within the 6-bit vmcnt counter, at most 8.
-constexpr int depth_for(int K) { return 63 / (3 * K) < 8 ? 63 / (3 * K) : 8; }
-
 template <int K, int SPW, bool DEF>
 hipError_t launch_k(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int zp, int sdt, const uint16_t *X, int n_tokens, float *Y,
                     int grid, int batch, hipStream_t stream)
 {
-    constexpr int D = depth_for(K);
+    constexpr int D = depth_for<K, SPW>();
     return launch(decode_kernel<K, D, SPW, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros,
                   rows, cols, rows * cols / 16, rows * cols / 128, X, n_tokens, Y, zp, sdt, batch);
 }
@@ -355,12 +416,17 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
 
 bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens)
 {
-    // Measured crossover: with one stage the items are too small to amortise
-    // their loads of scales and zero-points, and below about 6144 rows a
-    // wave gets too few items to amortise the kernel's start (activations,
-    // group sums, first loads); the general kernel is faster there.
-    return G == 128 && k >= 2 && rows >= 6144 && n_tokens >= 1 && n_tokens <= 4 &&
-           cols % 4096 == 0 && cols / 4096 <= kDecodeMaxSetsPerWave;
+    if (G != 128 || n_tokens < 1 || n_tokens > 4 || cols % 4096 != 0 ||
+        cols / 4096 > kDecodeMaxSetsPerWave)
+        return false;
+    // Measured crossover against the general kernel (one token, packages
+    // read from HBM): from 3 stages this form is faster on every shape; with
+    // 2 stages an item is small, and for 1025 to 6143 rows its per-item and
+    // start-up work (activations, group sums, the ring's first loads) costs
+    // more than the general kernel's less efficient loads; with 1 stage the
+    // general kernel is faster everywhere.
+    if (k >= 3) return true;
+    return k == 2 && (rows >= 6144 || rows <= 1024);
 }
 
 hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const float *zeros,
@@ -369,13 +435,14 @@ hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const
                                 hipStream_t stream)
 {
     const char *sc = static_cast<const char *>(scales);
-    // Batches of up to 8 tiles, sized so that every workgroup (one per CU)
-    // gets the same number of batches: R rounds of cus batches.
+    // Batches of up to 8 tiles, sized so that every resident workgroup
+    // gets the same number of batches: R rounds of one batch per workgroup.
+    const int64_t slots = (int64_t)cus * wgs_per_cu((int)(cols / 4096));
     const int64_t tiles = (rows + 3) / 4;
-    const int64_t rounds = (tiles + (int64_t)cus * kBatch - 1) / ((int64_t)cus * kBatch);
-    const int64_t batch = (tiles + (int64_t)cus * rounds - 1) / ((int64_t)cus * rounds);
+    const int64_t rounds = (tiles + slots * kBatch - 1) / (slots * kBatch);
+    const int64_t batch = (tiles + slots * rounds - 1) / (slots * rounds);
     const int64_t batches = (tiles + batch - 1) / batch;
-    const int grid = (int)(batches < cus ? batches : cus);
+    const int grid = (int)(batches < slots ? batches : slots);
     const int nt = (int)n_tokens;
     const bool def = scale_type == kScaleF32 && zero_point != kZpSymmetric;
     return def ? launch_d<true>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, nt, Y,

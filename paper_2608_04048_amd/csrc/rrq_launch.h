@@ -37,9 +37,10 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
                          int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
                          hipStream_t stream);
 
-// The decode form of the linear layer (up to 4 tokens, groups of 128, at
-// least 2 stages and 6144 rows, cols a multiple of 4096 up to 4096
-// kDecodeMaxSetsPerWave); launch_linear covers every other case.
+// The decode form of the linear layer (up to 4 tokens, groups of 128, cols
+// a multiple of 4096 up to 4096 kDecodeMaxSetsPerWave, and the stage counts
+// and row counts where it is the faster one: linear_decode_fits);
+// launch_linear covers every other case.
 constexpr int kDecodeMaxSetsPerWave = 4;
 bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens);
 hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const float *zeros,

@@ -41,6 +41,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rrq_dma.h"
 #include "rrq_launch.h"
 
 namespace rrq_detail {
@@ -51,12 +52,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr uint32_t kRsrcWord3 = 0x00020000u;
 constexpr uint32_t kOnePair = 0x3F803F80u;    // two bfloat16 1.0
 constexpr uint32_t kCodeMask = 0x00600060u;   // top two mantissa bits of both halves
-// Offset added to an activation load that must not touch memory: past the
-// activation buffer's size (below 2^30 bytes), so it reads zeros.
-constexpr uint32_t kSkip = 0x80000000u;
 
 // Package stage format (values of the C ABI's enums).
 constexpr int kZpSymmetric = 2;
@@ -108,72 +105,6 @@ struct Chunk {
         return (TT == 4 ? 4 * tk : tk) & (X_SLOTS - 1);
     }
 };
-
-// Raw buffer descriptor (gfx9 family): accesses at or beyond bytes read zero.
-__device__ __forceinline__ u32x4 make_desc(const void *base, uint32_t bytes)
-{
-    const uint64_t a = reinterpret_cast<uint64_t>(base);
-    u32x4 d;
-    d[0] = (uint32_t)a;
-    d[1] = (uint32_t)(a >> 32) & 0xFFFFu;
-    d[2] = bytes;
-    d[3] = kRsrcWord3;
-    return d;
-}
-
-// LDS-DMA loads: every lane reads from the buffer at byte offset
-// soff + voff (both range-checked against the descriptor's size) and the
-// wave writes LDS at lds + lane * 16 (dwordx4) or lds + lane * 4 (dword,
-// ushort). lds is a wave-uniform LDS byte address. m0, which carries it, is
-// restored. The wait states the compiler cannot see inside the block are
-// explicit: 5 before the load reads SGPRs that a VALU instruction may have
-// just written, 1 after writing m0.
-__device__ __forceinline__ void dma_x4(const u32x4 &desc, uint32_t soff, uint32_t lds,
-                                       uint32_t voff)
-{
-    uint32_t m0;
-    asm volatile("s_nop 4\n\t"
-                 "s_mov_b32 %0, m0\n\t"
-                 "s_mov_b32 m0, %2\n\t"
-                 "s_nop 0\n\t"
-                 "buffer_load_dwordx4 %1, %3, %4 offen lds\n\t"
-                 "s_mov_b32 m0, %0"
-                 : "=&s"(m0) : "v"(voff), "s"(lds), "s"(desc), "s"(soff) : "memory");
-}
-
-__device__ __forceinline__ void dma_dword(const u32x4 &desc, uint32_t soff, uint32_t lds,
-                                          uint32_t voff)
-{
-    uint32_t m0;
-    asm volatile("s_nop 4\n\t"
-                 "s_mov_b32 %0, m0\n\t"
-                 "s_mov_b32 m0, %2\n\t"
-                 "s_nop 0\n\t"
-                 "buffer_load_dword %1, %3, %4 offen lds\n\t"
-                 "s_mov_b32 m0, %0"
-                 : "=&s"(m0) : "v"(voff), "s"(lds), "s"(desc), "s"(soff) : "memory");
-}
-
-__device__ __forceinline__ void dma_ushort(const u32x4 &desc, uint32_t soff, uint32_t lds,
-                                           uint32_t voff)
-{
-    uint32_t m0;
-    asm volatile("s_nop 4\n\t"
-                 "s_mov_b32 %0, m0\n\t"
-                 "s_mov_b32 m0, %2\n\t"
-                 "s_nop 0\n\t"
-                 "buffer_load_ushort %1, %3, %4 offen lds\n\t"
-                 "s_mov_b32 m0, %0"
-                 : "=&s"(m0) : "v"(voff), "s"(lds), "s"(desc), "s"(soff) : "memory");
-}
-
-// Wait until at most N of the wave's vector-memory instructions are in
-// flight.
-template <int N>
-__device__ __forceinline__ void wait_vm()
-{
-    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
-}
 
 __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x4 &c)
 {

@@ -1,6 +1,7 @@
-"""GPU parity of rrq_linear's decode form (up to 4 tokens, groups of 128, at
-least 2 stages and 6144 rows, cols a multiple of 4096), through the C ABI,
-against the oracle's Eq. 20 product in float64 on sampled output rows.
+"""GPU parity of rrq_linear's decode form (up to 4 tokens, groups of 128,
+cols a multiple of 4096 up to 16384; 3 or 4 stages at any row count, 2
+stages from 6144 rows and up to 1024 rows), through the C ABI, against the
+oracle's Eq. 20 product in float64 on sampled output rows.
 
 * exact: power-of-two scales, integer or dyadic zero-points and
   small-integer activations make every intermediate exactly representable,
@@ -33,8 +34,8 @@ def _log(msg):
 
 def _sample_rows(rows, seed):
     rng = np.random.default_rng(seed)
-    idx = np.unique(np.concatenate([np.arange(8), np.arange(rows - 8, rows),
-                                    rng.choice(rows, 256, replace=False)]))
+    idx = np.unique(np.concatenate([np.arange(min(8, rows)), np.arange(max(rows - 8, 0), rows),
+                                    rng.choice(rows, min(256, rows), replace=False)]))
     return idx
 
 
@@ -58,6 +59,9 @@ def _run(gpu, codes, s, z, rows, cols, k, xb, zp=None, sd=None, s_raw=None):
 @pytest.mark.parametrize("rows,cols,M,k", [
     (6144, 4096, 1, 2), (6144, 4096, 4, 4), (6150, 8192, 3, 3), (6147, 12288, 2, 4),
     (8192, 16384, 1, 2), (24576, 4096, 4, 3),
+    # few tiles (fewer workgroups than CUs), ragged last tile, small matrices
+    (1, 4096, 1, 3), (5, 4096, 2, 4), (1023, 4096, 1, 4), (1021, 4096, 4, 2), (2047, 4096, 4, 2),
+    (4096, 4096, 1, 3), (4099, 8192, 2, 4), (1024, 16384, 1, 3),
 ])
 def test_decode_form_exact(gpu, rows, cols, M, k):
     _log(f"decode exact rows={rows} cols={cols} M={M} k={k}")
