@@ -228,6 +228,67 @@ def time_linear(w, W_flat, codes, scales, zeros, stream, tokens=(1, 16), ks=(1, 
     return out
 
 
+def time_linear_shape(rows, cols, ks, tokens, G=128, S=4, min_bytes=600 << 20, replays=7):
+    """rrq_linear on one weight shape, as a decode loop meets it: P distinct
+    packages (seeded Gaussian weights, together at least min_bytes, so that
+    every call reads its package from HBM rather than the 256 MB MALL), one
+    call per package captured in a HIP graph; the graph is replayed and timed
+    with HIP events. Returns per-call microseconds and algorithmic HBM
+    bytes per call for every (tokens, k)."""
+    import torch
+
+    import paper_2608_04048_amd as rrq
+
+    n = rows * cols
+    P = max(2, min(64, min_bytes // (S * n // 4 + 8 * S * n // G) + 1))
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2608)
+    W = (torch.randn(n, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    stream = torch.cuda.current_stream()
+    pks = []
+    for _ in range(P):
+        c = torch.empty((S, n // 16), dtype=torch.int32, device="cuda")
+        sc = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+        zz = torch.empty((S, n // G), dtype=torch.float32, device="cuda")
+        rrq.rrq_construct(W, rows, cols, G, S, c, sc, zz, stream)
+        pks.append((c, sc, zz))
+    max_m = max(tokens)
+    X = torch.randn((max_m, cols), generator=g, device="cuda").to(torch.bfloat16)
+    Y = torch.empty((P, max_m * rows), dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    out = {"metric": "rrq_linear per-call time", "rows": rows, "cols": cols, "group_size": G,
+           "packages": P, "results": {}}
+    cs = torch.cuda.Stream()
+    for M in tokens:
+        for k in ks:
+            def run(st, M=M, k=k):
+                for j, (c, sc, zz) in enumerate(pks):
+                    rrq.rrq_linear(c, sc, zz, rows, cols, G, S, k, X, M, Y[j], st)
+            run(stream)
+            cs.wait_stream(stream)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=cs):
+                run(cs)
+            stream.wait_stream(cs)
+            ms = []
+            for _ in range(replays):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                with torch.cuda.stream(stream):
+                    graph.replay()
+                b.record(stream)
+                b.synchronize()
+                ms.append(a.elapsed_time(b))
+            del graph
+            us = sorted(ms)[len(ms) // 2] * 1e3 / P
+            nbytes = k * n // 4 + 8 * k * (n // G) + 2 * M * cols + 4 * M * rows
+            out["results"][f"M{M}_k{k}"] = {
+                "us_per_call": round(us, 2), "bytes_per_call": nbytes,
+                "hbm_gbs": round(nbytes / (us * 1e-6) / 1e9, 1),
+                "hbm_frac": round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    return out
+
+
 def format_bytes(n, G, S, zero_point, scale_type):
     """Algorithmic HBM bytes of one construct launch in a stage format:
     bf16 in, codes, scales (4 or 2 bytes) and zeros (none if symmetric)."""
@@ -408,6 +469,14 @@ def main():
                     help="skip timing rrq_linear (decode passes over every tensor)")
     ap.add_argument("--no-stream-probe", action="store_true",
                     help="skip the 2 : 1.25 read/write streaming probe")
+    ap.add_argument("--linear-shape", default="", metavar="RxC",
+                    help="instead of the benchmark, time rrq_linear on one weight shape: one "
+                         "call per package over enough distinct packages to exceed the 256 MB "
+                         "MALL, replayed as a HIP graph (per-call microseconds)")
+    ap.add_argument("--linear-k", default="4", metavar="K,...",
+                    help="prefix stage counts for --linear-shape")
+    ap.add_argument("--linear-tokens", default="1", metavar="M,...",
+                    help="token counts for --linear-shape")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device-to-device copy of MIB "
                          "MiB three times (calibrates profiler byte counters)")
@@ -433,6 +502,12 @@ def main():
         print(json.dumps({"copy_probe_bytes": src.numel() * 4, "copies": 3}), flush=True)
         return
     rrq.load_library()
+    if args.linear_shape:
+        rows, cols = (int(v) for v in args.linear_shape.lower().split("x"))
+        print(json.dumps(time_linear_shape(rows, cols, [int(k) for k in args.linear_k.split(",")],
+                                           [int(m) for m in args.linear_tokens.split(",")])),
+              flush=True)
+        return
     w = wl.workload(args.workload)
     G, S, n = w.group_size, w.n_stages, w.numel
     cols = w.tensors[0].cols

@@ -43,6 +43,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rrq_code_operands.h"
 #include "rrq_dma.h"
 #include "rrq_launch.h"
 
@@ -64,22 +65,6 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x
 {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-
-// B operands of the two blocks of one code word: register q (of 8) holds
-// codes q and q + 8 as 1 + code / 4; block 0 takes registers 0..3, block 1
-// registers 4..7.
-__device__ __forceinline__ void word_operands(uint32_t w, uint32_t mask, uint32_t one,
-                                              u32x4 &b0, u32x4 &b1)
-{
-    b0[0] = ((w << 5) & mask) | one;
-    b0[1] = ((w << 3) & mask) | one;
-    b0[2] = ((w << 1) & mask) | one;
-    b0[3] = ((w >> 1) & mask) | one;
-    b1[0] = ((w >> 3) & mask) | one;
-    b1[1] = ((w >> 5) & mask) | one;
-    b1[2] = ((w >> 7) & mask) | one;
-    b1[3] = ((w >> 9) & mask) | one;
 }
 
 // One item's LDS slot (a 4-row tile and a set of 4 groups, all K stages):
@@ -304,12 +289,11 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
             for (int st = 0; st < K; ++st) {
                 const u32x2 w = *reinterpret_cast<const u32x2 *>(
                     slot + 1024 * (st >> 1) + 512 * (st & 1) + r * 128 + gb * 32 + j * 8);
-                u32x4 b[4];
-                word_operands(w[0], mask, one, b[0], b[1]);
-                word_operands(w[1], mask, one, b[2], b[3]);
+                u32x4 b[2][2];
+                code_operands_pair(w[0], w[1], mask, one, b);
                 f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int q = 0; q < 4; ++q) p = mfma(a[set][q], b[q], p);
+                for (int q = 0; q < 4; ++q) p = mfma(a[set][q], b[q >> 1][q & 1], p);
                 const uint32_t sw = *reinterpret_cast<const uint32_t *>(slot + L::SCALES + 4 * (16 * st + n));
                 const uint32_t zw = *reinterpret_cast<const uint32_t *>(slot + L::ZEROS + 4 * (16 * st + n));
                 float s, z;

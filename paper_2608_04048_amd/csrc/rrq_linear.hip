@@ -41,6 +41,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "rrq_code_operands.h"
 #include "rrq_dma.h"
 #include "rrq_launch.h"
 
@@ -124,21 +125,6 @@ __device__ __forceinline__ u32x4 code_operand(uint32_t w, uint32_t mask, uint32_
     b[2] = ((w << 1) & mask) | one;
     b[3] = ((w >> 1) & mask) | one;
     return b;
-}
-
-// The same for both halves of two words at once (G = 128: the lane's two
-// words of a group), with 64-bit shifts: the bits one word's shift carries
-// into the other land outside the mask. b[h][v] is word v, half h.
-__device__ __forceinline__ void code_operands2(uint32_t w0, uint32_t w1, uint32_t mask,
-                                               uint32_t one, u32x4 (&b)[2][2])
-{
-    const uint64_t w = ((uint64_t)w1 << 32) | w0;
-    const uint64_t s[8] = {w << 5, w << 3, w << 1, w >> 1, w >> 3, w >> 5, w >> 7, w >> 9};
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        b[q >> 2][0][q & 3] = ((uint32_t)s[q] & mask) | one;
-        b[q >> 2][1][q & 3] = ((uint32_t)(s[q] >> 32) & mask) | one;
-    }
 }
 
 // A operand of one block from two runs of 4 activations (inputs p0 .. p0 + 3
@@ -318,9 +304,9 @@ __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int
                 const u32x2 w = *reinterpret_cast<const u32x2 *>(
                     row + 16 * ((2 * q + (j >> 1)) ^ cs) + 8 * (j & 1));
                 u32x4 bop[2][2];
-                code_operands2(w[0], w[1], mask, one, bop);
+                code_operands_pair(w[0], w[1], mask, one, bop);
 #pragma unroll
-                for (int b = 0; b < NB; ++b) pq = mfma(a[b], bop[b & 1][b >> 1], pq);
+                for (int b = 0; b < NB; ++b) pq = mfma(a[b], bop[b >> 1][b & 1], pq);
             } else if constexpr (G == 64) {
                 const uint32_t word = *reinterpret_cast<const uint32_t *>(row + 16 * (q ^ cs) + 4 * j);
 #pragma unroll
