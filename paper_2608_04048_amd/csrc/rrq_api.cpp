@@ -115,10 +115,12 @@ int reconstruct_common(const uint32_t *codes, const void *scales, const float *z
     if (!aligned(codes, 16) || !aligned(W_out, 16)) return RRQ_ERR_ALIGN;
     const int64_t n_groups = n / group_size;
     int grid = 0;
-    // one wave tile = 64 lanes x 4 chunks x (8 or 4) elements; 4 waves per workgroup
-    const int per_lane = rrq_detail::kReconstructChunksBF16 * 8;
-    st = grid_for(n, rrq_detail::kReconstructThreads * per_lane, rrq_detail::kReconstructBlocksPerCU,
-                  &grid);
+    // one wave tile = 64 lanes x (4 or 8) chunks x (8 or 4) elements; 4 waves
+    // per workgroup
+    const bool bf16 = out_dtype == RRQ_BF16;
+    const int per_lane = rrq_detail::reconstruct_chunks(k_stages, bf16) * (bf16 ? 8 : 4);
+    st = grid_for(n, rrq_detail::kReconstructThreads * per_lane,
+                  rrq_detail::reconstruct_blocks_per_cu(k_stages, bf16), &grid);
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_reconstruct(codes, scales, zeros, n_groups, group_size,
                                                   n_stages, k_stages, W_out,

@@ -842,8 +842,7 @@ hipError_t launch_reconstruct_k(const uint32_t *codes, const char *scales, const
                                 int64_t n_elems, int64_t n_groups, int g_shift, void *out,
                                 int f16, int grid, hipStream_t stream)
 {
-    return launch(reconstruct_kernel<K, BF16, BF16 ? kReconstructChunksBF16 : kReconstructChunksF32,
-                                     SC16, SYM>,
+    return launch(reconstruct_kernel<K, BF16, reconstruct_chunks(K, BF16), SC16, SYM>,
                   grid, kReconstructThreads, stream, codes, scales, zeros, n_elems, n_groups,
                   g_shift, out, f16);
 }

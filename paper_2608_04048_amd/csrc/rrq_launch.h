@@ -58,11 +58,14 @@ constexpr int kMaxStages = 4;
 // Workgroups the construct kernel keeps resident per compute unit.
 constexpr int kConstructBlocksPerCU = 8;
 // Reconstruct: threads per workgroup (4 waves), 16-byte output chunks per
-// lane per tile (8 bfloat16 or 4 binary32 elements each), and resident
-// workgroups per CU.
+// lane per tile (8 bfloat16 or 4 binary32 elements each) and resident
+// workgroups per CU, as measured on the 36-layer stack (6.9e9 weights): 8
+// chunks per lane keep more loads in flight for 1 or 2 stages, 4 are faster
+// from 3 stages on (the loads of K stages x 8 chunks crowd the registers);
+// 2 workgroups per CU write faster than 8 (fewer concurrent write streams),
+// except for binary32 output from 3 stages on.
 constexpr int kReconstructThreads = 256;
-constexpr int kReconstructChunksBF16 = 4;
-constexpr int kReconstructChunksF32 = 4;
-constexpr int kReconstructBlocksPerCU = 8;
+constexpr int reconstruct_chunks(int k, bool bf16) { return (void)bf16, k <= 2 ? 8 : 4; }
+constexpr int reconstruct_blocks_per_cu(int k, bool bf16) { return bf16 || k <= 2 ? 2 : 8; }
 
 }  // namespace rrq_detail
