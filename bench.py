@@ -289,6 +289,28 @@ def time_linear_shape(rows, cols, ks, tokens, G=128, S=4, min_bytes=600 << 20, r
     return out
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def time_prefill(tokens=2048, ks=(4, 1),
+                 shapes=((4096, 4096, "q_proj/o_proj"), (12288, 4096, "gate_proj/up_proj"),
+                         (4096, 12288, "down_proj"))):
+    """rrq_linear at prefill size on the Qwen3-8B layer shapes (time_linear_shape),
+    against the bf16 matrix-core peak: the stage-sum form does k products of
+    2 M rows cols flops each (every stage on the matrix cores)."""
+    out = {"tokens": tokens}
+    for rows, cols, name in shapes:
+        r = time_linear_shape(rows, cols, list(ks), [tokens])
+        for key, v in r["results"].items():
+            k = int(key.split("_k")[1])
+            flops = 2.0 * tokens * rows * cols * k
+            tf = flops / (v["us_per_call"] * 1e-6) / 1e12
+            out[f"{rows}x{cols}_k{k}"] = {"proj": name, "us_per_call": v["us_per_call"],
+                                          "stage_tflops": round(tf, 1),
+                                          "mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+    return out
+
+
 def format_bytes(n, G, S, zero_point, scale_type):
     """Algorithmic HBM bytes of one construct launch in a stage format:
     bf16 in, codes, scales (4 or 2 bytes) and zeros (none if symmetric)."""
@@ -660,6 +682,8 @@ def main():
     if not args.no_linear:
         print("bench: timing rrq_linear decode passes", file=sys.stderr, flush=True)
         result["linear"] = time_linear(w, W.view(-1), codes, scales, zeros, stream)
+        print("bench: timing rrq_linear at prefill size", file=sys.stderr, flush=True)
+        result["prefill"] = time_prefill()
     if not args.no_stream_probe:
         result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
         result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)

@@ -148,13 +148,16 @@ int linear_common(const uint32_t *codes, const void *scales, const float *zeros,
     if (!aligned(codes, 16) || !aligned(X, 16) || !aligned(Y, 4)) return RRQ_ERR_ALIGN;
     const int cus = current_cu_count();
     if (cus <= 0) return RRQ_ERR_HIP;
-    hipError_t e = rrq_detail::linear_decode_fits(rows, cols, group_size, k_stages, n_tokens)
-                       ? rrq_detail::launch_linear_decode(codes, scales, zeros, rows, cols, k_stages,
-                                                          zero_point, scale_type, X, n_tokens, Y,
-                                                          cus, stream)
-                       : rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size,
-                                                   n_stages, k_stages, zero_point, scale_type, X,
-                                                   n_tokens, Y, stream);
+    hipError_t e;
+    if (rrq_detail::linear_decode_fits(rows, cols, group_size, k_stages, n_tokens))
+        e = rrq_detail::launch_linear_decode(codes, scales, zeros, rows, cols, k_stages, zero_point,
+                                             scale_type, X, n_tokens, Y, cus, stream);
+    else if (rrq_detail::linear_prefill_fits(rows, cols, group_size, n_tokens))
+        e = rrq_detail::launch_linear_prefill(codes, scales, zeros, rows, cols, k_stages,
+                                              zero_point, scale_type, X, n_tokens, Y, stream);
+    else
+        e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size, n_stages,
+                                      k_stages, zero_point, scale_type, X, n_tokens, Y, stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 

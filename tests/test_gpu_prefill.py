@@ -1,0 +1,137 @@
+"""GPU parity of rrq_linear's prefill form (groups of 128, at least 128 tokens),
+through the C ABI:
+
+* exact: power-of-two scales, integer or dyadic zero-points and
+  small-integer activations make every intermediate exactly representable,
+  so all outputs must equal the oracle's Eq. 20 product bit for bit (ragged
+  token and row tiles, one to many groups per row, every stage count and
+  format);
+* same order: the prefill form accumulates in the general kernel's order, so
+  on realistic packages its outputs equal, bit for bit, those of the same
+  tokens sent 16 at a time (which the general kernel serves);
+* bounded: realistic packages built by the oracle stay within the bound
+  stated in include/rrq.h.
+Packages come from the oracle or a seeded generator, never from the GPU.
+"""
+
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import rrq_oracle as npo
+
+pytestmark = pytest.mark.gpu
+U = 2.0 ** -24
+G = 128
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _run(gpu, codes, s_raw, z, rows, cols, k, xb, zp="int", sd="f32"):
+    import torch
+    M = xb.size // cols
+    c = torch.from_numpy(codes.view(np.int32).copy()).cuda()
+    sc = torch.from_numpy(s_raw.copy()).cuda()
+    ze = None if z is None else torch.from_numpy(z.copy()).cuda()
+    X = torch.from_numpy(xb.view(np.int16).reshape(M, cols).copy()).cuda().view(torch.bfloat16)
+    Y = torch.full((M, rows), float("nan"), dtype=torch.float32, device="cuda")
+    gpu.rrq_linear_format(c, sc, ze, rows, cols, G, codes.shape[0], gpu.ZERO_POINTS[zp],
+                          gpu.SCALE_TYPES[sd], k, X, M, Y)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy()
+
+
+def _exact(rows, cols, M, seed):
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(0, 2 ** 32, (4, rows * cols // 16), dtype=np.uint64).astype(np.uint32)
+    s = (2.0 ** rng.integers(-4, -1, (4, rows * cols // G))).astype(np.float32)
+    z = rng.integers(0, 4, (4, rows * cols // G)).astype(np.float32)
+    xb = npo.f32_to_bf16_bits(rng.integers(-4, 5, (M, cols)).astype(np.float32))
+    return codes, s, z, xb
+
+
+@pytest.mark.parametrize("rows,cols,M", [
+    (16, 128, 128), (5, 384, 140), (64, 1024, 192), (100, 4096, 129), (257, 2048, 130),
+    (64, 12288, 200), (1, 4224, 161),
+])
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_prefill_exact(gpu, rows, cols, M, k):
+    _log(f"prefill exact rows={rows} cols={cols} M={M} k={k}")
+    codes, s, z, xb = _exact(rows, cols, M, rows + cols + M)
+    y = _run(gpu, codes, s, z, rows, cols, k, xb)
+    ref = npo.linear(codes, s, z, rows, cols, G, k, xb)
+    assert np.all(np.abs(ref) < 2.0 ** 20)
+    bad = np.argwhere(y.astype(np.float64) != ref)
+    assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
+
+
+@pytest.mark.parametrize("zp,sd", [("sym", "f16"), ("real", "f32"), ("int", "bf16")])
+def test_prefill_exact_formats(gpu, zp, sd):
+    rows, cols, M, k = 70, 2048, 148, 3
+    _log(f"prefill exact format {zp}/{sd}")
+    codes, s, z, xb = _exact(rows, cols, M, 99)
+    if zp == "sym":
+        zz, zv = None, np.full_like(s, 2.0)
+    elif zp == "real":
+        zz = (np.random.default_rng(5).integers(0, 13, s.shape) * 0.25).astype(np.float32)
+        zv = zz
+    else:
+        zz = zv = z
+    s_raw = (s.astype(np.float16).view(np.uint16) if sd == "f16"
+             else (s.view(np.uint32) >> 16).astype(np.uint16) if sd == "bf16" else s)
+    y = _run(gpu, codes, s_raw, zz, rows, cols, k, xb, zp, sd)
+    ref = npo.linear(codes, s, zv, rows, cols, G, k, xb)
+    assert np.array_equal(y.astype(np.float64), ref)
+
+
+def _realistic(rows, cols, seed, zp="int", sd="f32"):
+    rng = np.random.default_rng(seed)
+    w = (rng.standard_normal(rows * cols) * 0.02).astype(np.float32)
+    w = np.where(rng.random(w.size) < 1e-3, w * 20, w).astype(np.float32)
+    oc, os_, oz = oracle.c_construct_format(npo.f32_to_bf16_bits(w), G, 4, zp, sd)
+    return oc, os_, oz
+
+
+@pytest.mark.parametrize("rows,cols,M,k", [(300, 4096, 160, 4), (64, 12288, 136, 2),
+                                           (129, 1024, 250, 1)])
+def test_prefill_equals_16_token_calls(gpu, rows, cols, M, k):
+    """The prefill form and the general kernel's 16-token tiles accumulate
+    every output in the same order: identical bits on a realistic package."""
+    _log(f"prefill vs 16-token calls rows={rows} cols={cols} M={M} k={k}")
+    oc, os_, oz = _realistic(rows, cols, rows + M)
+    rng = np.random.default_rng(M)
+    xb = npo.f32_to_bf16_bits(rng.standard_normal((M, cols)).astype(np.float32))
+    y = _run(gpu, oc, os_, oz, rows, cols, k, xb)
+    parts = [_run(gpu, oc, os_, oz, rows, cols, k, xb.reshape(M, cols)[m:m + 16].reshape(-1))
+             for m in range(0, M, 16)]
+    y16 = np.concatenate(parts, axis=0)
+    assert np.array_equal(y.view(np.uint32), y16.view(np.uint32))
+
+
+@pytest.mark.parametrize("zp,sd", [("int", "f32"), ("sym", "f16")])
+def test_prefill_realistic_within_bound(gpu, zp, sd):
+    rows, cols, M = 192, 4096, 144
+    oc, os_, oz = _realistic(rows, cols, 7, zp, sd)
+    sv = npo.load_scales(os_, sd)
+    zv = np.full_like(sv, 2.0) if zp == "sym" else oz
+    rng = np.random.default_rng(8)
+    xb = npo.f32_to_bf16_bits(rng.standard_normal((M, cols)).astype(np.float32))
+    xa = np.abs(npo.bf16_bits_to_f32(xb).reshape(M, cols).astype(np.float64))
+    T = xa.reshape(M, cols // G, G).sum(axis=2)
+    for k in (1, 4):
+        y = _run(gpu, oc, os_, None if zp == "sym" else oz, rows, cols, k, xb, zp, sd)
+        ref = npo.linear(oc, sv, zv, rows, cols, G, k, xb)
+        A = sum(T @ (np.abs(sv[t].astype(np.float64)) * (11 + np.abs(zv[t].astype(np.float64))))
+                .reshape(rows, cols // G).T for t in range(k))
+        p = cols // G
+        n = k * (min(p, 4 * math.ceil(p / 16)) + 1)
+        tol = 1.05 * U * A * (G + 2 * n + 24) + 1e-300
+        err = np.abs(y.astype(np.float64) - ref)
+        assert np.all(err <= tol), f"k={k}: {np.max(err / tol)}"
+        _log(f"prefill realistic {zp}/{sd} k={k}: max err / bound = {np.max(err / tol):.3g}")
