@@ -297,7 +297,9 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *              aligned (read only).
  *   n_tokens   >= 1; up to 4 tokens are served by one pass over the
  *              package (single-token decode reads it once), more tokens 16
- *              per pass.
+ *              per pass, and from 128 tokens (groups of 128) 64-token tiles
+ *              run as a matrix-core product with the 16-token tiles'
+ *              accumulation order (the same results).
  *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
  *   stream     HIP stream the work is enqueued on.
  *
