@@ -135,3 +135,22 @@ def test_prefill_realistic_within_bound(gpu, zp, sd):
         err = np.abs(y.astype(np.float64) - ref)
         assert np.all(err <= tol), f"k={k}: {np.max(err / tol)}"
         _log(f"prefill realistic {zp}/{sd} k={k}: max err / bound = {np.max(err / tol):.3g}")
+
+
+@pytest.mark.parametrize("rows,cols,k", [(4096, 4096, 4), (12288, 4096, 1)])
+def test_prefill_full_size_sampled(gpu, rows, cols, k):
+    """The benchmark's prefill size (2048 tokens, Qwen3-8B layer shapes, the
+    launch configuration the bench times) on an exact package: sampled rows,
+    every token, bit-exact."""
+    M = 2048
+    _log(f"prefill full size rows={rows} cols={cols} M={M} k={k}")
+    codes, s, z, xb = _exact(rows, cols, M, rows + k)
+    y = _run(gpu, codes, s, z, rows, cols, k, xb)
+    rng = np.random.default_rng(k)
+    idx = np.unique(np.concatenate([np.arange(16), np.arange(rows - 16, rows),
+                                    rng.choice(rows, 48, replace=False)]))
+    ref = npo.linear(codes, s, z, rows, cols, G, k, xb, row_index=idx)
+    got = y[:, idx].astype(np.float64)
+    bad = np.argwhere(got != ref)
+    assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
+    assert not np.any(np.isnan(y)), "unwritten outputs"
