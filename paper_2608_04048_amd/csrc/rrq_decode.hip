@@ -214,21 +214,27 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
     const int my_tiles = my_batches * batch;
     const int total = my_tiles * SPW;                  // items
 
-    // DMA of item it (tile it / SPW of this workgroup's sequence, set
-    // it % SPW of this wave's) into slot it % D. Items past the end, and
-    // tiles past the last row, read through an empty descriptor (no memory
-    // access, zeros in the slot): every item issues the same loads.
-    auto issue = [&](int it) {
-        const int ti = it / SPW;
-        const int64_t tile = ((int64_t)blockIdx.x + (int64_t)(ti / batch) * gridDim.x) * batch +
-                             ti % batch;
-        const uint32_t set = set0 + (uint32_t)(it % SPW);
-        const bool live = it < total && tile < n_tiles;
-        const uint32_t code_base = live ? (uint32_t)(tile * 4) * row_bytes + set * 128 : 0u;
-        const uint32_t grp_base = live ? (uint32_t)(tile * 4) * gpr + set * 4 : 0u;
-        const uint32_t lds = lds_ring + (uint32_t)(it % D) * L::BYTES;
-        const u32x4 c_src = live ? dc : dnone, s_src = live ? ds : dnone,
-                    z_src = live ? dz : dnone;
+    // DMA of the items in order, one call per item: item it is tile it / SPW
+    // of this workgroup's sequence (batch b, tile t of it: tile
+    // (blockIdx + b grid) batch + t), set it % SPW of this wave's, into slot
+    // it % D. The position is kept as running counters, so an item costs a
+    // few scalar additions rather than divisions. Items past the end, and
+    // tiles past the last row, read through descriptors of size 0 (no
+    // memory access, zeros in the slot): every item issues the same loads.
+    // (tile indices fit 32 bits: rows < 2^26)
+    int is_set = 0, is_tt = 0, is_slot = 0, issued = 0;
+    int is_tile = (int)blockIdx.x * batch;
+    const int batch_jump = ((int)gridDim.x - 1) * batch + 1;
+    const int tiles = (int)n_tiles;
+    auto issue_next = [&]() {
+        const bool live = issued < total && is_tile < tiles;
+        const uint32_t set = set0 + (uint32_t)is_set;
+        const uint32_t row4 = live ? (uint32_t)is_tile * 4 : 0u;
+        const uint32_t code_base = row4 * row_bytes + set * 128;
+        const uint32_t grp_base = row4 * gpr + set * 4;
+        const uint32_t lds = lds_ring + (uint32_t)is_slot * L::BYTES;
+        u32x4 c_src = dc, s_src = ds, z_src = dz;
+        if (!live) c_src[2] = s_src[2] = z_src[2] = 0u;
         // the reads of the item that used this slot have completed
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
@@ -239,6 +245,17 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
         else
             dma_ushort(s_src, grp_base * 2, lds + L::SCALES, dma_scale);
         dma_dword(z_src, grp_base * 4, lds + L::ZEROS, dma_zero);
+        ++issued;
+        if (++is_slot == D) is_slot = 0;
+        if (++is_set == SPW) {
+            is_set = 0;
+            if (++is_tt == batch) {
+                is_tt = 0;
+                is_tile += batch_jump;
+            } else {
+                ++is_tile;
+            }
+        }
     };
 
     // Activations first (the lane as A row: token ta, tokens past n_tokens
@@ -257,7 +274,7 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
         }
     }
 #pragma unroll
-    for (int d = 0; d < D; ++d) issue(d);
+    for (int d = 0; d < D; ++d) issue_next();
     wait_runs<D * L::DMA>(run);
 
     u32x4 a[SPW][4];
@@ -275,15 +292,14 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
         }
     }
 
-    int n_red = 0;
+    int n_red = 0, slot_i = 0, tt = 0, bi = 0;
     for (int ti = 0; ti < my_tiles; ++ti) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int set = 0; set < SPW; ++set) {
-            const int it = ti * SPW + set;
             // this item's loads have landed; the next D - 1 items' may not
             wait_vm<(D - 1) * L::DMA>();
-            const char *slot = my_ring + (it % D) * L::BYTES;
+            const char *slot = my_ring + slot_i * L::BYTES;
             float c = 0.0f;
 #pragma unroll
             for (int st = 0; st < K; ++st) {
@@ -315,15 +331,16 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sx[set][i], acc[i]);
             // the slot is free: refill it with the item D ahead
-            issue(it + D);
+            issue_next();
+            if (++slot_i == D) slot_i = 0;
         }
         // end of this wave's share of the tile: its diagonal entry (token j,
         // row r, group gb) summed over the 4 groups of the lanes
         // n = 4 r .. 4 r + 3, kept for the batch reduction
         float y = gb == 0 ? acc[0] : gb == 1 ? acc[1] : gb == 2 ? acc[2] : acc[3];
-        y += __shfl_xor(y, 1, 64);
-        y += __shfl_xor(y, 2, 64);
-        const int tt = ti % batch;
+        // (quad permutations [1 0 3 2] and [2 3 0 1]: lanes n ^ 1, n ^ 2)
+        y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0xB1, 0xF, 0xF, false));
+        y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0x4E, 0xF, 0xF, false));
         if (gb == 0) red[n_red & 1][wave][tt][4 * j + r] = y;
         if (tt == batch - 1) {
             // end of the batch: sum the waves' partial sums in wave order
@@ -337,13 +354,16 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
                 float out = red[n_red & 1][0][tb][e];
 #pragma unroll
                 for (int w = 1; w < kWaves; ++w) out += red[n_red & 1][w][tb][e];
-                const int64_t tile =
-                    ((int64_t)blockIdx.x + (int64_t)(ti / batch) * gridDim.x) * batch + tb;
+                const int64_t tile = ((int64_t)blockIdx.x + (int64_t)bi * gridDim.x) * batch + tb;
                 const int64_t o = tile * 4 + (e & 3);
                 const int tok = e >> 2;
                 if (tok < n_tokens && o < rows) Y[(int64_t)tok * rows + o] = out;
             }
             ++n_red;
+            tt = 0;
+            ++bi;
+        } else {
+            ++tt;
         }
     }
     // no DMA load may still write this workgroup's LDS once it ends
@@ -404,13 +424,14 @@ bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_toke
         cols / 4096 > kDecodeMaxSetsPerWave)
         return false;
     // Measured crossover against the general kernel (one token, packages
-    // read from HBM): from 3 stages this form is faster on every shape; with
-    // 2 stages an item is small, and for 1025 to 6143 rows its per-item and
-    // start-up work (activations, group sums, the ring's first loads) costs
-    // more than the general kernel's less efficient loads; with 1 stage the
-    // general kernel is faster everywhere.
-    if (k >= 3) return true;
-    return k == 2 && (rows >= 6144 || rows <= 1024);
+    // read from HBM): from 2 stages this form is as fast or faster on every
+    // shape; with 1 stage an item is small and its per-item work costs more
+    // than the general kernel's less efficient loads, except on small
+    // matrices (latency-bound: this form fills the GPU with 4-row tiles) and
+    // on tall ones with up to 2 sets of 4 groups per wave (two workgroups per
+    // CU).
+    if (k >= 2) return true;
+    return rows <= 1024 || (rows >= 12288 && cols <= 8192);
 }
 
 hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const float *zeros,

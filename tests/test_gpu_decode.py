@@ -1,7 +1,7 @@
 """GPU parity of rrq_linear's decode form (up to 4 tokens, groups of 128,
-cols a multiple of 4096 up to 16384; 3 or 4 stages at any row count, 2
-stages from 6144 rows and up to 1024 rows), through the C ABI, against the
-oracle's Eq. 20 product in float64 on sampled output rows.
+cols a multiple of 4096 up to 16384; 2 to 4 stages at any row count, 1 stage
+up to 1024 rows or from 12288 rows with up to 8192 cols), through the C ABI,
+against the oracle's Eq. 20 product in float64 on sampled output rows.
 
 * exact: power-of-two scales, integer or dyadic zero-points and
   small-integer activations make every intermediate exactly representable,
@@ -62,6 +62,8 @@ def _run(gpu, codes, s, z, rows, cols, k, xb, zp=None, sd=None, s_raw=None):
     # few tiles (fewer workgroups than CUs), ragged last tile, small matrices
     (1, 4096, 1, 3), (5, 4096, 2, 4), (1023, 4096, 1, 4), (1021, 4096, 4, 2), (2047, 4096, 4, 2),
     (4096, 4096, 1, 3), (4099, 8192, 2, 4), (1024, 16384, 1, 3),
+    # one stage
+    (1000, 4096, 2, 1), (12290, 8192, 1, 1), (13, 12288, 4, 1),
 ])
 def test_decode_form_exact(gpu, rows, cols, M, k):
     _log(f"decode exact rows={rows} cols={cols} M={M} k={k}")
