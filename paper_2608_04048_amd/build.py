@@ -40,6 +40,7 @@ HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra"]
 # would only add copies).
 SOURCE_FLAGS = {"rrq_linear": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
                 "rrq_decode": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+                "rrq_batch": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
                 "rrq_prefill": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
@@ -67,7 +68,7 @@ def build(keep_asm: bool = False) -> str:
     cc = hipcc()
     os.makedirs(BUILD_DIR, exist_ok=True)
     kern_objs = []
-    for name in ("rrq_kernels", "rrq_linear", "rrq_decode", "rrq_prefill"):
+    for name in ("rrq_kernels", "rrq_linear", "rrq_decode", "rrq_batch", "rrq_prefill"):
         obj = os.path.join(BUILD_DIR, name + ".o")
         cmd = [cc, *DEVICE_FLAGS, *SOURCE_FLAGS.get(name, []), f"-I{INCLUDE}", f"-I{CSRC}", "-c",
                os.path.join(CSRC, name + ".hip"), "-o", obj]

@@ -152,6 +152,9 @@ int linear_common(const uint32_t *codes, const void *scales, const float *zeros,
     if (rrq_detail::linear_decode_fits(rows, cols, group_size, k_stages, n_tokens))
         e = rrq_detail::launch_linear_decode(codes, scales, zeros, rows, cols, k_stages, zero_point,
                                              scale_type, X, n_tokens, Y, cus, stream);
+    else if (rrq_detail::linear_batch_fits(rows, cols, group_size, k_stages, n_tokens))
+        e = rrq_detail::launch_linear_batch(codes, scales, zeros, rows, cols, k_stages, zero_point,
+                                            scale_type, X, n_tokens, Y, cus, stream);
     else if (rrq_detail::linear_prefill_fits(rows, cols, group_size, n_tokens))
         e = rrq_detail::launch_linear_prefill(codes, scales, zeros, rows, cols, k_stages,
                                               zero_point, scale_type, X, n_tokens, Y, stream);

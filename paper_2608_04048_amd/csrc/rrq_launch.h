@@ -42,6 +42,16 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
 // and row counts where it is the faster one: linear_decode_fits);
 // launch_linear covers every other case.
 constexpr int kDecodeMaxSetsPerWave = 4;
+// The batch form (groups of 128, kBatchMinTokens to 16 tokens, at most 4096
+// cols, and the row and stage counts where it is the faster one:
+// linear_batch_fits). The kernel itself takes up to 8192 cols: the A operands
+// of a wave's groups stay in its registers.
+constexpr int kBatchMinTokens = 5;
+bool linear_batch_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens);
+hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const float *zeros,
+                               int64_t rows, int64_t cols, int k, int zero_point, int scale_type,
+                               const uint16_t *X, int64_t n_tokens, float *Y, int cus,
+                               hipStream_t stream);
 // The prefill form (groups of 128, at least kPrefillMinTokens tokens, 64-token
 // x 64-row tiles). Measured against the general kernel on the Qwen3-8B
 // shapes: from 128 tokens it is faster on all of them (2-3x from 256); below
