@@ -22,6 +22,7 @@ import sys
 from collections import defaultdict
 
 DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "linear_kernel", "decode_kernel",
+                 "batch_kernel", "prefill_kernel",
                  "stream_probe_kernel", "read_probe_kernel", "write_probe_kernel",
                  "copyBuffer"]
 
