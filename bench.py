@@ -52,6 +52,18 @@ def reconstruct_bytes(n, G, k, out_bytes):
     return k * n // 4 + 2 * 4 * k * (n // G) + out_bytes * n
 
 
+def cpu_model():
+    """The host CPU's model name (Linux), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(w, W_dev, budget_s=12.0, threads=0):
     """The C oracle (as it stands) on the host cores: whole tensors of the
     workload in order, passes repeated, until about budget_s seconds of
@@ -89,7 +101,7 @@ def cpu_baseline(w, W_dev, budget_s=12.0, threads=0):
     sample = (f"{n_calls} tensor calls over {len(w.tensors)} tensors of {w.name} "
               f"({passes} pass(es)), {done_elems} weights, construct only, {elapsed:.1f} s")
     return {"value": round(2 * done_elems / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "sample": sample}
+            "kind": "oracle", "sample": sample, "cpu": cpu_model()}
 
 
 def from_base_bytes(n, G, S):
