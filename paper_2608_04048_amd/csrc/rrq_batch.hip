@@ -192,7 +192,10 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
 
     // The ring's first items, then the activations of this wave's groups
     // (lane as A row: token n, tokens past n_tokens reading zeros), waited
-    // for explicitly with the runs tied to the wait.
+    // for explicitly with the runs tied to the wait. The prologue runs at a
+    // raised wave priority (measured 1-5% faster at 2 to 4 stages, same
+    // outputs): it is a serial stretch that every later item waits for.
+    __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int d = 0; d < D; ++d) issue_next();
     u32x4 a[kMaxGroupsPerWave][4];
@@ -224,6 +227,7 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
         }
     }
 
+    __builtin_amdgcn_s_setprio(0);
     int slot_i = 0, n_red = 0;
     for (int ti = 0; ti < my_tiles; ++ti) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
