@@ -517,7 +517,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build measures one GPU only (the path needs no exchange between "
+        print("bench.py: the benchmark runs on one GPU only (the path needs no exchange between "
               "GPUs); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
