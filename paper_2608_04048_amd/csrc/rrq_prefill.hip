@@ -92,7 +92,7 @@ __device__ __forceinline__ void act_operands(const u32x4 (&run)[4], u32x4 (&a)[4
     }
 }
 
-template <int K, bool DEF>
+template <int K, bool DEF, bool MFMA_PRIO>
 __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
@@ -175,6 +175,10 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     // Quarter length as in the general kernel (4 waves, 2-group chunks).
     const uint32_t per_q = (((gpr + 3) / 4 + 1) / 2) * 2;
     const u32x4 ones = {one, one, one, one};
+    // MFMA_PRIO (2 to 4 stages, long token runs): the stage products of a
+    // group (its MFMA stretch) are issued at a raised wave priority, so that
+    // the matrix core keeps being fed while the other wave of the SIMD builds
+    // operands (measured 4-9% faster from 1024 tokens; not for short runs).
 
     f32x4 run[4], cur[4];
 #pragma unroll
@@ -229,6 +233,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
             for (int b = 0; b < 4; ++b) acc = mfma(a[tt][b], ones, acc);
             sx[tt] = acc;
         }
+        if constexpr (MFMA_PRIO) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int t = 0; t < K; ++t) {
             const u32x2 w = *reinterpret_cast<const u32x2 *>(
@@ -244,6 +249,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
                 for (int i = 0; i < 4; ++i) cur[tt][i] = __builtin_fmaf(s4[t], p[i], cur[tt][i]);
             }
         }
+        if constexpr (MFMA_PRIO) __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
@@ -290,6 +296,10 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
+// From this many tokens the 2-4 stage kernels issue their MFMA stretches at
+// a raised wave priority (A/B: faster from 1024 tokens, slower at 256).
+constexpr int64_t kPrefillPrioTokens = 1024;
+
 template <bool DEF>
 hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int64_t n_tokens,
@@ -299,11 +309,15 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
     const int64_t tiles = (int64_t)row_tiles * ((n_tokens + kTokens - 1) / kTokens);
     const int grid = (int)tiles;
     const int64_t pw = rows * cols / 16, pg = rows * cols / 128;
+    const bool prio = n_tokens >= kPrefillPrioTokens;
     switch (k) {
-    case 1: return launch(prefill_kernel<1, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    case 2: return launch(prefill_kernel<2, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    case 3: return launch(prefill_kernel<3, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    case 4: return launch(prefill_kernel<4, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
+    case 1: return launch(prefill_kernel<1, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
+    case 2: return prio ? launch(prefill_kernel<2, DEF, true>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
+                        : launch(prefill_kernel<2, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
+    case 3: return prio ? launch(prefill_kernel<3, DEF, true>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
+                        : launch(prefill_kernel<3, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
+    case 4: return prio ? launch(prefill_kernel<4, DEF, true>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
+                        : launch(prefill_kernel<4, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
     default: return hipErrorInvalidValue;
     }
 }

@@ -59,6 +59,8 @@ def _exact(rows, cols, M, seed):
 @pytest.mark.parametrize("rows,cols,M", [
     (16, 128, 128), (5, 384, 140), (64, 1024, 192), (100, 4096, 129), (257, 2048, 130),
     (64, 12288, 200), (1, 4224, 161),
+    # from 1024 tokens the 2-4 stage kernels raise their MFMA stretches' priority
+    (70, 1024, 1100), (33, 2048, 1024),
 ])
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_prefill_exact(gpu, rows, cols, M, k):
@@ -71,10 +73,11 @@ def test_prefill_exact(gpu, rows, cols, M, k):
     assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
 
 
+@pytest.mark.parametrize("M", [148, 1030])
 @pytest.mark.parametrize("zp,sd", [("sym", "f16"), ("real", "f32"), ("int", "bf16")])
-def test_prefill_exact_formats(gpu, zp, sd):
-    rows, cols, M, k = 70, 2048, 148, 3
-    _log(f"prefill exact format {zp}/{sd}")
+def test_prefill_exact_formats(gpu, zp, sd, M):
+    rows, cols, k = 70, 2048, 3
+    _log(f"prefill exact format {zp}/{sd} M={M}")
     codes, s, z, xb = _exact(rows, cols, M, 99)
     if zp == "sym":
         zz, zv = None, np.full_like(s, 2.0)
@@ -99,7 +102,7 @@ def _realistic(rows, cols, seed, zp="int", sd="f32"):
 
 
 @pytest.mark.parametrize("rows,cols,M,k", [(300, 4096, 160, 4), (64, 12288, 152, 2),
-                                           (129, 1024, 250, 1)])
+                                           (129, 1024, 250, 1), (100, 2048, 1056, 3)])
 def test_prefill_equals_16_token_calls(gpu, rows, cols, M, k):
     """The prefill form and the general kernel's 16-token tiles accumulate
     every output in the same order: identical bits on a realistic package.
