@@ -100,8 +100,28 @@ def cpu_baseline(w, W_dev, budget_s=12.0, threads=0):
         passes += 1
     sample = (f"{n_calls} tensor calls over {len(w.tensors)} tensors of {w.name} "
               f"({passes} pass(es)), {done_elems} weights, construct only, {elapsed:.1f} s")
-    return {"value": round(2 * done_elems / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads,
-            "kind": "oracle", "sample": sample, "cpu": cpu_model()}
+    result = {"value": round(2 * done_elems / elapsed / 1e9, 4), "unit": "GB/s", "cores": threads,
+              "kind": "oracle", "sample": sample, "cpu": cpu_model()}
+
+    # Per-core figure: one OpenMP thread on one decoder layer (the first
+    # layer of a stack, i.e. the single-layer workload's bits), one pass.
+    layer = [t for t in w.tensors if t.name.startswith("layers.0.")] or list(w.tensors)
+    oracle.c_set_threads(1)
+    try:
+        el1, n1 = 0.0, 0
+        for t in layer:
+            bits = W_dev[t.offset:t.offset + t.numel].cpu().view(torch.int16).numpy().view(np.uint16)
+            t0 = time.perf_counter()
+            oracle.c_construct(bits, G, S)
+            el1 += time.perf_counter() - t0
+            n1 += t.numel
+    finally:
+        oracle.c_set_threads(threads)
+    result["one_thread"] = {
+        "value": round(2 * n1 / el1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+        "sample": f"{len(layer)} tensors of one decoder layer ({n1} weights), construct only, "
+                  f"{el1:.1f} s"}
+    return result
 
 
 def from_base_bytes(n, G, S):
@@ -476,6 +496,42 @@ def stream_probe(src_bytes, flush_buf=None, launches=10):
                        "frac": round(serial_gbs / HBM_PEAK_GBS, 4)}}
 
 
+def construct_probe(W, n, G, S, codes, scales, zeros, stream, flush_buf=None, launches=10,
+                    blocks_per_cu=(8, 4, 16)):
+    """Construction's own memory traffic with no arithmetic
+    (hbm_probe_construct): the same input, the same output planes and
+    addresses as the construct call, the same tiles and launch (8 one-wave
+    workgroups per CU), and the same workload; also at other occupancies.
+    Overwrites the package buffers."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+
+    moved = construct_bytes(n, G, S)
+    out = {}
+    for bpc in blocks_per_cu:
+        def run():
+            probe.hbm_probe_construct(W, n // G, G, S, codes, scales, zeros, bpc, stream)
+        run()
+        vals = []
+        for _ in range(launches):
+            if flush_buf is not None:
+                flush_buf.fill_(1.0)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            run()
+            b.record(stream)
+            b.synchronize()
+            vals.append(a.elapsed_time(b))
+        t = sum(vals) / len(vals)
+        gbs = moved / (t * 1e-3) / 1e9
+        out[bpc] = {"ms": round(t, 4), "gbs": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
+    res = dict(out[blocks_per_cu[0]])
+    res["bytes"] = moved
+    res["by_blocks_per_cu"] = {str(k): v for k, v in out.items()}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -699,10 +755,20 @@ def main():
     if not args.no_stream_probe:
         result["stream_probe"] = stream_probe(min(2 * n, 16 << 30), flush_buf)
         result["construct_frac_of_probe"] = round(c_achieved / result["stream_probe"]["gbs"], 4)
+        if not args.per_tensor:
+            print("bench: construct-pattern probe", file=sys.stderr, flush=True)
+            cp = construct_probe(W, n, G, S, codes, scales, zeros, stream, flush_buf)
+            result["stream_probe"]["construct_pattern"] = cp
+            result["construct_frac_of_construct_pattern"] = round(c_achieved / cp["gbs"], 4)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, W.view(-1), args.cpu_budget, args.cpu_threads)
     print(json.dumps(result), flush=True)
+    # Release the device buffers and let queued work drain before the
+    # interpreter exits, so that the process ends right after its line.
+    del W, codes, scales, zeros, outs, calls, flush_buf
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
 
 
 if __name__ == "__main__":

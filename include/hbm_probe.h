@@ -5,7 +5,8 @@
  * 2-bit code planes plus binary32 scale and zero per group of 128), so the
  * mixed probe reads B bytes and writes 5B/8 bytes with the same kind of wide,
  * coalesced accesses, and no arithmetic; the read-only and write-only probes
- * give each direction's own ceiling. Measurement aids only: they compute
+ * give each direction's own ceiling, and the construct-pattern probe replays
+ * construction's own loads and stores. Measurement aids only: they compute
  * nothing of the method.
  */
 #ifndef HBM_PROBE_H
@@ -60,6 +61,36 @@ int hbm_probe_read(const void *src, size_t src_bytes, uint32_t *out, hipStream_t
  * Returns as hbm_probe_read.
  */
 int hbm_probe_write(void *dst, size_t dst_bytes, uint32_t value, hipStream_t stream);
+
+/*
+ * hbm_probe_construct - enqueue one pass with package construction's own
+ * memory traffic and no quantization arithmetic: n_groups groups of
+ * group_size bfloat16 weights are read once, in the construct kernel's tiles
+ * of 64 groups (one wave each, next tile prefetched, LDS transpose), and per
+ * stage each group stores its group_size / 16 code words, one 32-bit scale
+ * and one 32-bit zero-point into the planes of rrq_construct's layout. With
+ * w[0..group_size/2 - 1] the group's 32-bit words (little-endian pairs of
+ * bfloat16) and k the stage:
+ *   codes[k][g * group_size/16 + j] = (XOR of w[j + m * group_size/16] over m) ^ k
+ *   scales[k][g] = w[0] ^ k,   zeros[k][g] = w[1] ^ k.
+ *
+ *   W            device, n_groups * group_size * 2 bytes, 16-byte aligned.
+ *   n_groups     >= 1.
+ *   group_size   32, 64 or 128.
+ *   n_stages     1 .. 4.
+ *   codes        device, n_stages * n_groups * group_size / 16 uint32, 16-byte aligned.
+ *   scales,
+ *   zeros        device, n_stages * n_groups uint32 each, 4-byte aligned.
+ *   blocks_per_cu  resident one-wave workgroups per compute unit, 1 .. 32;
+ *                0 = the construct kernel's 8.
+ *
+ * Returns 0, or 1 (NULL), 2 (misaligned), 3 (bad size or argument) with
+ * nothing enqueued, or 7 if the launch failed. Outputs must not overlap W or
+ * each other. The caller owns every buffer; nothing is allocated.
+ */
+int hbm_probe_construct(const void *W, int64_t n_groups, int32_t group_size, int32_t n_stages,
+                        uint32_t *codes, uint32_t *scales, uint32_t *zeros,
+                        int32_t blocks_per_cu, hipStream_t stream);
 
 #ifdef __cplusplus
 }

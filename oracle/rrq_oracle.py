@@ -438,12 +438,6 @@ def group_pmr(x: np.ndarray, group_size: int) -> np.ndarray:
     return np.where(S > 0, pmr, np.float32(0.0)).astype(np.float32)
 
 
-def tensor_pmr_stats(pmr_groups: np.ndarray):
-    """The paper's tensor-level indicators from per-group PMR values of one
-    tensor: its largest group PMR (the tensor-wise maximum)."""
-    return float(np.max(pmr_groups))
-
-
 # ---------------------------------------------------------------------------
 # Stage-sum linear layer (the prefill / decode product of Eq. 20)
 # ---------------------------------------------------------------------------

@@ -1,7 +1,10 @@
 // Streaming probes. The mixed one has construction's read/write ratio
 // (2 : 1.25): it reads every 16-byte chunk of src and writes 5 of every 8
 // chunks to dst, each lane keeping four loads in flight before it stores. The
-// read-only and write-only ones bound each direction on its own.
+// read-only and write-only ones bound each direction on its own. The
+// construct-pattern probe replays package construction's own memory traffic
+// (its tiles, loads, LDS transpose, prefetch and the 16 stores per tile over
+// 12 output planes) with no quantization arithmetic.
 
 #include "hbm_probe.h"
 
@@ -14,6 +17,8 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 constexpr int kBlocksPerCU = 8;
+// The construct kernel's launch: one-wave workgroups, 8 per compute unit.
+constexpr int kConstructProbeBlocksPerCU = 8;
 
 __global__ __launch_bounds__(kThreads) void stream_probe_kernel(const uint4 *__restrict__ src,
                                                                 uint4 *__restrict__ dst,
@@ -82,6 +87,115 @@ __global__ __launch_bounds__(kThreads) void write_probe_kernel(uint4 *__restrict
     }
 }
 
+// Construct-pattern probe. One wave per workgroup takes tiles of 64 groups of
+// G bfloat16 weights in a grid-stride loop, exactly as the construct kernel
+// does: 16-byte loads with each wave instruction covering 1 KiB, the next tile
+// prefetched into registers while the current one is handled, the tile
+// transposed through LDS half a group at a time (rows padded by 16 bytes), and
+// per stage the same store instructions into the same planes: the lane's
+// G / 16 code words (16-byte stores, 2 KiB per wave instruction at G = 128),
+// one 32-bit scale and one 32-bit zero-point (256 bytes per wave
+// instruction). The values stored are XORs of the group's 32-bit words, so
+// every load is live and the stores are checkable:
+//   code word j of stage k  = (XOR of the group's words j, j + G/16, ...) ^ k
+//   scale of stage k        = (group word 0) ^ k
+//   zero of stage k         = (group word 1) ^ k
+// Buffer resources drop stores past the last group and read zeros past the
+// input, as in the construct kernel.
+typedef uint32_t pu32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t pu32x2 __attribute__((ext_vector_type(2)));
+using prsrc_t = __amdgpu_buffer_rsrc_t;
+
+__device__ __forceinline__ prsrc_t probe_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                             0x00020000);
+}
+
+template <int CH>
+__device__ __forceinline__ void probe_load_tile(const uint4 *__restrict__ W, int64_t n_groups,
+                                                int64_t tile, int lane, pu32x4 (&v)[CH])
+{
+    const int64_t g0 = tile * 64;
+    const int64_t left = n_groups - g0;
+    const uint32_t bytes = left <= 0 ? 0u : (uint32_t)(left < 64 ? left : 64) * CH * 16;
+    const prsrc_t src = probe_rsrc(W + (left <= 0 ? 0 : g0 * CH), bytes);
+#pragma unroll
+    for (int i = 0; i < CH; ++i)
+        v[i] = __builtin_amdgcn_raw_buffer_load_b128(src, (i * 64 + lane) * 16, 0, 0);
+}
+
+template <int G>
+__global__ __launch_bounds__(64) void construct_probe_kernel(const uint4 *__restrict__ W,
+                                                             int64_t n_groups, int n_stages,
+                                                             uint32_t *__restrict__ codes,
+                                                             uint32_t *__restrict__ scales,
+                                                             uint32_t *__restrict__ zeros)
+{
+    constexpr int CH = G / 8, HC = CH / 2, WPG = G / 16, ROW = HC + 1;
+    constexpr int GROUPS_PER_LOAD = 64 / CH;
+    __shared__ pu32x4 tile_lds[64 * ROW];
+
+    const int lane = threadIdx.x;
+    const int64_t n_tiles = (n_groups + 63) / 64;
+    const int my_half = (lane % CH) / HC;
+    pu32x4 *const wr_base = tile_lds + (lane / CH) * ROW + (lane % HC);
+    const pu32x4 *const rd_base = tile_lds + lane * ROW;
+
+    int64_t tile = blockIdx.x;
+    pu32x4 v[CH];
+    if (tile < n_tiles) probe_load_tile<CH>(W, n_groups, tile, lane, v);
+    for (; tile < n_tiles; tile += gridDim.x) {
+        const int64_t g0 = tile * 64;
+        const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
+        uint32_t acc[WPG] = {};
+        uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __syncthreads();
+            if (my_half == h) {
+#pragma unroll
+                for (int i = 0; i < CH; ++i) wr_base[i * GROUPS_PER_LOAD * ROW] = v[i];
+            }
+            __syncthreads();
+#pragma unroll
+            for (int c = 0; c < HC; ++c) {
+                const pu32x4 x = rd_base[c];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int wi = (h * HC + c) * 4 + q;   // word index within the group
+                    acc[wi % WPG] ^= x[q];
+                    if (wi == 0) w0 = x[q];
+                    if (wi == 1) w1 = x[q];
+                }
+            }
+        }
+        probe_load_tile<CH>(W, n_groups, tile + gridDim.x, lane, v);
+        const int64_t words_per_stage = n_groups * WPG;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t groups =
+                __builtin_amdgcn_readfirstlane(k < n_stages ? groups_here : 0u);
+            const prsrc_t rc = probe_rsrc(codes + k * words_per_stage + g0 * WPG,
+                                          groups * WPG * 4);
+            if constexpr (WPG >= 4) {
+#pragma unroll
+                for (int i = 0; i < WPG; i += 4) {
+                    const pu32x4 o = {acc[i] ^ k, acc[i + 1] ^ k, acc[i + 2] ^ k, acc[i + 3] ^ k};
+                    __builtin_amdgcn_raw_buffer_store_b128(o, rc, lane * WPG * 4 + 4 * i, 0, 0);
+                }
+            } else {
+                const pu32x2 o = {acc[0] ^ k, acc[1] ^ k};
+                __builtin_amdgcn_raw_buffer_store_b64(o, rc, lane * WPG * 4, 0, 0);
+            }
+            __builtin_amdgcn_raw_buffer_store_b32(
+                w0 ^ k, probe_rsrc(scales + k * n_groups + g0, groups * 4), lane * 4, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(
+                w1 ^ k, probe_rsrc(zeros + k * n_groups + g0, groups * 4), lane * 4, 0, 0);
+        }
+    }
+}
+
 int grid_limit(int per_cu, int64_t work, int per_block, int *grid)
 {
     int dev = 0, cus = 0;
@@ -141,5 +255,41 @@ extern "C" int hbm_probe_stream(const void *src, size_t src_bytes, void *dst, hi
     if (blocks > (int64_t)cus * kBlocksPerCU) blocks = (int64_t)cus * kBlocksPerCU;
     hipLaunchKernelGGL(stream_probe_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
                        static_cast<const uint4 *>(src), static_cast<uint4 *>(dst), n16);
+    return hipGetLastError() == hipSuccess ? 0 : 7;
+}
+
+extern "C" int hbm_probe_construct(const void *W, int64_t n_groups, int32_t group_size,
+                                   int32_t n_stages, uint32_t *codes, uint32_t *scales,
+                                   uint32_t *zeros, int32_t blocks_per_cu, hipStream_t stream)
+{
+    if (!W || !codes || !scales || !zeros) return 1;
+    if ((reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(codes)) % 16 != 0 ||
+        (reinterpret_cast<uintptr_t>(scales) | reinterpret_cast<uintptr_t>(zeros)) % 4 != 0)
+        return 2;
+    if (group_size != 32 && group_size != 64 && group_size != 128) return 3;
+    if (n_groups < 1 || n_stages < 1 || n_stages > 4 || blocks_per_cu < 0 || blocks_per_cu > 32)
+        return 3;
+    // per-tile offsets of every plane stay in 64-bit pointers; sizes per
+    // tile fit 32 bits
+    if (n_groups > INT64_MAX / (4 * group_size)) return 3;
+    int grid = 0;
+    if (grid_limit(blocks_per_cu ? blocks_per_cu : kConstructProbeBlocksPerCU, n_groups, 64,
+                   &grid))
+        return 7;
+    const uint4 *w4 = static_cast<const uint4 *>(W);
+    switch (group_size) {
+    case 32:
+        hipLaunchKernelGGL(construct_probe_kernel<32>, dim3((unsigned)grid), dim3(64), 0, stream,
+                           w4, n_groups, (int)n_stages, codes, scales, zeros);
+        break;
+    case 64:
+        hipLaunchKernelGGL(construct_probe_kernel<64>, dim3((unsigned)grid), dim3(64), 0, stream,
+                           w4, n_groups, (int)n_stages, codes, scales, zeros);
+        break;
+    default:
+        hipLaunchKernelGGL(construct_probe_kernel<128>, dim3((unsigned)grid), dim3(64), 0, stream,
+                           w4, n_groups, (int)n_stages, codes, scales, zeros);
+        break;
+    }
     return hipGetLastError() == hipSuccess ? 0 : 7;
 }

@@ -1,7 +1,7 @@
 """Binding of libhbm_probe.so (include/hbm_probe.h): streaming kernels used by
 the benchmark as practical HBM ceilings: one with package construction's
 read/write ratio (reads B bytes, writes 5B/8), a read-only and a write-only
-one."""
+one, and one that replays package construction's own loads and stores."""
 
 from __future__ import annotations
 
@@ -28,6 +28,10 @@ def load_library() -> ctypes.CDLL:
         lib.hbm_probe_write.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32,
                                         ctypes.c_void_p]
         lib.hbm_probe_write.restype = ctypes.c_int
+        lib.hbm_probe_construct.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                            ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
+        lib.hbm_probe_construct.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -68,3 +72,14 @@ def hbm_probe_write(dst, dst_bytes: int, value: int, stream=None) -> None:
                                         _sp(stream))
     if st != 0:
         raise RuntimeError(f"hbm_probe_write failed with status {st}")
+
+
+def hbm_probe_construct(W, n_groups: int, group_size: int, n_stages: int, codes, scales, zeros,
+                        blocks_per_cu: int = 0, stream=None) -> None:
+    """Enqueue one pass with construction's memory traffic (see
+    include/hbm_probe.h for what it stores)."""
+    st = load_library().hbm_probe_construct(_ptr(W), int(n_groups), int(group_size),
+                                            int(n_stages), _ptr(codes), _ptr(scales),
+                                            _ptr(zeros), int(blocks_per_cu), _sp(stream))
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_construct failed with status {st}")

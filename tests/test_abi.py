@@ -187,7 +187,8 @@ def test_probe_library_exports_declared_function():
     from paper_2608_04048_amd import probe
     text = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
     names = sorted(set(re.findall(r"\b(hbm_probe_\w+)\s*\(", text)))
-    assert names == ["hbm_probe_read", "hbm_probe_stream", "hbm_probe_write"]
+    assert names == ["hbm_probe_construct", "hbm_probe_read", "hbm_probe_stream",
+                     "hbm_probe_write"]
     lib = probe.load_library()
     out = os.popen(f"nm -D --defined-only {probe.LIB_PATH}").read()
     for name in names:
@@ -227,6 +228,23 @@ def test_read_probe_rejects(src, nbytes, out, status):
 def test_write_probe_rejects(dst, nbytes, status):
     from paper_2608_04048_amd import probe
     assert probe.load_library().hbm_probe_write(dst, nbytes, 0, None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(W=0), 1), (dict(codes=0), 1), (dict(scales=0), 1), (dict(zeros=0), 1),
+    (dict(W=FAKE + 8), 2), (dict(codes=FAKE + 4), 2), (dict(scales=FAKE + 2), 2),
+    (dict(zeros=FAKE + 1), 2), (dict(G=16), 3), (dict(G=256), 3), (dict(n_groups=0), 3),
+    (dict(S=0), 3), (dict(S=5), 3), (dict(bpc=-1), 3), (dict(bpc=33), 3),
+])
+def test_construct_probe_rejects(kw, status):
+    """Argument errors are returned before anything is enqueued (no GPU is
+    touched: these checks precede every HIP call)."""
+    from paper_2608_04048_amd import probe
+    a = dict(W=FAKE, n_groups=64, G=128, S=4, codes=FAKE, scales=FAKE, zeros=FAKE, bpc=0)
+    a.update(kw)
+    assert probe.load_library().hbm_probe_construct(
+        a["W"], a["n_groups"], a["G"], a["S"], a["codes"], a["scales"], a["zeros"], a["bpc"],
+        None) == status
 
 
 def _linear_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128, S=4, k=4,

@@ -175,7 +175,7 @@ def test_distribution_sweep(gpu, name):
     w = wl.workload(name)
     W = wl.materialize(w)
     bits = W.cpu().view(torch.int16).numpy().view(np.uint16)
-    _check_case(gpu, bits, 12288, 4096, w.group_size, 4, ks=(1, 4), tag=name)
+    _check_case(gpu, bits, 12288, 4096, w.group_size, 4, tag=name)
 
 
 def test_flat_call_equals_per_tensor_calls(gpu):
@@ -197,45 +197,86 @@ def test_flat_call_equals_per_tensor_calls(gpu):
     assert all(torch.equal(x, y) for x, y in zip((codes, scales, zeros), again))
 
 
-def _sampled_stack_check(gpu, name, n_sample=4096):
-    """A full-size stack in one flat call (the benchmark's launch shape);
-    outputs of sampled groups against the oracle run on those groups."""
+def _dev(a):
+    """Host numpy array -> device tensor of the same bytes (int32 / int16)."""
+    import torch
+    if a.dtype in (np.uint32, np.float32):
+        a = a.view(np.int32)
+    elif a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _same(got, want_np):
+    """Device tensor vs host oracle array, bit for bit, compared on the device."""
+    import torch
+    want = _dev(want_np)
+    g = got.contiguous().view(want.dtype).reshape(want.shape)
+    if torch.equal(g, want):
+        return True, ""
+    bad = (g != want).nonzero()[:5].cpu().numpy().tolist()
+    return False, f"first differing indices {bad}"
+
+
+def _full_stack_check(gpu, name, recon):
+    """A full-size stack as one flat construct call and one flat reconstruct
+    call per (k, dtype), the launch shape the benchmark times; every output
+    compared with the C oracle, tensor by tensor (Alg. 1, Eq. 1-8).
+
+    recon: (k, dtype) pairs of the whole-stack reconstructions to check."""
     import torch
     w = wl.workload(name)
     G, S = w.group_size, w.n_stages
-    _log(f"materialize {name}: {w.numel} elements")
+    _log(f"{name}: materialize {w.numel} weights, {len(w.tensors)} tensors")
     W = wl.materialize(w)
     rows = w.numel // 4096
     codes, scales, zeros = gpu.construct(W.view(rows, 4096), G, S)
     torch.cuda.synchronize()
-    ng = w.n_groups
-    rng = np.random.default_rng(17)
-    idx = np.unique(np.concatenate([
-        rng.integers(0, ng, n_sample), np.arange(64), np.arange(ng - 64, ng),
-        [t.offset // G for t in w.tensors], [(t.offset + t.numel) // G - 1 for t in w.tensors]]))
-    idx_t = torch.from_numpy(idx).cuda()
-    wg = W.view(ng, G)[idx_t].cpu().view(torch.int16).numpy().view(np.uint16).reshape(-1)
-    oc, os_, oz = oracle.c_construct(wg, G, S)
-    gc = codes.view(S, ng, G // 16)[:, idx_t].cpu().numpy().view(np.uint32).reshape(S, -1)
-    assert np.array_equal(gc, oc)
-    assert np.array_equal(_u32(scales[:, idx_t]), os_.view(np.uint32))
-    assert np.array_equal(_u32(zeros[:, idx_t]), oz.view(np.uint32))
-    for k in w.recon_k:
-        out = gpu.reconstruct(codes, scales, zeros, rows, 4096, G, k, torch.bfloat16)
+    host_pkg = []
+    for i, t in enumerate(w.tensors):
+        bits = W[t.offset:t.offset + t.numel].cpu().view(torch.int16).numpy().view(np.uint16)
+        oc, os_, oz = oracle.c_construct(bits, G, S)
+        a, b = t.offset // 16, (t.offset + t.numel) // 16
+        ok, why = _same(codes[:, a:b], oc)
+        assert ok, f"{name} {t.name}: codes differ ({why})"
+        a, b = t.offset // G, (t.offset + t.numel) // G
+        ok, why = _same(scales[:, a:b], os_)
+        assert ok, f"{name} {t.name}: scales differ ({why})"
+        ok, why = _same(zeros[:, a:b], oz)
+        assert ok, f"{name} {t.name}: zeros differ ({why})"
+        host_pkg.append((oc, os_, oz))
+        if i % 28 == 27 or i + 1 == len(w.tensors):
+            _log(f"{name}: package of {i + 1}/{len(w.tensors)} tensors bit-exact")
+    del W
+    torch.cuda.empty_cache()
+    for k, dt in recon:
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        out = gpu.reconstruct(codes, scales, zeros, rows, 4096, G, k, tdt)
         torch.cuda.synchronize()
-        got = out.view(ng, G)[idx_t].cpu().view(torch.int16).numpy().view(np.uint16).reshape(-1)
-        assert np.array_equal(got, oracle.c_reconstruct(oc, os_, oz, G, k, "bf16")), f"k={k}"
+        for t, (oc, os_, oz) in zip(w.tensors, host_pkg):
+            want = oracle.c_reconstruct(oc, os_, oz, G, k, dt)
+            ok, why = _same(out.view(-1)[t.offset:t.offset + t.numel], want)
+            assert ok, f"{name} {t.name}: reconstruction k={k} {dt} differs ({why})"
+        _log(f"{name}: reconstruction k={k} {dt} of all {len(w.tensors)} tensors bit-exact")
         del out
-    del W, codes, scales, zeros
+        torch.cuda.empty_cache()
+    del codes, scales, zeros
     torch.cuda.empty_cache()
 
 
-def test_qwen3_8b_stack36_sampled(gpu):
-    _sampled_stack_check(gpu, "qwen3_8b_stack36")
+@pytest.mark.timeout(900)
+def test_qwen3_8b_stack36_full(gpu):
+    """The 36-layer Qwen3-8B-shaped stack (6.95e9 weights): package and the
+    k = 2, 4 reconstructions in both output types, every element."""
+    _full_stack_check(gpu, "qwen3_8b_stack36",
+                      [(2, "bf16"), (4, "bf16"), (2, "f32"), (4, "f32")])
 
 
-def test_dense32b_stack64_sampled(gpu):
-    _sampled_stack_check(gpu, "dense32b_stack64")
+@pytest.mark.timeout(900)
+def test_dense32b_stack64_full(gpu):
+    """The 64-layer 32B-class stack (2.92e10 weights): package and the k = 3
+    reconstruction in both output types, every element."""
+    _full_stack_check(gpu, "dense32b_stack64", [(3, "bf16"), (3, "f32")])
 
 
 # ---------------------------------------------------------------------------
@@ -283,6 +324,48 @@ def test_reconstruct_random_packages(gpu):
                 want = oracle.c_reconstruct(codes, sc, ze, G, k, dt)
                 gb = got.cpu().view(torch.int32 if dt == "f32" else torch.int16).numpy().reshape(-1)
                 assert np.array_equal(gb.view(want.dtype), want), (G, S, k, dt)
+
+
+def test_flipped_code_bit(gpu):
+    """A package with one code bit flipped 
+    the GPU reconstruction equals the oracle's of the same flipped package,
+    and differs from the unflipped one in exactly the element that owns the
+    bit (binary32 output) or at most there (bfloat16 output), and only for
+    prefixes that include the flipped stage (Eq. 8)."""
+    import torch
+    rows, cols, G, S = 48, 1280, 128, 4
+    n = rows * cols
+    bits = _random_bits(131, n)
+    oc, os_, oz = oracle.c_construct(bits, G, S)
+    rng = np.random.default_rng(7)
+    ts, tz = _dev(os_), _dev(oz)
+    checked = 0
+    for _ in range(12):
+        t, word, bit = int(rng.integers(0, S)), int(rng.integers(0, n // 16)), int(rng.integers(0, 32))
+        e = word * 16 + bit // 2
+        if os_[t, e // G] == 0:
+            continue
+        fc = oc.copy()
+        fc[t, word] ^= np.uint32(1 << bit)
+        tc = _dev(fc)
+        for k in range(1, S + 1):
+            for dt, tdt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+                got = gpu.reconstruct(tc, ts, tz, rows, cols, G, k, tdt)
+                torch.cuda.synchronize()
+                want = oracle.c_reconstruct(fc, os_, oz, G, k, dt)
+                gb = got.cpu().contiguous().view(torch.int32 if dt == "f32" else torch.int16)
+                gb = gb.numpy().reshape(-1).view(want.dtype)
+                assert np.array_equal(gb, want), (t, word, bit, k, dt)
+                base = oracle.c_reconstruct(oc, os_, oz, G, k, dt)
+                diff = np.nonzero(gb != base)[0].tolist()
+                if k <= t:
+                    assert diff == [], (t, word, bit, k, dt, diff)
+                elif dt == "f32":
+                    assert diff == [e], (t, word, bit, k, dt, diff)
+                else:
+                    assert set(diff) <= {e}, (t, word, bit, k, dt, diff)
+        checked += 1
+    assert checked >= 8
 
 
 def test_stream_argument(gpu):

@@ -1,5 +1,8 @@
-"""The HBM streaming probe writes exactly what include/hbm_probe.h states:
-the first 80 bytes of every 128 bytes of src, packed into dst."""
+"""The HBM probes write exactly what include/hbm_probe.h states: the mixed
+probe packs the first 80 bytes of every 128 bytes of src into dst, the
+read-only probe XORs what it reads, the write-only probe fills, and the
+construct-pattern probe stores XORs of each group's words in rrq_construct's
+planes."""
 
 import numpy as np
 import pytest
@@ -53,3 +56,38 @@ def test_write_probe_fill(gpu, nbytes):
     d = dst.cpu().numpy().view(np.uint32)
     assert np.all(d[:nbytes // 4] == 0x12345678)
     assert np.all(d[nbytes // 4:] == 0xFFFFFFFF)   # nothing written past the end
+
+
+@pytest.mark.parametrize("G,n_groups,S,bpc", [
+    (128, 64 * 3 + 5, 4, 0), (64, 1000, 3, 0), (32, 64 * 300 + 17, 4, 0),
+    (128, 64 * 2048 + 3, 4, 0), (128, 64 * 700 + 9, 2, 1), (32, 64 * 40, 1, 32),
+])
+def test_construct_probe_output(gpu, G, n_groups, S, bpc):
+    """The construct-pattern probe stores exactly what include/hbm_probe.h
+    states, in rrq_construct's planes, and nothing past them."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+    print(f"construct probe G={G} n_groups={n_groups} S={S} blocks_per_cu={bpc}", flush=True)
+    nw = n_groups * G // 2                      # 32-bit words of input
+    g = torch.Generator(device="cuda").manual_seed(n_groups + G)
+    src = torch.randint(-2**31, 2**31 - 1, (nw,), dtype=torch.int32, device="cuda", generator=g)
+    wpg = G // 16
+    codes = torch.full((S * n_groups * wpg + 8,), -1, dtype=torch.int32, device="cuda")
+    scales = torch.full((S * n_groups + 8,), -1, dtype=torch.int32, device="cuda")
+    zeros = torch.full((S * n_groups + 8,), -1, dtype=torch.int32, device="cuda")
+    probe.hbm_probe_construct(src, n_groups, G, S, codes, scales, zeros, bpc)
+    torch.cuda.synchronize()
+    w = src.cpu().numpy().view(np.uint32).reshape(n_groups, G // 2)
+    acc = np.bitwise_xor.reduce(w.reshape(n_groups, (G // 2) // wpg, wpg), axis=1)
+    c = codes.cpu().numpy().view(np.uint32)
+    sc = scales.cpu().numpy().view(np.uint32)
+    ze = zeros.cpu().numpy().view(np.uint32)
+    for k in range(S):
+        kk = np.uint32(k)
+        assert np.array_equal(c[k * n_groups * wpg:(k + 1) * n_groups * wpg],
+                              (acc ^ kk).reshape(-1)), f"codes of stage {k}"
+        assert np.array_equal(sc[k * n_groups:(k + 1) * n_groups], w[:, 0] ^ kk), f"scales {k}"
+        assert np.array_equal(ze[k * n_groups:(k + 1) * n_groups], w[:, 1] ^ kk), f"zeros {k}"
+    assert np.all(c[S * n_groups * wpg:] == 0xFFFFFFFF)
+    assert np.all(sc[S * n_groups:] == 0xFFFFFFFF) and np.all(ze[S * n_groups:] == 0xFFFFFFFF)

@@ -347,6 +347,33 @@ def test_bf16_rounding_ties_and_carry():
     assert np.array_equal(torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16), want)
 
 
+def test_flipped_code_bit_changes_exactly_its_element():
+    """Eq. 8 sums per-element stage values: flipping one bit of a stored code
+    changes the prefix reconstruction in exactly one element, the one the
+    packing rule (element e in word e // 16, bits 2 (e % 16) .. +1) assigns
+    to that bit, and only for prefixes that include the flipped stage."""
+    rng = np.random.default_rng(41)
+    G, S, n = 32, 4, 32 * 24
+    x = (rng.standard_normal(n) * 0.02).astype(np.float32)
+    bits = o.f32_to_bf16_bits(x)
+    codes, scales, zeros = o.construct(bits, 1, n, G, S)
+    checked = 0
+    for _ in range(40):
+        t, word, bit = int(rng.integers(0, S)), int(rng.integers(0, n // 16)), int(rng.integers(0, 32))
+        e = word * 16 + bit // 2
+        if scales[t, e // G] == 0:      # a degenerate stage has no grid to move on
+            continue
+        flipped = codes.copy()
+        flipped[t, word] ^= np.uint32(1 << bit)
+        for k in range(1, S + 1):
+            a = o.reconstruct(codes, scales, zeros, G, k)
+            b = o.reconstruct(flipped, scales, zeros, G, k)
+            diff = np.nonzero(a.view(np.uint32) != b.view(np.uint32))[0].tolist()
+            assert diff == ([e] if k > t else []), (t, word, bit, k, diff)
+        checked += 1
+    assert checked >= 30
+
+
 def test_pack_layout():
     Q = np.zeros(32, dtype=np.uint8)
     Q[0], Q[1], Q[15], Q[16] = 1, 2, 3, 3
