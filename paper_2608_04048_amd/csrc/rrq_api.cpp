@@ -90,12 +90,15 @@ int construct_common(const uint16_t *W, int64_t rows, int64_t cols, int32_t grou
     if (!aligned(W, 16) || !aligned(codes, 16) || (pmr && !aligned(pmr, 4))) return RRQ_ERR_ALIGN;
     if (from_base && n_stages == 1) return RRQ_OK;   // the package is the base alone
     const int64_t n_groups = n / group_size;
+    const int cus = current_cu_count();
+    if (cus <= 0) return RRQ_ERR_HIP;
+    const int lanes = rrq_detail::construct_lanes(n_groups, group_size, pmr != nullptr, cus);
     int grid = 0;
-    st = grid_for(n_groups, 64, rrq_detail::kConstructBlocksPerCU, &grid);
+    st = grid_for(n_groups * lanes, 64, rrq_detail::construct_blocks_per_cu(group_size, lanes), &grid);
     if (st != RRQ_OK) return st;
     hipError_t e = rrq_detail::launch_construct(W, n_groups, group_size, n_stages, codes, scales,
                                                 zeros, pmr, from_base, zero_point, scale_type,
-                                                grid, stream);
+                                                lanes, grid, stream);
     return e == hipSuccess ? RRQ_OK : RRQ_ERR_HIP;
 }
 

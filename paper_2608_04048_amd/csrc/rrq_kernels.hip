@@ -308,6 +308,30 @@ __device__ __forceinline__ void group_range(const float (&r)[G], float &lo, floa
     hi = fmaxf(h0, h1);
 }
 
+// Range of a group split over L consecutive lanes (L = 1, 2 or 4): each lane
+// holds a contiguous share of the group and its own partial lo, hi; DPP quad
+// permutes exchange them (min and max are exact, so the order of combination
+// does not matter).
+template <int CTRL>
+__device__ __forceinline__ float dpp_quad(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+template <int L>
+__device__ __forceinline__ void combine_range(float &lo, float &hi)
+{
+    static_assert(L == 1 || L == 2 || L == 4, "lanes per group");
+    if constexpr (L >= 2) {   // partner lane ^ 1: quad_perm [1, 0, 3, 2]
+        lo = fminf(lo, dpp_quad<0xB1>(lo));
+        hi = fmaxf(hi, dpp_quad<0xB1>(hi));
+    }
+    if constexpr (L >= 4) {   // partner lane ^ 2: quad_perm [2, 3, 0, 1]
+        lo = fminf(lo, dpp_quad<0x4E>(lo));
+        hi = fmaxf(hi, dpp_quad<0x4E>(hi));
+    }
+}
+
 // Stores one lane's code words of one stage at byte offset off of the
 // stage's per-tile resource.
 template <int G>
@@ -370,7 +394,8 @@ struct TileOut {
     char *scales;        // binary32, or 16-bit patterns (the kernel's SC)
     float *zeros;
     int64_t words_per_stage, n_groups;
-    uint32_t groups_here;
+    uint32_t shares_here;   // lane shares of groups in the tile (codes)
+    uint32_t groups_here;   // groups in the tile (scales, zeros)
 };
 
 // Scale storage SC (kScaleF32, kScaleF16, kScaleBF16): the binary32 value of
@@ -395,32 +420,35 @@ __device__ __forceinline__ float round_scale(float s)
 // the wait for the prefetched tile at the top of the tile loop count past
 // the previous tile's stores instead of draining them (loads and stores share
 // one in-order counter on this architecture).
-template <int G, int ZP, int SC>
+template <int E, int L, int ZP, int SC>
 __device__ __forceinline__ void store_stage(const TileOut &o, int k, int lane,
-                                            const uint32_t (&words)[G / 16], float s, float z,
+                                            const uint32_t (&words)[E / 16], float s, float z,
                                             bool active = true)
 {
     // Lanes past the last group fall outside the resources; their stores
-    // are dropped.
-    // (read back as a wave-uniform value: the resource must stay scalar)
+    // are dropped. The L lanes of a group store the same scale and zero-point
+    // to the same address.
+    // (read back as wave-uniform values: the resources must stay scalar)
+    const uint32_t shares = __builtin_amdgcn_readfirstlane(active ? o.shares_here : 0u);
     const uint32_t groups = __builtin_amdgcn_readfirstlane(active ? o.groups_here : 0u);
-    store_words<G>(make_rsrc(o.codes + k * o.words_per_stage, groups * (G / 16) * 4),
-                   lane * (G / 16) * 4, words);
+    const uint32_t gl = (uint32_t)lane / L;
+    store_words<E>(make_rsrc(o.codes + k * o.words_per_stage, shares * (E / 16) * 4),
+                   lane * (E / 16) * 4, words);
     if constexpr (SC == kScaleF32) {
         __builtin_amdgcn_raw_buffer_store_b32(
             __float_as_uint(s), make_rsrc(o.scales + k * o.n_groups * 4, groups * 4),
-            lane * 4, 0, 0);
+            gl * 4, 0, 0);
     } else {
         // s already holds a value of the 16-bit type: the conversion is exact
         const uint16_t b = SC == kScaleF16 ? __builtin_bit_cast(uint16_t, (_Float16)s)
                                            : (uint16_t)(__float_as_uint(s) >> 16);
         __builtin_amdgcn_raw_buffer_store_b16(
-            b, make_rsrc(o.scales + k * o.n_groups * 2, groups * 2), lane * 2, 0, 0);
+            b, make_rsrc(o.scales + k * o.n_groups * 2, groups * 2), gl * 2, 0, 0);
     }
     if constexpr (ZP != kZpSymmetric)
         __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(z),
                                               make_rsrc(o.zeros + k * o.n_groups, groups * 4),
-                                              lane * 4, 0, 0);
+                                              gl * 4, 0, 0);
 }
 
 // fl(d / 3) for every finite d >= 0 in five fewer dependent steps than the
@@ -497,33 +525,36 @@ __device__ __forceinline__ void fill_table(const DequantTable &tab, int lane, fl
 }
 
 // Loads one lane's base stage (plane 0 of the package) for tile `tile`: its
-// group's code words, scale and zero-point. Lanes past the input, and a tile
-// past the end, read zeros.
-template <int G, int ZP, int SC>
+// share's code words (E elements, L lanes per group), the group's scale and
+// zero-point. Lanes past the input, and a tile past the end, read zeros.
+template <int E, int L, int ZP, int SC>
 __device__ __forceinline__ void load_base(const uint32_t *codes, const char *scales,
                                           const float *zeros, int64_t n_groups, int64_t tile,
-                                          int lane, uint32_t (&bw)[G / 16], float &s0, float &z0)
+                                          int lane, uint32_t (&bw)[E / 16], float &s0, float &z0)
 {
-    const int64_t left = n_groups - tile * 64;
-    const int64_t g0 = left <= 0 ? 0 : tile * 64;
-    const uint32_t groups_here = left <= 0 ? 0u : (uint32_t)(left < 64 ? left : 64);
-    const rsrc_t rc = make_rsrc(codes + g0 * (G / 16), groups_here * (G / 16) * 4);
-    if constexpr (G / 16 >= 4) {
+    const int64_t left = n_groups * L - tile * 64;
+    const int64_t first = left <= 0 ? 0 : tile * 64;          // first share of the tile
+    const uint32_t shares_here = left <= 0 ? 0u : (uint32_t)(left < 64 ? left : 64);
+    const int64_t g0 = first / L;
+    const uint32_t groups_here = shares_here / L;
+    const uint32_t gl = (uint32_t)lane / L;
+    const rsrc_t rc = make_rsrc(codes + first * (E / 16), shares_here * (E / 16) * 4);
+    if constexpr (E / 16 >= 4) {
 #pragma unroll
-        for (int i = 0; i < G / 16; i += 4) {
-            const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rc, lane * (G / 16) * 4 + 4 * i, 0, 0);
+        for (int i = 0; i < E / 16; i += 4) {
+            const u32x4 x = __builtin_amdgcn_raw_buffer_load_b128(rc, lane * (E / 16) * 4 + 4 * i, 0, 0);
             bw[i] = x.x; bw[i + 1] = x.y; bw[i + 2] = x.z; bw[i + 3] = x.w;
         }
     } else {
-        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(rc, lane * (G / 16) * 4, 0, 0);
+        const u32x2 x = __builtin_amdgcn_raw_buffer_load_b64(rc, lane * (E / 16) * 4, 0, 0);
         bw[0] = x.x; bw[1] = x.y;
     }
     if constexpr (SC == kScaleF32) {
         s0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-            make_rsrc(scales + g0 * 4, groups_here * 4), lane * 4, 0, 0));
+            make_rsrc(scales + g0 * 4, groups_here * 4), gl * 4, 0, 0));
     } else {
         const uint16_t b = __builtin_amdgcn_raw_buffer_load_b16(
-            make_rsrc(scales + g0 * 2, groups_here * 2), lane * 2, 0, 0);
+            make_rsrc(scales + g0 * 2, groups_here * 2), gl * 2, 0, 0);
         s0 = SC == kScaleF16 ? (float)__builtin_bit_cast(_Float16, b)
                              : __uint_as_float((uint32_t)b << 16);
     }
@@ -531,40 +562,53 @@ __device__ __forceinline__ void load_base(const uint32_t *codes, const char *sca
         z0 = 2.0f;
     else
         z0 = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-            make_rsrc(zeros + g0, groups_here * 4), lane * 4, 0, 0));
+            make_rsrc(zeros + g0, groups_here * 4), gl * 4, 0, 0));
 }
 
-// Two waves per SIMD: the G = 128 kernel holds 128 residuals plus the
-// prefetched next tile per lane, so 256 VGPRs is the budget.
+// One group per lane (L = 1), or a group split over L = 2 or 4 consecutive
+// lanes, each holding a contiguous share of E = G / L elements (for calls too
+// small to give every wave many tiles: the serial work per wave and tile
+// drops L-fold). A tile is 64 shares; every per-element step is the same, the
+// group's range is combined across its lanes, and each lane then forms the
+// same scale, reciprocal and zero-point.
+// Waves per SIMD: a lane holding E = 128 elements keeps 128 residuals plus
+// the prefetched next tile, so 256 VGPRs is the budget (two waves); E = 64
+// needs 156 (three waves: the lookups in flight stay the same), E = 32 about
+// 80 (four waves).
 // FROM_BASE: plane 0 of codes / scales / zeros holds a base checkpoint on
 // entry (read only); the kernel forms R_0 = W - dequant(base) and writes the
 // residual stages 1 .. n_stages - 1 (n_stages >= 2).
-// ZP: zero-point kind; SC: scale storage type. pmr (may be NULL): per-group
-// peak-to-mean ratios of W as a side output. STATS_ONLY: only pmr.
-template <int G, bool FROM_BASE, int ZP, int SC, bool STATS_ONLY = false>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void construct_kernel(const uint4 *__restrict__ W,
-                                                       int64_t n_groups, int n_stages,
-                                                       uint32_t *__restrict__ codes,
-                                                       char *__restrict__ scales,
-                                                       float *__restrict__ zeros,
-                                                       float *__restrict__ pmr)
+// ZP: zero-point kind; SC: scale storage type. pmr (may be NULL; L = 1
+// only): per-group peak-to-mean ratios of W as a side output. STATS_ONLY:
+// only pmr.
+constexpr int construct_waves_per_simd(int E) { return E >= 128 ? 2 : E >= 64 ? 3 : 4; }
+
+template <int G, bool FROM_BASE, int ZP, int SC, bool STATS_ONLY = false, int L = 1>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
+    construct_waves_per_simd(G / L), construct_waves_per_simd(G / L)))) void construct_kernel(
+    const uint4 *__restrict__ W, int64_t n_groups, int n_stages, uint32_t *__restrict__ codes,
+    char *__restrict__ scales, float *__restrict__ zeros, float *__restrict__ pmr)
 {
+    static_assert(L == 1 || !STATS_ONLY, "the peak-to-mean ratio needs one lane per group");
     if (FROM_BASE && n_stages < 2) return;
-    constexpr int CH = G / 8;            // 16-byte chunks (8 bfloat16) per group
-    constexpr int HC = CH / 2;           // chunks per half group
-    constexpr int WPG = G / 16;          // code words per group and stage
-    constexpr int ROW = HC + 1;          // LDS row of one half group, padded by 16 bytes
-    constexpr int GROUPS_PER_LOAD = 64 / CH;
-    // The tile is transposed through LDS half a group at a time. Padding each
+    constexpr int E = G / L;             // elements per lane
+    static_assert(E >= 32, "a lane holds at least 32 elements");
+    constexpr int CH = E / 8;            // 16-byte chunks (8 bfloat16) per lane share
+    constexpr int HC = CH / 2;           // chunks per half share
+    constexpr int WPG = E / 16;          // code words per lane share and stage
+    constexpr int ROW = HC + 1;          // LDS row of one half share, padded by 16 bytes
+    constexpr int SHARES_PER_LOAD = 64 / CH;
+    // The tile is transposed through LDS half a share at a time. Padding each
     // row by one chunk spreads both access patterns over all banks: a row
-    // write (lanes -> consecutive chunks of a group) and a column read
-    // (lanes -> the same chunk of consecutive groups).
+    // write (lanes -> consecutive chunks of a share) and a column read
+    // (lanes -> the same chunk of consecutive shares).
     __shared__ uint4 tile_lds[64 * ROW];
     __shared__ f32x2 table_lds[16 * 64];
 
     const int lane = threadIdx.x;
-    const int64_t n_tiles = (n_groups + 63) / 64;
-    // A lane's loaded chunks all have the same index within their group
+    const int64_t n_shares = n_groups * L;
+    const int64_t n_tiles = (n_shares + 63) / 64;
+    // A lane's loaded chunks all have the same index within their share
     // (lane % CH), so each lane writes in exactly one of the two passes.
     const int my_half = (lane % CH) / HC;
     uint4 *const wr_base = tile_lds + (lane / CH) * ROW + (lane % HC);
@@ -577,29 +621,31 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
     uint32_t bw[WPG];            // base stage of the tile in v (with a base)
     float bs = 0.f, bz = 0.f;
     if (tile < n_tiles) {
-        load_tile<CH>(W, n_groups, tile, lane, v);
+        load_tile<CH>(W, n_shares, tile, lane, v);
         if constexpr (FROM_BASE)
-            load_base<G, ZP, SC>(codes, scales, zeros, n_groups, tile, lane, bw, bs, bz);
+            load_base<E, L, ZP, SC>(codes, scales, zeros, n_groups, tile, lane, bw, bs, bz);
     }
     // The stores of one tile, dropped (see store_stage): the loop is entered
     // with the same operations outstanding as after each tile.
     {
         // (distinct planes, so that no store looks overwritten by the next)
-        const TileOut none = {codes, scales, zeros, 1, 1, 0u};
+        const TileOut none = {codes, scales, zeros, 1, 1, 0u, 0u};
         const uint32_t zw[WPG] = {};
-        store_pmr<G>(pmr, 0, 0u, lane, 0.f, 0.f, 0.f);
+        if constexpr (L == 1) store_pmr<G>(pmr, 0, 0u, lane, 0.f, 0.f, 0.f);
         if constexpr (!STATS_ONLY) {
 #pragma unroll
             for (int k = 0; k < kMaxStages; ++k)
-                store_stage<G, ZP, SC>(none, k, lane, zw, 0.f, 0.f, false);
+                store_stage<E, L, ZP, SC>(none, k, lane, zw, 0.f, 0.f, false);
         }
     }
 
     for (; tile < n_tiles; tile += gridDim.x) {
-        const int64_t g0 = tile * 64;
-        const uint32_t groups_here = (uint32_t)(n_groups - g0 < 64 ? n_groups - g0 : 64);
+        const int64_t first = tile * 64;               // first share of the tile
+        const uint32_t shares_here = (uint32_t)(n_shares - first < 64 ? n_shares - first : 64);
+        const int64_t g0 = first / L;                  // first group of the tile
+        const uint32_t groups_here = shares_here / L;
 
-        float r[G];
+        float r[E];
         float bl0 = 0.f, bl1 = 0.f, bh0 = 0.f, bh1 = 0.f;   // range of R_0 (with a base)
         serial_priority(true);
         if constexpr (FROM_BASE) fill_table(tab, lane, bs, bz);
@@ -608,41 +654,43 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             __syncthreads();   // earlier reads of the buffer are complete
             if (my_half == h) {
 #pragma unroll
-                for (int i = 0; i < CH; ++i) wr_base[i * GROUPS_PER_LOAD * ROW] = v[i];
+                for (int i = 0; i < CH; ++i) wr_base[i * SHARES_PER_LOAD * ROW] = v[i];
             }
             __syncthreads();
-            gather_half<G>(rd_base, h, r);
+            gather_half<E>(rd_base, h, r);
             // With a base checkpoint, R_0 = W - dequant(base), half by half.
             if constexpr (FROM_BASE) {
-                if (h == 0) subtract_base_half<G, 0>(r, bw, tab, bl0, bl1, bh0, bh1);
-                else subtract_base_half<G, 1>(r, bw, tab, bl0, bl1, bh0, bh1);
+                if (h == 0) subtract_base_half<E, 0>(r, bw, tab, bl0, bl1, bh0, bh1);
+                else subtract_base_half<E, 1>(r, bw, tab, bl0, bl1, bh0, bh1);
             }
         }
 
         serial_priority(false);
         // |x| sum for the peak-to-mean side output (the weights, before any stage)
-        const bool stats = !FROM_BASE && pmr != nullptr;
+        const bool stats = L == 1 && !FROM_BASE && pmr != nullptr;
         float abs_sum = 0.f;
-        if (stats) abs_sum = group_abs_sum<G>(r);
+        if (stats) abs_sum = group_abs_sum<E>(r);
 
         // Prefetch the next tile while this one is quantized.
-        load_tile<CH>(W, n_groups, tile + gridDim.x, lane, v);
+        load_tile<CH>(W, n_shares, tile + gridDim.x, lane, v);
 
         constexpr int64_t scale_bytes = SC == kScaleF32 ? 4 : 2;
-        const TileOut out = {codes + g0 * WPG, scales + g0 * scale_bytes, zeros + g0,
-                             n_groups * WPG, n_groups, groups_here};
+        const TileOut out = {codes + first * WPG, scales + g0 * scale_bytes, zeros + g0,
+                             n_shares * WPG, n_groups, shares_here, groups_here};
 
         float lo, hi, inv = 0.f, sq = 0.f, z = 0.f, m = 0.f;
         uint32_t words[WPG] = {};
         if constexpr (FROM_BASE) {
             lo = fminf(bl0, bl1);
             hi = fmaxf(bh0, bh1);
+            combine_range<L>(lo, hi);
         } else {
             serial_priority(true);
-            group_range<G>(r, lo, hi);
+            group_range<E>(r, lo, hi);
+            combine_range<L>(lo, hi);
             serial_priority(false);
         }
-        store_pmr<G>(pmr, g0, stats ? groups_here : 0u, lane, lo, hi, abs_sum);
+        if constexpr (L == 1) store_pmr<G>(pmr, g0, stats ? groups_here : 0u, lane, lo, hi, abs_sum);
         if constexpr (STATS_ONLY) continue;
         // Stage slots 0 .. kMaxStages - 2 hold the stages that update the
         // residual; a slot outside 1 + FROM_BASE .. n_stages - 1 computes
@@ -654,19 +702,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2, 2))) void
                 serial_priority(true);
                 stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
                 fill_table(tab, lane, sq, z);
-                stage_elements<G, true, ZP>(r, inv, m, z, tab, words, lo, hi);
+                stage_elements<E, true, ZP>(r, inv, m, z, tab, words, lo, hi);
+                combine_range<L>(lo, hi);
             }
-            store_stage<G, ZP, SC>(out, k, lane, words, sq, z, active);
+            store_stage<E, L, ZP, SC>(out, k, lane, words, sq, z, active);
         }
         // The next tile's base stage, loaded where the last stage leaves
         // registers free; only this stage's stores are issued after it.
         if constexpr (FROM_BASE)
-            load_base<G, ZP, SC>(codes, scales, zeros, n_groups, tile + gridDim.x, lane, bw, bs,
-                                 bz);
+            load_base<E, L, ZP, SC>(codes, scales, zeros, n_groups, tile + gridDim.x, lane, bw,
+                                    bs, bz);
         serial_priority(true);
         stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
-        stage_elements<G, false, ZP>(r, inv, m, z, tab, words, lo, hi);
-        store_stage<G, ZP, SC>(out, n_stages - 1, lane, words, sq, z);
+        stage_elements<E, false, ZP>(r, inv, m, z, tab, words, lo, hi);
+        store_stage<E, L, ZP, SC>(out, n_stages - 1, lane, words, sq, z);
     }
 }
 
@@ -794,25 +843,28 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
 
 template <bool FROM_BASE, int ZP, int SC>
 hipError_t launch_construct_s(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
-                              char *scales, float *zeros, float *pmr, int grid, hipStream_t stream)
+                              char *scales, float *zeros, float *pmr, int lanes, int grid,
+                              hipStream_t stream)
 {
-    switch (G) {
-    case 32: return launch(construct_kernel<32, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros, pmr);
-    case 64: return launch(construct_kernel<64, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros, pmr);
-    case 128: return launch(construct_kernel<128, FROM_BASE, ZP, SC>, grid, 64, stream, w4, n_groups, S, codes, scales, zeros, pmr);
-    default: return hipErrorInvalidValue;
-    }
+#define RRQ_CONSTRUCT_CASE(GS, LS)                                                                 \
+    if (G == GS && lanes == LS)                                                                    \
+        return launch(construct_kernel<GS, FROM_BASE, ZP, SC, false, LS>, grid, 64, stream, w4,   \
+                      n_groups, S, codes, scales, zeros, pmr);
+    RRQ_CONSTRUCT_CASE(32, 1) RRQ_CONSTRUCT_CASE(64, 1) RRQ_CONSTRUCT_CASE(128, 1)
+    RRQ_CONSTRUCT_CASE(64, 2) RRQ_CONSTRUCT_CASE(128, 4)
+#undef RRQ_CONSTRUCT_CASE
+    return hipErrorInvalidValue;
 }
 
 template <bool FROM_BASE, int ZP>
 hipError_t launch_construct_g(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
-                              char *scales, float *zeros, float *pmr, int scale_type, int grid,
-                              hipStream_t stream)
+                              char *scales, float *zeros, float *pmr, int scale_type, int lanes,
+                              int grid, hipStream_t stream)
 {
     switch (scale_type) {
-    case kScaleF32: return launch_construct_s<FROM_BASE, ZP, kScaleF32>(w4, n_groups, G, S, codes, scales, zeros, pmr, grid, stream);
-    case kScaleF16: return launch_construct_s<FROM_BASE, ZP, kScaleF16>(w4, n_groups, G, S, codes, scales, zeros, pmr, grid, stream);
-    case kScaleBF16: return launch_construct_s<FROM_BASE, ZP, kScaleBF16>(w4, n_groups, G, S, codes, scales, zeros, pmr, grid, stream);
+    case kScaleF32: return launch_construct_s<FROM_BASE, ZP, kScaleF32>(w4, n_groups, G, S, codes, scales, zeros, pmr, lanes, grid, stream);
+    case kScaleF16: return launch_construct_s<FROM_BASE, ZP, kScaleF16>(w4, n_groups, G, S, codes, scales, zeros, pmr, lanes, grid, stream);
+    case kScaleBF16: return launch_construct_s<FROM_BASE, ZP, kScaleBF16>(w4, n_groups, G, S, codes, scales, zeros, pmr, lanes, grid, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -820,27 +872,28 @@ hipError_t launch_construct_g(const uint4 *w4, int64_t n_groups, int G, int S, u
 template <bool FROM_BASE>
 hipError_t launch_construct_b(const uint4 *w4, int64_t n_groups, int G, int S, uint32_t *codes,
                               char *scales, float *zeros, float *pmr, int zero_point,
-                              int scale_type, int grid, hipStream_t stream)
+                              int scale_type, int lanes, int grid, hipStream_t stream)
 {
     switch (zero_point) {
-    case kZpInteger: return launch_construct_g<FROM_BASE, kZpInteger>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, grid, stream);
-    case kZpReal: return launch_construct_g<FROM_BASE, kZpReal>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, grid, stream);
-    case kZpSymmetric: return launch_construct_g<FROM_BASE, kZpSymmetric>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, grid, stream);
+    case kZpInteger: return launch_construct_g<FROM_BASE, kZpInteger>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, lanes, grid, stream);
+    case kZpReal: return launch_construct_g<FROM_BASE, kZpReal>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, lanes, grid, stream);
+    case kZpSymmetric: return launch_construct_g<FROM_BASE, kZpSymmetric>(w4, n_groups, G, S, codes, scales, zeros, pmr, scale_type, lanes, grid, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
                             uint32_t *codes, void *scales, float *zeros, float *pmr,
-                            bool from_base, int zero_point, int scale_type, int grid,
+                            bool from_base, int zero_point, int scale_type, int lanes, int grid,
                             hipStream_t stream)
 {
+    if (lanes != 1 && pmr != nullptr) return hipErrorInvalidValue;
     const uint4 *w4 = reinterpret_cast<const uint4 *>(W);
     char *sc = static_cast<char *>(scales);
     return from_base ? launch_construct_b<true>(w4, n_groups, G, S, codes, sc, zeros, nullptr,
-                                                zero_point, scale_type, grid, stream)
+                                                zero_point, scale_type, lanes, grid, stream)
                      : launch_construct_b<false>(w4, n_groups, G, S, codes, sc, zeros, pmr,
-                                                 zero_point, scale_type, grid, stream);
+                                                 zero_point, scale_type, lanes, grid, stream);
 }
 
 hipError_t launch_group_pmr(const uint16_t *W, int64_t n_groups, int G, float *pmr, int grid,

@@ -16,9 +16,10 @@ namespace rrq_detail {
 // stages 1 .. S-1 are written.
 // pmr (NULL for none; ignored with from_base): per-group peak-to-mean
 // ratios of W as a side output.
+// lanes: lanes per group (construct_lanes), grid: workgroups of one wave.
 hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
                             uint32_t *codes, void *scales, float *zeros, float *pmr,
-                            bool from_base, int zero_point, int scale_type, int grid,
+                            bool from_base, int zero_point, int scale_type, int lanes, int grid,
                             hipStream_t stream);
 
 // Per-group peak-to-mean ratios of W only.
@@ -75,8 +76,36 @@ constexpr int64_t kLinearMaxDim = int64_t(1) << 26;
 // Stages a package holds at most (RRQ_MAX_STAGES of rrq.h).
 constexpr int kMaxStages = 4;
 
-// Workgroups the construct kernel keeps resident per compute unit.
+// Workgroups (one wave each) the construct kernel keeps resident per compute
+// unit with one lane per group: two per SIMD.
 constexpr int kConstructBlocksPerCU = 8;
+// Lanes per group of the construct kernel. A wave takes tiles of 64 lane
+// shares; one share (a whole group at L = 1) is a long serial stretch of work
+// per wave (4 stages x G elements), and a call ends with its waves' last
+// tiles. A call with few tiles per resident wave therefore ends on that
+// latency, so such calls split each group over L = G / 32 lanes (32 elements
+// each): the serial work per wave drops L-fold and four waves per SIMD fit
+// instead of two. Measured on Qwen3-8B shapes at G = 128 (per call, MALL
+// flushed): 1024 x 4096 12.4 -> 7.9 us, 4096 x 4096 21.9 -> 20.0 us,
+// 12288 x 4096 53.8 -> 49.4 us (3 tiles per slot), 47104 x 4096 equal at
+// 11.5 tiles per slot; L = 2 at G = 128 was never the fastest. The
+// peak-to-mean side output needs one lane per group. tiles1 = tiles at L = 1.
+constexpr int64_t kConstructSplitMaxTilesPerSlot = 8;
+inline int construct_lanes(int64_t n_groups, int G, bool pmr, int cus)
+{
+    if (pmr || G == 32) return 1;
+    const int64_t tiles1 = (n_groups + 63) / 64;
+    const int64_t slots = (int64_t)cus * kConstructBlocksPerCU;
+    return tiles1 <= kConstructSplitMaxTilesPerSlot * slots ? G / 32 : 1;
+}
+// Resident one-wave workgroups per compute unit at L lanes per group: the
+// waves per SIMD the registers allow (two at 128 elements per lane, four at
+// 32), capped by LDS at 32 elements per lane (a wave's transpose buffer and
+// dequantization table take 11 KiB of 160).
+constexpr int construct_blocks_per_cu(int G, int lanes)
+{
+    return lanes == 1 ? kConstructBlocksPerCU : (G / lanes >= 64 ? 12 : 14);
+}
 // Reconstruct: threads per workgroup (4 waves), 16-byte output chunks per
 // lane per tile (8 bfloat16 or 4 binary32 elements each) and resident
 // workgroups per CU, as measured on the 36-layer stack (6.9e9 weights): 8

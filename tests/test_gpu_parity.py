@@ -197,6 +197,31 @@ def test_flat_call_equals_per_tensor_calls(gpu):
     assert all(torch.equal(x, y) for x, y in zip((codes, scales, zeros), again))
 
 
+@pytest.mark.parametrize("G", [64, 128])
+def test_split_lanes_equal_one_lane_per_group(gpu, G):
+    """Small calls split each group over G / 32 lanes, large calls keep one
+    lane per group; both give the same package (groups never span rows, so
+    slices of one flat call are independent calls). The flat call here has
+    more than 8 tiles per resident wave, the slices far fewer."""
+    import torch
+    n = 72 * 2 ** 20 * (G // 64)             # > 8 * 2048 tiles of 64 groups
+    cols = 4096
+    g = torch.Generator(device="cuda").manual_seed(G)
+    W = (torch.randn(n // cols, cols, generator=g, device="cuda") * 0.02).to(torch.bfloat16)
+    codes, scales, zeros = gpu.construct(W, G, 4)
+    piece = 1024 * cols
+    for off in range(0, n, n // 8):
+        c2, s2, z2 = gpu.construct(W.view(-1)[off:off + piece].view(-1, cols), G, 4)
+        torch.cuda.synchronize()
+        assert torch.equal(codes[:, off // 16:(off + piece) // 16], c2)
+        assert torch.equal(scales[:, off // G:(off + piece) // G], s2)
+        assert torch.equal(zeros[:, off // G:(off + piece) // G], z2)
+    bits = W.view(-1)[:piece].cpu().view(torch.int16).numpy().view(np.uint16)
+    oc, os_, oz = oracle.c_construct(bits, G, 4)
+    assert np.array_equal(_u32(codes[:, :piece // 16]), oc)
+    assert np.array_equal(_u32(scales[:, :piece // G]), os_.view(np.uint32))
+
+
 def _dev(a):
     """Host numpy array -> device tensor of the same bytes (int32 / int16)."""
     import torch
