@@ -496,6 +496,45 @@ def stream_probe(src_bytes, flush_buf=None, launches=10):
                        "frac": round(serial_gbs / HBM_PEAK_GBS, 4)}}
 
 
+def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5):
+    """rrq_construct called once per weight tensor (each tensor its own
+    package, laid out back to back in the package buffers), the way a
+    checkpoint stored tensor by tensor is quantized: mean time of one pass
+    over every tensor, HIP events on the launch stream."""
+    import torch
+
+    import paper_2608_04048_amd as rrq
+
+    G, S, n = w.group_size, w.n_stages, w.numel
+    cflat, sflat, zflat = codes.view(-1), scales.view(-1), zeros.view(-1)
+    calls = []
+    for t in w.tensors:
+        c = cflat[S * t.offset // 16:S * (t.offset + t.numel) // 16].view(S, t.numel // 16)
+        sc = sflat[S * t.offset // G:S * (t.offset + t.numel) // G].view(S, t.numel // G)
+        zz = zflat[S * t.offset // G:S * (t.offset + t.numel) // G].view(S, t.numel // G)
+        calls.append((W_flat[t.offset:t.offset + t.numel], t.rows, t.cols, c, sc, zz))
+
+    def one_pass():
+        for Wc, r_, c_, cc, sc, zz in calls:
+            rrq.rrq_construct(Wc, r_, c_, G, S, cc, sc, zz, stream)
+
+    one_pass()
+    ms = []
+    for _ in range(passes):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        one_pass()
+        b.record(stream)
+        b.synchronize()
+        ms.append(a.elapsed_time(b))
+    t = sum(ms) / len(ms)
+    cb = construct_bytes(n, G, S)
+    return {"calls": len(calls), "construct_ms": round(t, 4),
+            "gbs_bf16_weights": round(2 * n / (t * 1e-3) / 1e9, 1),
+            "hbm_gbs": round(cb / (t * 1e-3) / 1e9, 1),
+            "hbm_frac": round(cb / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def construct_probe(W, n, G, S, codes, scales, zeros, stream, flush_buf=None, launches=10,
                     blocks_per_cu=(8, 4, 16)):
     """Construction's own memory traffic with no arithmetic
@@ -529,6 +568,39 @@ def construct_probe(W, n, G, S, codes, scales, zeros, stream, flush_buf=None, la
     res = dict(out[blocks_per_cu[0]])
     res["bytes"] = moved
     res["by_blocks_per_cu"] = {str(k): v for k, v in out.items()}
+    return res
+
+
+def reconstruct_probe(n, G, ks, codes, scales, zeros, outs, stream, flush_buf=None,
+                      launches=10):
+    """Reconstruction's memory traffic with no arithmetic
+    (hbm_probe_reconstruct), bfloat16 out, at every prefix k the workload
+    reconstructs: the same package planes and output buffers and the same
+    launch as rrq_reconstruct (two 256-thread workgroups per CU)."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+
+    res = {}
+    for k in ks:
+        def run():
+            probe.hbm_probe_reconstruct(codes, scales, zeros, n // G, G, k, outs[k], 0, stream)
+        run()
+        vals = []
+        for _ in range(launches):
+            if flush_buf is not None:
+                flush_buf.fill_(1.0)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            run()
+            b.record(stream)
+            b.synchronize()
+            vals.append(a.elapsed_time(b))
+        t = sum(vals) / len(vals)
+        moved = reconstruct_bytes(n, G, k, 2)
+        gbs = moved / (t * 1e-3) / 1e9
+        res[str(k)] = {"ms": round(t, 4), "gbs": round(gbs, 1),
+                       "frac": round(gbs / HBM_PEAK_GBS, 4), "bytes": moved}
     return res
 
 
@@ -729,6 +801,9 @@ def main():
     if (rec is not None and w.name == "qwen3_8b_stack36" and not args.per_tensor
             and rec[0] == profiling.kernel_source_sha256()):
         result["roofline"]["traffic"] = rec[1]
+    if not args.per_tensor and len(w.tensors) > 1:
+        print("bench: timing one construct call per tensor", file=sys.stderr, flush=True)
+        result["per_tensor"] = time_per_tensor(w, W.view(-1), codes, scales, zeros, stream)
     if S >= 2 and not args.no_from_base:
         fb_ms, fb_min = time_from_base(calls, G, S, stream, flush_buf)
         fb_bytes = from_base_bytes(n, G, S)
@@ -760,6 +835,11 @@ def main():
             cp = construct_probe(W, n, G, S, codes, scales, zeros, stream, flush_buf)
             result["stream_probe"]["construct_pattern"] = cp
             result["construct_frac_of_construct_pattern"] = round(c_achieved / cp["gbs"], 4)
+            print("bench: reconstruct-pattern probe", file=sys.stderr, flush=True)
+            rp = reconstruct_probe(n, G, w.recon_k, codes, scales, zeros, outs, stream, flush_buf)
+            result["stream_probe"]["reconstruct_pattern"] = rp
+            result["reconstruct_frac_of_reconstruct_pattern"] = {
+                str(k): round(rp[str(k)]["ms"] / recon[str(k)]["ms"], 4) for k in w.recon_k}
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(w, W.view(-1), args.cpu_budget, args.cpu_threads)

@@ -5,8 +5,8 @@
  * 2-bit code planes plus binary32 scale and zero per group of 128), so the
  * mixed probe reads B bytes and writes 5B/8 bytes with the same kind of wide,
  * coalesced accesses, and no arithmetic; the read-only and write-only probes
- * give each direction's own ceiling, and the construct-pattern probe replays
- * construction's own loads and stores. Measurement aids only: they compute
+ * give each direction's own ceiling, and the construct-pattern and
+ * reconstruct-pattern probes replay those kernels' own loads and stores. Measurement aids only: they compute
  * nothing of the method.
  */
 #ifndef HBM_PROBE_H
@@ -91,6 +91,33 @@ int hbm_probe_write(void *dst, size_t dst_bytes, uint32_t value, hipStream_t str
 int hbm_probe_construct(const void *W, int64_t n_groups, int32_t group_size, int32_t n_stages,
                         uint32_t *codes, uint32_t *scales, uint32_t *zeros,
                         int32_t blocks_per_cu, hipStream_t stream);
+
+/*
+ * hbm_probe_reconstruct - enqueue one pass with the memory traffic of
+ * rrq_reconstruct (k_stages prefix, bfloat16 output) and no dequantization
+ * arithmetic: for every chunk of 8 consecutive elements (16 output bytes)
+ * and every stage t < k_stages it loads the chunk's code word (word
+ * e / 16 of plane t), its group's scale and its group's zero-point (32-bit
+ * words of plane t), and stores the chunk once. With x the XOR over the
+ * stages of those three words, chunk c (elements 8c .. 8c + 7) stores the
+ * 32-bit words x, x + 1, x + 2, x + 3 at out + 4c.
+ *
+ *   codes       device, planes of n_groups * group_size / 16 uint32 (at least
+ *               k_stages planes), 16-byte aligned.
+ *   scales,
+ *   zeros       device, planes of n_groups uint32 each, 4-byte aligned.
+ *   n_groups    >= 1.
+ *   group_size  32, 64 or 128.
+ *   k_stages    1 .. 4.
+ *   out         device, n_groups * group_size * 2 bytes, 16-byte aligned.
+ *   blocks_per_cu  resident 256-thread workgroups per compute unit, 1 .. 32;
+ *               0 = the reconstruct kernel's 2.
+ *
+ * Returns as hbm_probe_construct.
+ */
+int hbm_probe_reconstruct(const uint32_t *codes, const uint32_t *scales, const uint32_t *zeros,
+                          int64_t n_groups, int32_t group_size, int32_t k_stages, uint32_t *out,
+                          int32_t blocks_per_cu, hipStream_t stream);
 
 #ifdef __cplusplus
 }

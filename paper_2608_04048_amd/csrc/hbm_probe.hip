@@ -4,7 +4,8 @@
 // read-only and write-only ones bound each direction on its own. The
 // construct-pattern probe replays package construction's own memory traffic
 // (its tiles, loads, LDS transpose, prefetch and the 16 stores per tile over
-// 12 output planes) with no quantization arithmetic.
+// 12 output planes) with no quantization arithmetic, and the
+// reconstruct-pattern probe does the same for reconstruction (bfloat16 out).
 
 #include "hbm_probe.h"
 
@@ -196,6 +197,61 @@ __global__ __launch_bounds__(64) void construct_probe_kernel(const uint4 *__rest
     }
 }
 
+// Reconstruct-pattern probe: the reconstruct kernel's memory traffic for
+// bfloat16 output with no dequantization arithmetic. Workgroups of four
+// waves; a wave takes tiles of 64 U chunks of 8 elements (16 output bytes)
+// in a grid-stride loop, lane l owning chunks l, l + 64, ...; for each of the
+// k stages it loads the chunk's code word, its group's scale and its
+// group's zero-point (32-bit each), then stores the chunk with one 16-byte
+// store (each wave instruction covers 1 KiB). The stored chunk c is
+// {x, x + 1, x + 2, x + 3} with x the XOR over the k stages of those three
+// loaded words.
+template <int K, int U>
+__global__ __launch_bounds__(256) void reconstruct_probe_kernel(const uint32_t *__restrict__ codes,
+                                                                const uint32_t *__restrict__ scales,
+                                                                const uint32_t *__restrict__ zeros,
+                                                                int64_t n_elems, int64_t n_groups,
+                                                                int g_shift,
+                                                                uint32_t *__restrict__ out)
+{
+    constexpr int E = 8, CPW = 2, TILE = 64 * U;
+    const int lane = threadIdx.x & 63;
+    const int64_t n_chunks = n_elems / E, n_words = n_elems / 16;
+    const int64_t n_tiles = (n_chunks + TILE - 1) / TILE;
+    const int64_t n_waves = (int64_t)gridDim.x * 4;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < n_tiles; tile += n_waves) {
+        const int64_t c0 = tile * TILE;
+        const uint32_t chunks_here = (uint32_t)(n_chunks - c0 < TILE ? n_chunks - c0 : TILE);
+        const int64_t wfirst = c0 / CPW;
+        const uint32_t words_here = (chunks_here + CPW - 1) / CPW;
+        const int64_t gfirst = (c0 * E) >> g_shift;
+        const uint32_t groups_here =
+            (uint32_t)((((c0 + chunks_here) * E - 1) >> g_shift) - gfirst + 1);
+        uint32_t acc[U] = {};
+#pragma unroll
+        for (int t = 0; t < K; ++t) {
+            const prsrc_t rc = probe_rsrc(codes + t * n_words + wfirst, words_here * 4);
+            const prsrc_t rs = probe_rsrc(scales + t * n_groups + gfirst, groups_here * 4);
+            const prsrc_t rz = probe_rsrc(zeros + t * n_groups + gfirst, groups_here * 4);
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const uint32_t cl = j * 64 + lane;
+                const uint32_t gl = (uint32_t)((((c0 + cl) * E) >> g_shift) - gfirst);
+                acc[j] ^= __builtin_amdgcn_raw_buffer_load_b32(rc, (cl / CPW) * 4, 0, 0) ^
+                          __builtin_amdgcn_raw_buffer_load_b32(rs, gl * 4, 0, 0) ^
+                          __builtin_amdgcn_raw_buffer_load_b32(rz, gl * 4, 0, 0);
+            }
+        }
+        const prsrc_t ro = probe_rsrc(out + c0 * 4, chunks_here * 16);
+#pragma unroll
+        for (int j = 0; j < U; ++j) {
+            const pu32x4 v = {acc[j], acc[j] + 1, acc[j] + 2, acc[j] + 3};
+            __builtin_amdgcn_raw_buffer_store_b128(v, ro, (j * 64 + lane) * 16, 0, 0);
+        }
+    }
+}
+
 int grid_limit(int per_cu, int64_t work, int per_block, int *grid)
 {
     int dev = 0, cus = 0;
@@ -291,5 +347,38 @@ extern "C" int hbm_probe_construct(const void *W, int64_t n_groups, int32_t grou
                            w4, n_groups, (int)n_stages, codes, scales, zeros);
         break;
     }
+    return hipGetLastError() == hipSuccess ? 0 : 7;
+}
+
+extern "C" int hbm_probe_reconstruct(const uint32_t *codes, const uint32_t *scales,
+                                     const uint32_t *zeros, int64_t n_groups, int32_t group_size,
+                                     int32_t k_stages, uint32_t *out, int32_t blocks_per_cu,
+                                     hipStream_t stream)
+{
+    if (!codes || !scales || !zeros || !out) return 1;
+    if ((reinterpret_cast<uintptr_t>(codes) | reinterpret_cast<uintptr_t>(out)) % 16 != 0 ||
+        (reinterpret_cast<uintptr_t>(scales) | reinterpret_cast<uintptr_t>(zeros)) % 4 != 0)
+        return 2;
+    if (group_size != 32 && group_size != 64 && group_size != 128) return 3;
+    if (n_groups < 1 || k_stages < 1 || k_stages > 4 || blocks_per_cu < 0 || blocks_per_cu > 32)
+        return 3;
+    if (n_groups > INT64_MAX / (4 * group_size)) return 3;
+    const int64_t n = n_groups * group_size;
+    const int g_shift = group_size == 32 ? 5 : group_size == 64 ? 6 : 7;
+    // the reconstruct kernel's launch for bfloat16 output: 8 chunks per lane
+    // for 1 or 2 stages, 4 from 3 on; two workgroups of 256 per CU
+    const int U = k_stages <= 2 ? 8 : 4;
+    int grid = 0;
+    if (grid_limit(blocks_per_cu ? blocks_per_cu : 2, n, kThreads * U * 8, &grid)) return 7;
+#define RRQ_PROBE_RECON(KK, UU)                                                                   \
+    case KK:                                                                                       \
+        hipLaunchKernelGGL((reconstruct_probe_kernel<KK, UU>), dim3((unsigned)grid), dim3(kThreads), \
+                           0, stream, codes, scales, zeros, n, n_groups, g_shift, out);           \
+        break;
+    switch (k_stages) {
+        RRQ_PROBE_RECON(1, 8) RRQ_PROBE_RECON(2, 8) RRQ_PROBE_RECON(3, 4) RRQ_PROBE_RECON(4, 4)
+    default: return 3;
+    }
+#undef RRQ_PROBE_RECON
     return hipGetLastError() == hipSuccess ? 0 : 7;
 }

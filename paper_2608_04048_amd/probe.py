@@ -1,7 +1,8 @@
 """Binding of libhbm_probe.so (include/hbm_probe.h): streaming kernels used by
 the benchmark as practical HBM ceilings: one with package construction's
 read/write ratio (reads B bytes, writes 5B/8), a read-only and a write-only
-one, and one that replays package construction's own loads and stores."""
+one, and two that replay package construction's and reconstruction's own
+loads and stores."""
 
 from __future__ import annotations
 
@@ -32,6 +33,10 @@ def load_library() -> ctypes.CDLL:
                                             ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
         lib.hbm_probe_construct.restype = ctypes.c_int
+        lib.hbm_probe_reconstruct.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                              ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
+        lib.hbm_probe_reconstruct.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -83,3 +88,14 @@ def hbm_probe_construct(W, n_groups: int, group_size: int, n_stages: int, codes,
                                             _ptr(zeros), int(blocks_per_cu), _sp(stream))
     if st != 0:
         raise RuntimeError(f"hbm_probe_construct failed with status {st}")
+
+
+def hbm_probe_reconstruct(codes, scales, zeros, n_groups: int, group_size: int, k_stages: int,
+                          out, blocks_per_cu: int = 0, stream=None) -> None:
+    """Enqueue one pass with reconstruction's memory traffic, bfloat16 out
+    (see include/hbm_probe.h for what it stores)."""
+    st = load_library().hbm_probe_reconstruct(_ptr(codes), _ptr(scales), _ptr(zeros),
+                                              int(n_groups), int(group_size), int(k_stages),
+                                              _ptr(out), int(blocks_per_cu), _sp(stream))
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_reconstruct failed with status {st}")

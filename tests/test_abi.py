@@ -187,8 +187,8 @@ def test_probe_library_exports_declared_function():
     from paper_2608_04048_amd import probe
     text = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
     names = sorted(set(re.findall(r"\b(hbm_probe_\w+)\s*\(", text)))
-    assert names == ["hbm_probe_construct", "hbm_probe_read", "hbm_probe_stream",
-                     "hbm_probe_write"]
+    assert names == ["hbm_probe_construct", "hbm_probe_read", "hbm_probe_reconstruct",
+                     "hbm_probe_stream", "hbm_probe_write"]
     lib = probe.load_library()
     out = os.popen(f"nm -D --defined-only {probe.LIB_PATH}").read()
     for name in names:
@@ -244,6 +244,21 @@ def test_construct_probe_rejects(kw, status):
     a.update(kw)
     assert probe.load_library().hbm_probe_construct(
         a["W"], a["n_groups"], a["G"], a["S"], a["codes"], a["scales"], a["zeros"], a["bpc"],
+        None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(codes=0), 1), (dict(scales=0), 1), (dict(zeros=0), 1), (dict(out=0), 1),
+    (dict(codes=FAKE + 4), 2), (dict(out=FAKE + 8), 2), (dict(scales=FAKE + 2), 2),
+    (dict(zeros=FAKE + 1), 2), (dict(G=16), 3), (dict(n_groups=0), 3), (dict(k=0), 3),
+    (dict(k=5), 3), (dict(bpc=-1), 3), (dict(bpc=33), 3),
+])
+def test_reconstruct_probe_rejects(kw, status):
+    from paper_2608_04048_amd import probe
+    a = dict(codes=FAKE, scales=FAKE, zeros=FAKE, n_groups=64, G=128, k=2, out=FAKE, bpc=0)
+    a.update(kw)
+    assert probe.load_library().hbm_probe_reconstruct(
+        a["codes"], a["scales"], a["zeros"], a["n_groups"], a["G"], a["k"], a["out"], a["bpc"],
         None) == status
 
 

@@ -2,7 +2,7 @@
 probe packs the first 80 bytes of every 128 bytes of src into dst, the
 read-only probe XORs what it reads, the write-only probe fills, and the
 construct-pattern probe stores XORs of each group's words in rrq_construct's
-planes."""
+planes, and the reconstruct-pattern probe XORs of each chunk's loads."""
 
 import numpy as np
 import pytest
@@ -91,3 +91,35 @@ def test_construct_probe_output(gpu, G, n_groups, S, bpc):
         assert np.array_equal(ze[k * n_groups:(k + 1) * n_groups], w[:, 1] ^ kk), f"zeros {k}"
     assert np.all(c[S * n_groups * wpg:] == 0xFFFFFFFF)
     assert np.all(sc[S * n_groups:] == 0xFFFFFFFF) and np.all(ze[S * n_groups:] == 0xFFFFFFFF)
+
+
+@pytest.mark.parametrize("G,n_groups,k,bpc", [
+    (128, 3, 1, 0), (128, 64 * 33 + 7, 2, 0), (64, 1001, 3, 0), (32, 64 * 200 + 3, 4, 0),
+    (128, 64 * 2048 + 1, 4, 1), (64, 64 * 700, 2, 32),
+])
+def test_reconstruct_probe_output(gpu, G, n_groups, k, bpc):
+    """The reconstruct-pattern probe stores exactly what include/hbm_probe.h
+    states, and nothing past the output."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+    print(f"reconstruct probe G={G} n_groups={n_groups} k={k} blocks_per_cu={bpc}", flush=True)
+    n = n_groups * G
+    g = torch.Generator(device="cuda").manual_seed(n_groups * 7 + k)
+    rnd = lambda m: torch.randint(-2**31, 2**31 - 1, (m,), dtype=torch.int32, device="cuda",
+                                  generator=g)
+    codes, scales, zeros = rnd(4 * n // 16), rnd(4 * n_groups), rnd(4 * n_groups)
+    out = torch.full((n // 2 + 8,), -1, dtype=torch.int32, device="cuda")
+    probe.hbm_probe_reconstruct(codes, scales, zeros, n_groups, G, k, out, bpc)
+    torch.cuda.synchronize()
+    c = codes.cpu().numpy().view(np.uint32).reshape(4, n // 16)
+    s_ = scales.cpu().numpy().view(np.uint32).reshape(4, n_groups)
+    z_ = zeros.cpu().numpy().view(np.uint32).reshape(4, n_groups)
+    chunk = np.arange(n // 8)
+    x = np.zeros(n // 8, dtype=np.uint32)
+    for t in range(k):
+        x ^= c[t][chunk // 2] ^ s_[t][chunk * 8 // G] ^ z_[t][chunk * 8 // G]
+    want = np.stack([x, x + np.uint32(1), x + np.uint32(2), x + np.uint32(3)], axis=1).reshape(-1)
+    o = out.cpu().numpy().view(np.uint32)
+    assert np.array_equal(o[:n // 2], want)
+    assert np.all(o[n // 2:] == 0xFFFFFFFF)
