@@ -63,8 +63,17 @@ struct ItemSlot {
     static constexpr int DMA = CODE_DMA + 2;       // vector-memory loads per item
 };
 
+// Groups per wave GPW: the A operands of a wave's groups stay in its
+// registers (16 tokens x GPW groups, 16 GPW VGPRs). GPW = 4 serves rows of up
+// to 4096 inputs in at most 128 VGPRs, GPW = 8 up to 8192. One workgroup per
+// CU: with GPW = 4 two fit (four waves per SIMD), but measured on
+// 24576 x 4096 and 12288 x 4096 at 16 tokens that was 12-18% slower than
+// one (the rings are then shallower, 64 KiB per workgroup); the smaller
+// register set alone was 2-7% faster than GPW = 8 at one workgroup.
+constexpr int wgs_per_cu(int gpw) { return (void)gpw, 1; }
+
 // Ring depth: the 6-bit vmcnt counter and 96 KiB of LDS for the 8 rings.
-template <int K>
+template <int K, int GPW>
 constexpr int depth_for()
 {
     constexpr int by_count = 63 / ItemSlot<K>::DMA;
@@ -99,17 +108,21 @@ __device__ __forceinline__ u32x4 load_run(const u32x4 &desc, uint32_t voff)
     return v;
 }
 
-template <int K, bool DEF>
-__global__ __launch_bounds__(64 * kWaves) void batch_kernel(
+template <int K, bool DEF, int GPW>
+__global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int n_tokens, float *__restrict__ Y,
     int zero_point, int scale_type)
 {
     using L = ItemSlot<K>;
-    constexpr int D = depth_for<K>();
+    constexpr int D = depth_for<K, GPW>();
     __shared__ __attribute__((aligned(16))) char ring[kWaves][D][L::BYTES];
     __shared__ f32x4 red[2][kWaves][64];
+    // group sums of the wave's groups: Sx depends on the token only, so a
+    // wave keeps its 16 tokens x GPW groups here rather than in registers
+    // (lane k-slice j reads tokens 4 j .. 4 j + 3 as one 16-byte broadcast)
+    __shared__ f32x4 sx_lds[kWaves][GPW][4];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;
@@ -125,7 +138,7 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
     const int per_wave = ((gpr + kWaves - 1) / kWaves + 1) / 2 * 2;
     const int g_begin = per_wave * wave < gpr ? per_wave * wave : gpr;
     const int g_end = g_begin + per_wave < gpr ? g_begin + per_wave : gpr;
-    const int gw = g_end - g_begin;                     // 0 .. kMaxGroupsPerWave
+    const int gw = g_end - g_begin;                     // 0 .. GPW
 
     const uint32_t row_bytes = (uint32_t)(cols / 4);
     const uint32_t plane_bytes = (uint32_t)plane_words * 4;
@@ -149,6 +162,8 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
     const uint32_t dma_scale = pst < (uint32_t)K ? (prow * sbytes + pst * scale_plane) : kSkip;
     const uint32_t dma_zero = pst < (uint32_t)K ? (prow * 4 + pst * zero_plane) : kSkip;
 
+    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+        Y, (short)0, (int)((uint32_t)n_tokens * (uint32_t)rows * 4u), (int)kRsrcWord3);
     const uint32_t lds_ring = lds_address(&ring[wave][0][0]);
     const char *my_ring = &ring[wave][0][0];
 
@@ -198,14 +213,13 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
     __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int d = 0; d < D; ++d) issue_next();
-    u32x4 a[kMaxGroupsPerWave][4];
-    f32x4 sx[kMaxGroupsPerWave];
+    u32x4 a[GPW][4];
     {
         const u32x4 xs = make_desc(X, (uint32_t)n_tokens * (uint32_t)cols * 2);
         const uint32_t xrow = (n < n_tokens ? 0u : kSkip) + (uint32_t)n * (uint32_t)cols * 2;
-        u32x4 run[kMaxGroupsPerWave][4];
+        u32x4 run[GPW][4];
 #pragma unroll
-        for (int g = 0; g < kMaxGroupsPerWave; ++g) {
+        for (int g = 0; g < GPW; ++g) {
             // groups past this wave's range load nothing (an offset past the
             // buffer) and are never used
             const uint32_t off = (g < gw ? xrow : kSkip) + (uint32_t)(g_begin + g) * 256 + 64 * (uint32_t)j;
@@ -214,16 +228,17 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
         }
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int g = 0; g < kMaxGroupsPerWave; ++g)
+        for (int g = 0; g < GPW; ++g)
             asm volatile("" : "+v"(run[g][0]), "+v"(run[g][1]), "+v"(run[g][2]), "+v"(run[g][3]));
         const u32x4 ones = {one, one, one, one};
 #pragma unroll
-        for (int g = 0; g < kMaxGroupsPerWave; ++g) {
+        for (int g = 0; g < GPW; ++g) {
             act_operands(run[g], a[g]);
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int b = 0; b < 4; ++b) acc = mfma(a[g][b], ones, acc);
-            sx[g] = acc;
+            // C rows 4 j + i = tokens, the same in every column n
+            if (n == 0) sx_lds[wave][g][j] = acc;
         }
     }
 
@@ -232,7 +247,7 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
     for (int ti = 0; ti < my_tiles; ++ti) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int g = 0; g < kMaxGroupsPerWave; ++g) {
+        for (int g = 0; g < GPW; ++g) {
             if (g >= gw) break;
             // this item's loads have landed; the next D - 1 items' may not
             wait_vm<(D - 1) * L::DMA>();
@@ -265,8 +280,9 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
                 for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
                 c = __builtin_fmaf(s, 4.0f + z, c);
             }
+            const f32x4 sxg = sx_lds[wave][g][j];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sx[g][i], acc[i]);
+            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sxg[i], acc[i]);
             // the slot is free: refill it with the item D ahead
             issue_next();
             if (++slot_i == D) slot_i = 0;
@@ -283,12 +299,16 @@ __global__ __launch_bounds__(64 * kWaves) void batch_kernel(
                 const f32x4 q = red[n_red & 1][v][lane];
                 y[0] += q[0]; y[1] += q[1]; y[2] += q[2]; y[3] += q[3];
             }
-            // lane: tokens 4 j + i of output row 16 tile + n
-            const int64_t o = (int64_t)((int)blockIdx.x + ti * (int)gridDim.x) * 16 + n;
-            if (o < rows) {
+            // lane: tokens 4 j + i of output row 16 tile + n; 32-bit byte
+            // offsets into Y (n_tokens rows < 2^26 x 16 x 4 bytes < 2^32)
+            const uint32_t o = (uint32_t)((int)blockIdx.x + ti * (int)gridDim.x) * 16 + (uint32_t)n;
+            if (o < (uint32_t)rows) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    if (4 * j + i < n_tokens) Y[(int64_t)(4 * j + i) * rows + o] = y[i];
+                    if (4 * j + i < n_tokens)
+                        __builtin_amdgcn_raw_buffer_store_b32(
+                            __float_as_uint(y[i]), yr, ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4,
+                            0, 0);
             }
         }
         ++n_red;
@@ -305,19 +325,26 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-template <bool DEF>
+template <bool DEF, int GPW>
 hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int n_tokens,
                     float *Y, int grid, hipStream_t stream)
 {
     const int64_t pw = rows * cols / 16, pg = rows * cols / 128;
     switch (k) {
-    case 1: return launch(batch_kernel<1, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
-    case 2: return launch(batch_kernel<2, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
-    case 3: return launch(batch_kernel<3, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
-    case 4: return launch(batch_kernel<4, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 1: return launch(batch_kernel<1, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 2: return launch(batch_kernel<2, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 3: return launch(batch_kernel<3, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 4: return launch(batch_kernel<4, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
     default: return hipErrorInvalidValue;
     }
+}
+
+// Groups per wave of a row of cols inputs (the general kernel's 8-wave split).
+int64_t groups_per_wave(int64_t cols)
+{
+    const int64_t gpr = cols / 128;
+    return ((gpr + kWaves - 1) / kWaves + 1) / 2 * 2;
 }
 
 }  // namespace
@@ -330,8 +357,7 @@ bool linear_batch_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_token
     // it only gains where each workgroup streams several row tiles: measured
     // ahead of the general kernel from 12288 rows at 4096 columns or fewer (2 to
     // 4 stages), and from 24576 rows for one stage; behind it below.
-    const int64_t gpr = cols / 128;
-    const int64_t per_wave = ((gpr + kWaves - 1) / kWaves + 1) / 2 * 2;
+    const int64_t per_wave = groups_per_wave(cols);
     if (G != 128 || n_tokens < kBatchMinTokens || n_tokens > 16 || per_wave > kMaxGroupsPerWave)
         return false;
     return cols <= 4096 && (k >= 2 ? rows >= 12288 : rows >= 24576);
@@ -344,12 +370,20 @@ hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const 
 {
     const char *sc = static_cast<const char *>(scales);
     const int64_t tiles = (rows + 15) / 16;
-    const int grid = (int)(tiles < cus ? tiles : cus);
+    const bool small = groups_per_wave(cols) <= 4;
+    const int64_t slots = (int64_t)cus * (small ? wgs_per_cu(4) : wgs_per_cu(8));
+    const int grid = (int)(tiles < slots ? tiles : slots);
     const bool def = scale_type == kScaleF32 && zero_point != kZpSymmetric;
-    return def ? launch_d<true>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
-                                (int)n_tokens, Y, grid, stream)
-               : launch_d<false>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
-                                 (int)n_tokens, Y, grid, stream);
+    const int nt = (int)n_tokens;
+    if (small)
+        return def ? launch_d<true, 4>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
+                                       nt, Y, grid, stream)
+                   : launch_d<false, 4>(codes, sc, zeros, rows, cols, k, zero_point, scale_type,
+                                        X, nt, Y, grid, stream);
+    return def ? launch_d<true, 8>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, nt,
+                                   Y, grid, stream)
+               : launch_d<false, 8>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
+                                    nt, Y, grid, stream);
 }
 
 }  // namespace rrq_detail

@@ -19,6 +19,10 @@ def load_library() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(
                 f"{LIB_PATH} is missing: build it with `python -m paper_2608_04048_amd.build`")
+        # torch first: the library then binds to the HIP runtime torch has
+        # loaded (torch ships its own copy; loading the library first would
+        # bring a second runtime into the process, whose launches fail)
+        import torch  # noqa: F401
         lib = ctypes.CDLL(LIB_PATH)
         lib.hbm_probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                          ctypes.c_void_p]
