@@ -24,6 +24,7 @@ from collections import defaultdict
 DEFAULT_MATCH = ["construct_kernel", "reconstruct_kernel", "linear_kernel", "decode_kernel",
                  "batch_kernel", "prefill_kernel",
                  "stream_probe_kernel", "read_probe_kernel", "write_probe_kernel",
+                 "construct_probe_kernel", "reconstruct_probe_kernel",
                  "copyBuffer"]
 
 
