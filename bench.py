@@ -28,6 +28,7 @@ codes + fp32 scales and zeros out) / its mean duration, against 8 TB/s.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -497,10 +498,11 @@ def stream_probe(src_bytes, flush_buf=None, launches=10):
 
 
 def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5):
-    """rrq_construct called once per weight tensor (each tensor its own
-    package, laid out back to back in the package buffers), the way a
-    checkpoint stored tensor by tensor is quantized: mean time of one pass
-    over every tensor, HIP events on the launch stream."""
+    """Each weight tensor into its own package (laid out back to back in the
+    package buffers), the way a checkpoint stored tensor by tensor is
+    quantized: one rrq_construct call per tensor, and every tensor in one
+    rrq_construct_many call; mean time of one pass over every tensor, HIP
+    events on the launch stream."""
     import torch
 
     import paper_2608_04048_amd as rrq
@@ -518,21 +520,36 @@ def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5):
         for Wc, r_, c_, cc, sc, zz in calls:
             rrq.rrq_construct(Wc, r_, c_, G, S, cc, sc, zz, stream)
 
-    one_pass()
-    ms = []
-    for _ in range(passes):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        one_pass()
-        b.record(stream)
-        b.synchronize()
-        ms.append(a.elapsed_time(b))
-    t = sum(ms) / len(ms)
+    def many():
+        rrq.rrq_construct_many(calls, G, S, stream)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        gc.collect()
+        gc.disable()   # a collection pause would let the queue drain mid-pass
+        ms = []
+        for _ in range(passes):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            b.synchronize()
+            ms.append(a.elapsed_time(b))
+        gc.enable()
+        return sum(ms) / len(ms)
+
     cb = construct_bytes(n, G, S)
-    return {"calls": len(calls), "construct_ms": round(t, 4),
-            "gbs_bf16_weights": round(2 * n / (t * 1e-3) / 1e9, 1),
-            "hbm_gbs": round(cb / (t * 1e-3) / 1e9, 1),
-            "hbm_frac": round(cb / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    out = {}
+    for key, fn, ncalls in (("calls", one_pass, len(calls)), ("one_call", many, 1)):
+        t = timed(fn)
+        out[key] = {"api": "rrq_construct" if key == "calls" else "rrq_construct_many",
+                    "calls": ncalls, "construct_ms": round(t, 4),
+                    "gbs_bf16_weights": round(2 * n / (t * 1e-3) / 1e9, 1),
+                    "hbm_gbs": round(cb / (t * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(cb / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    out["tensors"] = len(calls)
+    return out
 
 
 def construct_probe(W, n, G, S, codes, scales, zeros, stream, flush_buf=None, launches=10,
@@ -723,11 +740,14 @@ def main():
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(2 + len(w.recon_k))]
               for _ in range(args.steps)]
     torch.cuda.synchronize()
+    gc.collect()
+    gc.disable()   # no collection pause inside the timed steps
     t0 = time.perf_counter()
     for s in range(args.steps):
         step(events[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gc.enable()
 
     cons_ms = [e[0].elapsed_time(e[1]) for e in events]
     rec_ms = {k: [e[1 + i].elapsed_time(e[2 + i]) for e in events] for i, k in enumerate(w.recon_k)}

@@ -162,6 +162,43 @@ int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int32_t group_s
                   hipStream_t stream);
 
 /*
+ * rrq_tensor - one weight tensor of rrq_construct_many: its bfloat16 input
+ * and the device buffers of its own package, all as for rrq_construct.
+ */
+typedef struct rrq_tensor {
+    const uint16_t *W;  /* device, [rows][cols] bfloat16 bit patterns, 16-byte aligned */
+    uint32_t *codes;    /* device, uint32 [S][rows*cols/16], 16-byte aligned (written) */
+    float *scales;      /* device, float [S][rows*cols/G], 4-byte aligned (written) */
+    float *zeros;       /* device, float [S][rows*cols/G], 4-byte aligned (written) */
+    int64_t rows, cols; /* shape, cols % G == 0 */
+} rrq_tensor;
+
+/*
+ * rrq_construct_many - rrq_construct of several weight tensors, each into its
+ * own package (Algorithm 1 without a base checkpoint, per tensor; the same
+ * arithmetic, so every package is bit-identical to rrq_construct's of that
+ * tensor). For a checkpoint stored tensor by tensor: the tensors' groups
+ * share the GPU in one pass (one launch per 64 tensors) instead of one launch
+ * each, whose start and end would otherwise leave most of the GPU idle on
+ * small tensors.
+ *
+ *   tensors    host array of n_tensors descriptors (read during the call
+ *              only); every descriptor as rrq_construct's arguments. The
+ *              packages must not overlap each other or any W.
+ *   n_tensors  >= 0 (0 enqueues nothing).
+ *   group_size, n_stages  as rrq_construct, for every tensor.
+ *   stream     HIP stream the work is enqueued on.
+ *
+ * Every descriptor is checked before anything is enqueued. Returns RRQ_OK,
+ * RRQ_ERR_NULL (tensors NULL with n_tensors > 0, or a NULL buffer),
+ * RRQ_ERR_ALIGN, RRQ_ERR_SHAPE (a bad shape, or n_tensors < 0), RRQ_ERR_GROUP,
+ * RRQ_ERR_STAGES with nothing enqueued, or RRQ_ERR_HIP if a launch failed
+ * (launches before it stay enqueued).
+ */
+int rrq_construct_many(const rrq_tensor *tensors, int32_t n_tensors, int32_t group_size,
+                       int32_t n_stages, hipStream_t stream);
+
+/*
  * rrq_construct_format - rrq_construct in a stage format (see enum
  * rrq_zero_point, enum rrq_scale_type). scales is float or uint16_t per group
  * and stage (4- or 2-byte aligned); zeros is written unless zero_point is

@@ -2,7 +2,7 @@
 reconstruction on AMD Instinct MI355X.
 
 Thin Python binding of librrq.so (include/rrq.h). The functions named like the
-C ABI (``rrq_construct``, ``rrq_construct_from_base``, ``rrq_reconstruct``,
+C ABI (``rrq_construct``, ``rrq_construct_many``, ``rrq_construct_from_base``, ``rrq_reconstruct``,
 ``rrq_linear``, their ``*_format`` twins, ``rrq_construct_stats``,
 ``rrq_group_pmr``, ``rrq_package_bytes``, ``rrq_status_string``) only marshal
 arguments: tensors become device pointers,
@@ -80,6 +80,8 @@ def load_library() -> ctypes.CDLL:
         lib.rrq_linear.restype = ctypes.c_int
         lib.rrq_construct_stats.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P, P, P, P]
         lib.rrq_construct_stats.restype = ctypes.c_int
+        lib.rrq_construct_many.argtypes = [P, I32, I32, I32, P]
+        lib.rrq_construct_many.restype = ctypes.c_int
         lib.rrq_group_pmr.argtypes = [P, I64, I64, I32, P, P]
         lib.rrq_group_pmr.restype = ctypes.c_int
         lib.rrq_construct_format.argtypes = [P, I64, I64, I32, I32, I32, I32, P, P, P, P]
@@ -176,6 +178,29 @@ def rrq_linear(codes, scales, zeros, rows: int, cols: int, group_size: int, n_st
                                    _stream(stream))
     if st != RRQ_OK:
         raise RRQError(st, "rrq_linear")
+
+
+class RrqTensor(ctypes.Structure):
+    """One descriptor of rrq_construct_many (struct rrq_tensor of rrq.h)."""
+    _fields_ = [("W", ctypes.c_void_p), ("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("zeros", ctypes.c_void_p), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64)]
+
+
+def rrq_construct_many(tensors, group_size: int, n_stages: int, stream=None) -> None:
+    """rrq_construct_many over a list of (W, rows, cols, codes, scales, zeros)
+    tuples (device tensors or addresses): each tensor into its own package,
+    in as few launches as the C ABI takes."""
+    import numpy as np
+    # struct rrq_tensor is four pointers and two int64: six 8-byte words
+    desc = np.array([(_ptr(W) or 0, _ptr(codes) or 0, _ptr(scales) or 0, _ptr(zeros) or 0,
+                      int(rows), int(cols))
+                     for W, rows, cols, codes, scales, zeros in tensors],
+                    dtype=np.uint64).reshape(-1, 6)
+    assert ctypes.sizeof(RrqTensor) == 48
+    st = load_library().rrq_construct_many(desc.ctypes.data if tensors else None, len(tensors),
+                                           group_size, n_stages, _stream(stream))
+    if st != RRQ_OK:
+        raise RRQError(st, "rrq_construct_many")
 
 
 def rrq_construct_format(W, rows: int, cols: int, group_size: int, n_stages: int,

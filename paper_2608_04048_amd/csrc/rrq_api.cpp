@@ -177,6 +177,58 @@ extern "C" int rrq_construct(const uint16_t *W, int64_t rows, int64_t cols, int3
                             codes, scales, zeros, false, stream);
 }
 
+extern "C" int rrq_construct_many(const rrq_tensor *tensors, int32_t n_tensors,
+                                  int32_t group_size, int32_t n_stages, hipStream_t stream)
+{
+    if (n_tensors < 0) return RRQ_ERR_SHAPE;
+    if (n_tensors == 0) return RRQ_OK;
+    if (!tensors) return RRQ_ERR_NULL;
+    int64_t total_groups = 0;
+    for (int32_t i = 0; i < n_tensors; ++i) {
+        const rrq_tensor &t = tensors[i];
+        if (!t.W || !t.codes || !t.scales || !t.zeros) return RRQ_ERR_NULL;
+        int64_t n = 0;
+        const int st = check_common(t.rows, t.cols, group_size, n_stages, &n);
+        if (st != RRQ_OK) return st;
+        if (!aligned(t.W, 16) || !aligned(t.codes, 16) || !aligned(t.scales, 4) ||
+            !aligned(t.zeros, 4))
+            return RRQ_ERR_ALIGN;
+        if (__builtin_add_overflow(total_groups, n / group_size, &total_groups))
+            return RRQ_ERR_SHAPE;
+    }
+    const int cus = current_cu_count();
+    if (cus <= 0) return RRQ_ERR_HIP;
+    constexpr int kPer = rrq_detail::kConstructManyPerLaunch;
+    for (int32_t c0 = 0; c0 < n_tensors; c0 += kPer) {
+        const int32_t cn = n_tensors - c0 < kPer ? n_tensors - c0 : kPer;
+        int64_t groups = 0;
+        for (int32_t i = 0; i < cn; ++i)
+            groups += tensors[c0 + i].rows * tensors[c0 + i].cols / group_size;
+        // lanes per group and grid as for one flat call of this size
+        const int lanes = rrq_detail::construct_lanes(groups, group_size, false, cus);
+        rrq_detail::ConstructMany a = {};
+        a.n = cn;
+        int64_t tiles_all = 0;
+        for (int32_t i = 0; i < cn; ++i) {
+            const rrq_tensor &t = tensors[c0 + i];
+            a.tile_first[i] = tiles_all;
+            a.W[i] = t.W;
+            a.codes[i] = t.codes;
+            a.scales[i] = t.scales;
+            a.zeros[i] = t.zeros;
+            a.n_groups[i] = t.rows * t.cols / group_size;
+            tiles_all += (a.n_groups[i] * lanes + 63) / 64;
+        }
+        a.tile_first[cn] = tiles_all;
+        const int64_t cap = (int64_t)cus * rrq_detail::construct_blocks_per_cu(group_size, lanes);
+        const int64_t wg = tiles_all < cap ? tiles_all : cap;
+        const hipError_t e = rrq_detail::launch_construct_many(a, group_size, n_stages, lanes,
+                                                               (int)wg, stream);
+        if (e != hipSuccess) return RRQ_ERR_HIP;
+    }
+    return RRQ_OK;
+}
+
 extern "C" int rrq_construct_format(const uint16_t *W, int64_t rows, int64_t cols,
                                     int32_t group_size, int32_t n_stages, int32_t zero_point,
                                     int32_t scale_type, uint32_t *codes, void *scales,

@@ -583,11 +583,51 @@ __device__ __forceinline__ void load_base(const uint32_t *codes, const char *sca
 // only pmr.
 constexpr int construct_waves_per_simd(int E) { return E >= 128 ? 2 : E >= 64 ? 3 : 4; }
 
-template <int G, bool FROM_BASE, int ZP, int SC, bool STATS_ONLY = false, int L = 1>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
-    construct_waves_per_simd(G / L), construct_waves_per_simd(G / L)))) void construct_kernel(
-    const uint4 *__restrict__ W, int64_t n_groups, int n_stages, uint32_t *__restrict__ codes,
-    char *__restrict__ scales, float *__restrict__ zeros, float *__restrict__ pmr)
+// The tensors a construct launch covers. Tiles are numbered over the whole
+// launch; a workgroup takes tiles first, first + stride, ... (the grid-stride
+// loop), and each tile lies in one tensor: `locate` advances a tensor index
+// (wave-uniform, only ever forward) to the tensor of tile t, `local` gives the
+// tile's number within it.
+struct OneTensor {
+    const uint4 *W;
+    uint32_t *codes;
+    char *scales;
+    float *zeros;
+    int64_t groups;
+    __device__ int64_t total_tiles(int L) const { return (groups * L + 63) / 64; }
+    __device__ void locate(int64_t, int &) const {}
+    __device__ int64_t local(int64_t t, int) const { return t; }
+    __device__ const uint4 *w(int) const { return W; }
+    __device__ uint32_t *c(int) const { return codes; }
+    __device__ char *sc(int) const { return scales; }
+    __device__ float *z(int) const { return zeros; }
+    __device__ int64_t n_groups(int) const { return groups; }
+};
+
+// Several tensors, each its own package, their tiles back to back
+// (ConstructMany of rrq_launch.h, in the kernel arguments): the resident
+// waves walk the tiles in order, as over one flat stack, so that at any time
+// they read and write one or two tensors' neighbouring tiles.
+struct ManyTensors {
+    const ConstructMany &a;
+    __device__ int64_t total_tiles(int) const { return a.tile_first[a.n]; }
+    __device__ void locate(int64_t t, int &i) const
+    {
+        while (i + 1 < a.n && t >= a.tile_first[i + 1]) ++i;
+        i = __builtin_amdgcn_readfirstlane(i);
+    }
+    __device__ int64_t local(int64_t t, int i) const { return t - a.tile_first[i]; }
+    __device__ const uint4 *w(int i) const { return static_cast<const uint4 *>(a.W[i]); }
+    __device__ uint32_t *c(int i) const { return static_cast<uint32_t *>(a.codes[i]); }
+    __device__ char *sc(int i) const { return static_cast<char *>(a.scales[i]); }
+    __device__ float *z(int i) const { return static_cast<float *>(a.zeros[i]); }
+    __device__ int64_t n_groups(int i) const { return a.n_groups[i]; }
+};
+
+template <int G, bool FROM_BASE, int ZP, int SC, bool STATS_ONLY, int L, class SRC>
+__device__ __forceinline__ void construct_tiles(const SRC &src, int n_stages,
+                                                float *__restrict__ pmr, int64_t first,
+                                                int64_t stride)
 {
     static_assert(L == 1 || !STATS_ONLY, "the peak-to-mean ratio needs one lane per group");
     if (FROM_BASE && n_stages < 2) return;
@@ -606,8 +646,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
     __shared__ f32x2 table_lds[16 * 64];
 
     const int lane = threadIdx.x;
-    const int64_t n_shares = n_groups * L;
-    const int64_t n_tiles = (n_shares + 63) / 64;
+    const int64_t n_tiles = src.total_tiles(L);
     // A lane's loaded chunks all have the same index within their share
     // (lane % CH), so each lane writes in exactly one of the two passes.
     const int my_half = (lane % CH) / HC;
@@ -616,20 +655,23 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
     const DequantTable tab = {reinterpret_cast<float *>(table_lds),
                               __uint_as_float((uint32_t)lane * 4)};
 
-    int64_t tile = blockIdx.x;
+    int64_t tile = first;
+    int ti = 0;                  // tensor of the current tile
+    src.locate(tile, ti);
     uint4 v[CH];
     uint32_t bw[WPG];            // base stage of the tile in v (with a base)
     float bs = 0.f, bz = 0.f;
     if (tile < n_tiles) {
-        load_tile<CH>(W, n_shares, tile, lane, v);
+        load_tile<CH>(src.w(ti), src.n_groups(ti) * L, src.local(tile, ti), lane, v);
         if constexpr (FROM_BASE)
-            load_base<E, L, ZP, SC>(codes, scales, zeros, n_groups, tile, lane, bw, bs, bz);
+            load_base<E, L, ZP, SC>(src.c(ti), src.sc(ti), src.z(ti), src.n_groups(ti),
+                                    src.local(tile, ti), lane, bw, bs, bz);
     }
     // The stores of one tile, dropped (see store_stage): the loop is entered
     // with the same operations outstanding as after each tile.
     {
         // (distinct planes, so that no store looks overwritten by the next)
-        const TileOut none = {codes, scales, zeros, 1, 1, 0u, 0u};
+        const TileOut none = {src.c(ti), src.sc(ti), src.z(ti), 1, 1, 0u, 0u};
         const uint32_t zw[WPG] = {};
         if constexpr (L == 1) store_pmr<G>(pmr, 0, 0u, lane, 0.f, 0.f, 0.f);
         if constexpr (!STATS_ONLY) {
@@ -639,10 +681,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
         }
     }
 
-    for (; tile < n_tiles; tile += gridDim.x) {
-        const int64_t first = tile * 64;               // first share of the tile
-        const uint32_t shares_here = (uint32_t)(n_shares - first < 64 ? n_shares - first : 64);
-        const int64_t g0 = first / L;                  // first group of the tile
+    for (; tile < n_tiles; tile += stride) {
+        const int64_t n_groups = src.n_groups(ti);
+        const int64_t n_shares = n_groups * L;
+        const int64_t s0 = src.local(tile, ti) * 64;   // first share of the tile
+        const uint32_t shares_here = (uint32_t)(n_shares - s0 < 64 ? n_shares - s0 : 64);
+        const int64_t g0 = s0 / L;                     // first group of the tile
         const uint32_t groups_here = shares_here / L;
 
         float r[E];
@@ -672,10 +716,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
         if (stats) abs_sum = group_abs_sum<E>(r);
 
         // Prefetch the next tile while this one is quantized.
-        load_tile<CH>(W, n_shares, tile + gridDim.x, lane, v);
+        int tn = ti;             // tensor of the next tile
+        src.locate(tile + stride, tn);
+        load_tile<CH>(src.w(tn), src.n_groups(tn) * L, src.local(tile + stride, tn), lane, v);
 
         constexpr int64_t scale_bytes = SC == kScaleF32 ? 4 : 2;
-        const TileOut out = {codes + first * WPG, scales + g0 * scale_bytes, zeros + g0,
+        const TileOut out = {src.c(ti) + s0 * WPG, src.sc(ti) + g0 * scale_bytes, src.z(ti) + g0,
                              n_shares * WPG, n_groups, shares_here, groups_here};
 
         float lo, hi, inv = 0.f, sq = 0.f, z = 0.f, m = 0.f;
@@ -710,13 +756,37 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
         // The next tile's base stage, loaded where the last stage leaves
         // registers free; only this stage's stores are issued after it.
         if constexpr (FROM_BASE)
-            load_base<E, L, ZP, SC>(codes, scales, zeros, n_groups, tile + gridDim.x, lane, bw,
-                                    bs, bz);
+            load_base<E, L, ZP, SC>(src.c(tn), src.sc(tn), src.z(tn), src.n_groups(tn),
+                                    src.local(tile + stride, tn), lane, bw, bs, bz);
         serial_priority(true);
         stage_params<ZP, SC>(lo, hi, inv, sq, z, m);
         stage_elements<E, false, ZP>(r, inv, m, z, tab, words, lo, hi);
         store_stage<E, L, ZP, SC>(out, n_stages - 1, lane, words, sq, z);
+        ti = tn;
     }
+}
+
+template <int G, bool FROM_BASE, int ZP, int SC, bool STATS_ONLY = false, int L = 1>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
+    construct_waves_per_simd(G / L), construct_waves_per_simd(G / L)))) void construct_kernel(
+    const uint4 *__restrict__ W, int64_t n_groups, int n_stages, uint32_t *__restrict__ codes,
+    char *__restrict__ scales, float *__restrict__ zeros, float *__restrict__ pmr)
+{
+    const OneTensor src = {W, codes, scales, zeros, n_groups};
+    construct_tiles<G, FROM_BASE, ZP, SC, STATS_ONLY, L>(src, n_stages, pmr, blockIdx.x,
+                                                         gridDim.x);
+}
+
+// Several tensors in one launch, each into its own package (integer
+// zero-points, binary32 scales).
+template <int G, int L>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(
+    construct_waves_per_simd(G / L), construct_waves_per_simd(G / L)))) void construct_many_kernel(
+    const ConstructMany a, int n_stages)
+{
+    const ManyTensors src = {a};
+    construct_tiles<G, false, kZpInteger, kScaleF32, false, L>(src, n_stages, nullptr,
+                                                               blockIdx.x, gridDim.x);
 }
 
 // Reconstruction. Lane work unit: a chunk of E consecutive elements whose
@@ -894,6 +964,18 @@ hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
                                                 zero_point, scale_type, lanes, grid, stream)
                      : launch_construct_b<false>(w4, n_groups, G, S, codes, sc, zeros, pmr,
                                                  zero_point, scale_type, lanes, grid, stream);
+}
+
+hipError_t launch_construct_many(const ConstructMany &a, int G, int S, int lanes, int grid,
+                                 hipStream_t stream)
+{
+#define RRQ_MANY_CASE(GS, LS)                                                                      \
+    if (G == GS && lanes == LS)                                                                    \
+        return launch(construct_many_kernel<GS, LS>, grid, 64, stream, a, S);
+    RRQ_MANY_CASE(32, 1) RRQ_MANY_CASE(64, 1) RRQ_MANY_CASE(128, 1)
+    RRQ_MANY_CASE(64, 2) RRQ_MANY_CASE(128, 4)
+#undef RRQ_MANY_CASE
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_group_pmr(const uint16_t *W, int64_t n_groups, int G, float *pmr, int grid,

@@ -22,6 +22,25 @@ hipError_t launch_construct(const uint16_t *W, int64_t n_groups, int G, int S,
                             bool from_base, int zero_point, int scale_type, int lanes, int grid,
                             hipStream_t stream);
 
+// Several tensors (each its own package, integer zero-points, binary32
+// scales) in one launch: tensor i has n_groups[i] groups at W[i] and its
+// package at codes[i], scales[i], zeros[i]; its tiles (of 64 lane shares at
+// the launch's lanes per group) are the launch's tiles tile_first[i] ..
+// tile_first[i + 1] - 1. At most kConstructManyPerLaunch tensors per launch
+// (the table travels in the kernel arguments, 3 KiB).
+constexpr int kConstructManyPerLaunch = 64;
+struct ConstructMany {
+    int64_t tile_first[kConstructManyPerLaunch + 1];
+    const void *W[kConstructManyPerLaunch];
+    void *codes[kConstructManyPerLaunch];
+    void *scales[kConstructManyPerLaunch];
+    void *zeros[kConstructManyPerLaunch];
+    int64_t n_groups[kConstructManyPerLaunch];
+    int32_t n;
+};
+hipError_t launch_construct_many(const ConstructMany &a, int G, int S, int lanes, int grid,
+                                 hipStream_t stream);
+
 // Per-group peak-to-mean ratios of W only.
 hipError_t launch_group_pmr(const uint16_t *W, int64_t n_groups, int G, float *pmr, int grid,
                             hipStream_t stream);

@@ -32,7 +32,8 @@ def test_library_exports_every_declared_function():
     lib = rrq.load_library()
     names = _declared_functions()
     assert names == ["rrq_construct", "rrq_construct_format", "rrq_construct_from_base",
-                     "rrq_construct_from_base_format", "rrq_construct_stats", "rrq_group_pmr",
+                     "rrq_construct_from_base_format", "rrq_construct_many",
+                     "rrq_construct_stats", "rrq_group_pmr",
                      "rrq_linear", "rrq_linear_format", "rrq_package_bytes", "rrq_reconstruct",
                      "rrq_reconstruct_format", "rrq_status_string"]
     for name in names:
@@ -128,6 +129,47 @@ def _from_base_status(W=FAKE, rows=64, cols=128, G=128, S=4, codes=FAKE, scales=
 ])
 def test_construct_from_base_rejects(kw, status):
     assert _from_base_status(**kw) == status
+
+
+def _many_status(tensors, n=None, G=128, S=4):
+    arr = (rrq.RrqTensor * max(1, len(tensors)))()
+    for i, t in enumerate(tensors):
+        arr[i] = rrq.RrqTensor(*t)
+    n = len(tensors) if n is None else n
+    p = ctypes.cast(arr, ctypes.c_void_p) if tensors else None
+    return rrq.load_library().rrq_construct_many(p, n, G, S, None)
+
+
+GOOD = (FAKE, FAKE, FAKE, FAKE, 64, 128)
+
+
+@pytest.mark.parametrize("bad,status", [
+    ((0, FAKE, FAKE, FAKE, 64, 128), rrq.RRQ_ERR_NULL),
+    ((FAKE, 0, FAKE, FAKE, 64, 128), rrq.RRQ_ERR_NULL),
+    ((FAKE, FAKE, 0, FAKE, 64, 128), rrq.RRQ_ERR_NULL),
+    ((FAKE, FAKE, FAKE, 0, 64, 128), rrq.RRQ_ERR_NULL),
+    ((FAKE + 8, FAKE, FAKE, FAKE, 64, 128), rrq.RRQ_ERR_ALIGN),
+    ((FAKE, FAKE + 4, FAKE, FAKE, 64, 128), rrq.RRQ_ERR_ALIGN),
+    ((FAKE, FAKE, FAKE + 2, FAKE, 64, 128), rrq.RRQ_ERR_ALIGN),
+    ((FAKE, FAKE, FAKE, FAKE + 1, 64, 128), rrq.RRQ_ERR_ALIGN),
+    ((FAKE, FAKE, FAKE, FAKE, 0, 128), rrq.RRQ_ERR_SHAPE),
+    ((FAKE, FAKE, FAKE, FAKE, 64, 100), rrq.RRQ_ERR_SHAPE),
+])
+def test_construct_many_rejects_any_bad_descriptor(bad, status):
+    """Every descriptor is checked before anything is enqueued: a bad one
+    anywhere in the list (here the last of 70, past the first launch's 64)
+    fails the whole call (no GPU is touched by these checks)."""
+    assert _many_status([GOOD] * 69 + [bad]) == status
+    assert _many_status([bad]) == status
+
+
+def test_construct_many_arguments():
+    assert _many_status([], n=0) == rrq.RRQ_OK            # nothing to do, nothing enqueued
+    assert rrq.load_library().rrq_construct_many(None, 3, 128, 4, None) == rrq.RRQ_ERR_NULL
+    assert _many_status([GOOD], n=-1) == rrq.RRQ_ERR_SHAPE
+    assert _many_status([GOOD], G=96) == rrq.RRQ_ERR_GROUP
+    assert _many_status([GOOD], S=5) == rrq.RRQ_ERR_STAGES
+    assert _many_status([GOOD], S=0) == rrq.RRQ_ERR_STAGES
 
 
 def test_construct_from_base_single_stage_is_a_no_op():
