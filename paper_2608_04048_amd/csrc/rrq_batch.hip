@@ -14,14 +14,21 @@
 // Work: the 8 waves of a workgroup split the groups of a row into contiguous
 // ranges of at most 8 (the general kernel's split for 8 waves), so a wave's A
 // operands and group sums (16 tokens x its groups) are loaded and formed once
-// and stay in registers. A workgroup takes 16-row tiles in turn; an item is
-// one group of a 16-row tile, all K stages: its codes, scales and
-// zero-points go from HBM into a ring of D LDS slots per wave by LDS-DMA
-// loads, a fixed count per item, and the wave waits for exactly the item it
-// reads. At the end of a tile the 8 waves' partial sums meet in LDS and are
-// summed in wave order: per output, the wave's groups in order (k FMAs and
-// the Sx term each) and then the 8 partials, the accumulation structure of
-// the general kernel's 8-wave tiles, so its error bound holds unchanged.
+// and stay in registers. A workgroup takes 16-row tiles in turn and streams
+// each tile stage by stage: a unit (one stage of the tile's 16 rows, every
+// group) goes from HBM into a ring of LDS slots shared by the 8 waves by
+// LDS-DMA loads, each wave issuing a fixed share of whole-row code runs and
+// 64-element runs of scales and zero-points (a 16-row slice of one group
+// would be 16 runs of 32 bytes, and its parameters 64 single words, which
+// the memory system serves far below its streaming rate). A wave waits for
+// its own share of the unit, one barrier per unit then makes every share
+// visible, and the wave works on its groups of the unit: per group, an
+// accumulator of the stages' 4 s P and a sum of the stages' s (4 + z). At
+// the end of a tile, per output, the wave adds its groups in order (each
+// its stage sum less c Sx) and the 8 waves' partial sums meet in LDS and are
+// summed in wave order. Each product term passes through at most k + 3 +
+// GPW roundings, fewer than in the general kernel's order, so the error
+// bound of include/rrq.h holds.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -39,7 +46,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kWaves = 8;                      // waves per workgroup
-constexpr int kMaxGroupsPerWave = 8;           // A operands held in registers
+constexpr int kGroupsPerWave = 4;             // A operands held in registers (cols <= 4096)
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
 constexpr uint32_t kCodeMask = 0x00600060u;    // top two mantissa bits of both halves
 constexpr int kZpSymmetric = 2;
@@ -51,35 +58,39 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-// One item's LDS slot (one group of a 16-row tile, all K stages): codes of
-// stage t at 1024 (t / 2) + 512 (t % 2), row-major 16 x 32 bytes; scales and
-// zero-points as 32-bit words, stage t of row r at 4 (16 t + r).
-template <int K>
-struct ItemSlot {
-    static constexpr int CODE_DMA = (K + 1) / 2;   // 1 KiB loads, two stages each
-    static constexpr int SCALES = CODE_DMA * 1024;
-    static constexpr int ZEROS = SCALES + 256;
-    static constexpr int BYTES = ZEROS + 256;
-    static constexpr int DMA = CODE_DMA + 2;       // vector-memory loads per item
+// A unit: one stage of a 16-row tile, every group of the rows, as the
+// workgroup's 8 waves share it in LDS: the 16 rows' codes (row r at r RB
+// bytes, RB = cols / 4, its 16-byte pieces XOR-swizzled within aligned runs
+// of 16 so that an MFMA's 16 rows read distinct banks), then the scales and
+// the zero-points of the 16 rows (one 32-bit word per element, group-major:
+// row r group g at 16 g + r, so that an MFMA's 16 rows read consecutive
+// words; a 16-bit scale in the low half). The waves fetch a unit together,
+// each a fixed share of 1 KiB code loads (whole rows) and 64-element
+// parameter loads (4 groups of the 16 rows); loads past the unit's end read
+// nothing, so every wave issues the same loads per unit.
+template <int GPW>
+struct Unit {
+    static constexpr int CODE = 16 * GPW * kWaves * 32;      // 16 rows of at most GPW x 8 groups
+    static constexpr int PAR = 16 * GPW * kWaves * 4;        // 16 rows x groups, one word each
+    static constexpr int BYTES = CODE + 2 * PAR;
+    static constexpr int CI = CODE / 1024 / kWaves;          // code loads per wave
+    static constexpr int PI = PAR / 256 / kWaves;            // loads per wave per parameter buffer
+    static constexpr int DMA = CI + 2 * PI;                  // loads per wave per unit
 };
 
 // Groups per wave GPW: the A operands of a wave's groups stay in its
-// registers (16 tokens x GPW groups, 16 GPW VGPRs). GPW = 4 serves rows of up
-// to 4096 inputs in at most 128 VGPRs, GPW = 8 up to 8192. One workgroup per
-// CU: with GPW = 4 two fit (four waves per SIMD), but measured on
-// 24576 x 4096 and 12288 x 4096 at 16 tokens that was 12-18% slower than
-// one (the rings are then shallower, 64 KiB per workgroup); the smaller
-// register set alone was 2-7% faster than GPW = 8 at one workgroup.
-constexpr int wgs_per_cu(int gpw) { return (void)gpw, 1; }
+// registers (16 tokens x GPW groups, 16 GPW VGPRs); GPW = 4 serves rows of up
+// to 4096 inputs. One workgroup per CU.
+constexpr int kRedBytes = 2 * kWaves * 64 * 16;
 
-// Ring depth: the 6-bit vmcnt counter and 96 KiB of LDS for the 8 rings.
-template <int K, int GPW>
-constexpr int depth_for()
+// Units resident: as many as the CU's 160 KiB of LDS holds beside the
+// reduction buffers and the group sums. The waves keep all but one in
+// flight: a unit's slot is refilled only once every wave has passed the next
+// unit's barrier, i.e. is done with it.
+template <int GPW>
+constexpr int unit_slots()
 {
-    constexpr int by_count = 63 / ItemSlot<K>::DMA;
-    constexpr int by_lds = 96 * 1024 / (kWaves * ItemSlot<K>::BYTES);
-    constexpr int d = by_count < by_lds ? by_count : by_lds;
-    return d < 16 ? d : 16;
+    return (160 * 1024 - kRedBytes - kWaves * GPW * 64) / Unit<GPW>::BYTES;
 }
 
 // A operands of one group for the lane (token n, k-slice j) from its inputs
@@ -109,15 +120,22 @@ __device__ __forceinline__ u32x4 load_run(const u32x4 &desc, uint32_t voff)
 }
 
 template <int K, bool DEF, int GPW>
-__global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel(
+__global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int n_tokens, float *__restrict__ Y,
     int zero_point, int scale_type)
 {
-    using L = ItemSlot<K>;
-    constexpr int D = depth_for<K, GPW>();
-    __shared__ __attribute__((aligned(16))) char ring[kWaves][D][L::BYTES];
+    using U = Unit<GPW>;
+    constexpr int NS = unit_slots<GPW>();
+    // Units per barrier: two where a tile has an even number of stages (half
+    // the barriers, twice the independent chains between them), else one.
+    constexpr int UPB = K % 2 == 0 ? 2 : 1;
+    // Units in flight: the refills after a barrier overwrite the slots of
+    // the UPB units before it, which every wave is done with by then.
+    constexpr int D = NS - UPB;
+    static_assert(D >= 2 * UPB && D * U::DMA + 4 * GPW <= 63, "unit ring");
+    __shared__ __attribute__((aligned(16))) char ring[NS][U::BYTES];
     __shared__ f32x4 red[2][kWaves][64];
     // group sums of the wave's groups: Sx depends on the token only, so a
     // wave keeps its 16 tokens x GPW groups here rather than in registers
@@ -129,6 +147,7 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel
     const int j = lane >> 4;
     const bool sym = zero_point == kZpSymmetric;
     const int gpr = (int)(cols / 128);                  // groups per row
+    const int cpr = (int)(cols / 64);                   // 16-byte code pieces per row
     uint32_t mask, one;
     asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
     asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
@@ -143,73 +162,91 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel
     const uint32_t row_bytes = (uint32_t)(cols / 4);
     const uint32_t plane_bytes = (uint32_t)plane_words * 4;
     const uint32_t sbytes = scale_type == kScaleF32 ? 4 : 2;
-    const uint32_t scale_plane = (uint32_t)plane_groups * sbytes;
-    const uint32_t zero_plane = (uint32_t)plane_groups * 4;
     const u32x4 dc = make_desc(codes, (uint32_t)K * plane_bytes);
-    const u32x4 ds = make_desc(scales, (uint32_t)K * scale_plane);
-    const u32x4 dz = make_desc(sym ? nullptr : zeros, sym ? 0u : (uint32_t)K * zero_plane);
+    const u32x4 ds = make_desc(scales, (uint32_t)K * (uint32_t)plane_groups * sbytes);
+    const u32x4 dz = make_desc(sym ? nullptr : zeros, sym ? 0u : (uint32_t)K * (uint32_t)plane_groups * 4);
+    u32x4 dc0 = dc, ds0 = ds, dz0 = dz;                 // size 0: no access
+    dc0[2] = ds0[2] = dz0[2] = 0u;
 
-    // DMA lane offsets within an item. Codes: lane l fills bytes 16 l of a
-    // 1 KiB load: stage 2 i + l / 32, row (l % 32) / 2, bytes 16 (l % 2) .. + 15
-    // of the row's 32 bytes of the group (a stage past K - 1 reads past the
-    // descriptor, or other data that is never read).
-    const uint32_t dma_code = (uint32_t)((lane & 31) >> 1) * row_bytes + 16 * (uint32_t)(lane & 1) +
-                              (uint32_t)(lane >> 5) * plane_bytes;
-    // Scales and zero-points: lane l -> stage l / 16, row l % 16; stages past
-    // K - 1 read nothing.
-    const uint32_t pst = (uint32_t)lane >> 4;
-    const uint32_t prow = (uint32_t)(lane & 15) * (uint32_t)gpr;
-    const uint32_t dma_scale = pst < (uint32_t)K ? (prow * sbytes + pst * scale_plane) : kSkip;
-    const uint32_t dma_zero = pst < (uint32_t)K ? (prow * 4 + pst * zero_plane) : kSkip;
+    // Code pieces within a row are swizzled by XOR with the row's low bits,
+    // over the largest run of 16 or fewer pieces that divides the row.
+    const int swz = (cpr & -cpr) < 16 ? (cpr & -cpr) - 1 : 15;
+    // This lane's loads of a unit (offsets from the unit's first row of the
+    // plane): code piece q = 64 (wave CI + i) + lane is row q / cpr, LDS piece
+    // q % cpr holding the row's piece (q % cpr) ^ (row & swz); parameter word
+    // e = 64 (wave PI + i) + lane holds row e % 16, group e / 16.
+    uint32_t v_code[U::CI], v_scale[U::PI], v_zero[U::PI];
+#pragma unroll
+    for (int i = 0; i < U::CI; ++i) {
+        const int q = 64 * (wave * U::CI + i) + lane;
+        const int r = q / cpr, c = q - r * cpr;
+        v_code[i] = q < 16 * cpr ? (uint32_t)r * row_bytes + (uint32_t)(c ^ (r & swz)) * 16 : kSkip;
+    }
+#pragma unroll
+    for (int i = 0; i < U::PI; ++i) {
+        const int e = 64 * (wave * U::PI + i) + lane;
+        const uint32_t el = (uint32_t)((e & 15) * gpr + (e >> 4));
+        v_scale[i] = e < 16 * gpr ? el * sbytes : kSkip;
+        v_zero[i] = e < 16 * gpr ? el * 4 : kSkip;
+    }
+    // This lane's reads (B column: row n, k-slice j): the 8 code bytes of
+    // group g_begin + g at code_rd[g] within a unit, its parameters at
+    // par_rd + 64 g.
+    uint32_t code_rd[GPW];
+#pragma unroll
+    for (int g = 0; g < GPW; ++g) {
+        const int c = 2 * (g_begin + g) + (j >> 1);
+        code_rd[g] = (uint32_t)n * row_bytes + (uint32_t)(c ^ (n & swz)) * 16 + (uint32_t)(j & 1) * 8;
+    }
+    const uint32_t par_rd = U::CODE + 4 * (uint32_t)(16 * g_begin + n);
 
     const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
         Y, (short)0, (int)((uint32_t)n_tokens * (uint32_t)rows * 4u), (int)kRsrcWord3);
-    const uint32_t lds_ring = lds_address(&ring[wave][0][0]);
-    const char *my_ring = &ring[wave][0][0];
+    const uint32_t lds_ring = lds_address(&ring[0][0]);
 
-    // Row tiles of this workgroup: blockIdx, blockIdx + grid, ...
+    // Row tiles of this workgroup: blockIdx, blockIdx + grid, ...; units in
+    // order: tile t, stage st = unit t K + st.
     const int tiles = (int)((rows + 15) / 16);
     const int my_tiles = (int)blockIdx.x < tiles ? (tiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
-    const int total = my_tiles * gw;                    // items of this wave
+    const int n_units = my_tiles * K;
 
-    // DMA of the items in order (tile-major, then this wave's groups), one
-    // call per item, position kept in running counters; items past the end
-    // and rows past the last read through descriptors of size 0 or past
-    // their end (zeros).
-    int is_g = 0, is_slot = 0, issued = 0;
+    // DMA of this wave's share of the units in order, one call per unit,
+    // position in running counters; units past the end read through
+    // descriptors of size 0 (zeros).
+    int is_u = 0, is_st = 0, is_slot = 0;
     int is_tile = (int)blockIdx.x;
     auto issue_next = [&]() {
-        const bool live = issued < total;
+        const bool live = is_u < n_units;
         const uint32_t row0 = live ? (uint32_t)is_tile * 16 : 0u;
-        const uint32_t g = (uint32_t)(g_begin + is_g);
-        const uint32_t code_base = row0 * row_bytes + g * 32;
-        const uint32_t grp = row0 * (uint32_t)gpr + g;
-        const uint32_t lds = lds_ring + (uint32_t)is_slot * L::BYTES;
-        u32x4 c_src = dc, s_src = ds, z_src = dz;
-        if (!live) c_src[2] = s_src[2] = z_src[2] = 0u;
-        // the reads of the item that used this slot have completed
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const uint32_t lds = lds_ring + (uint32_t)is_slot * U::BYTES;
+        const uint32_t code_off = (uint32_t)is_st * plane_bytes + row0 * row_bytes;
+        const uint32_t par_el = (uint32_t)is_st * (uint32_t)plane_groups + row0 * (uint32_t)gpr;
+        const u32x4 c_src = live ? dc : dc0, s_src = live ? ds : ds0, z_src = live ? dz : dz0;
 #pragma unroll
-        for (int i = 0; i < L::CODE_DMA; ++i)
-            dma_x4(c_src, code_base + 2u * i * plane_bytes, lds + 1024u * i, dma_code);
-        if (DEF || scale_type == kScaleF32)
-            dma_dword(s_src, grp * 4, lds + L::SCALES, dma_scale);
-        else
-            dma_ushort(s_src, grp * 2, lds + L::SCALES, dma_scale);
-        dma_dword(z_src, grp * 4, lds + L::ZEROS, dma_zero);
-        ++issued;
-        if (++is_slot == D) is_slot = 0;
-        if (++is_g == gw) {
-            is_g = 0;
+        for (int i = 0; i < U::CI; ++i)
+            dma_x4(c_src, code_off, lds + 1024u * (uint32_t)(wave * U::CI + i), v_code[i]);
+#pragma unroll
+        for (int i = 0; i < U::PI; ++i) {
+            const uint32_t at = 256u * (uint32_t)(wave * U::PI + i);
+            if (DEF || scale_type == kScaleF32)
+                dma_dword(s_src, par_el * 4, lds + U::CODE + at, v_scale[i]);
+            else
+                dma_ushort(s_src, par_el * 2, lds + U::CODE + at, v_scale[i]);
+            dma_dword(z_src, par_el * 4, lds + U::CODE + U::PAR + at, v_zero[i]);
+        }
+        ++is_u;
+        if (++is_slot == NS) is_slot = 0;
+        if (++is_st == K) {
+            is_st = 0;
             is_tile += (int)gridDim.x;
         }
     };
 
-    // The ring's first items, then the activations of this wave's groups
+    // The ring's first units, then the activations of this wave's groups
     // (lane as A row: token n, tokens past n_tokens reading zeros), waited
     // for explicitly with the runs tied to the wait. The prologue runs at a
-    // raised wave priority (measured 1-5% faster at 2 to 4 stages, same
-    // outputs): it is a serial stretch that every later item waits for.
+    // raised wave priority: it is a serial stretch that every later unit
+    // waits for.
     __builtin_amdgcn_s_setprio(2);
 #pragma unroll
     for (int d = 0; d < D; ++d) issue_next();
@@ -241,29 +278,41 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel
             if (n == 0) sx_lds[wave][g][j] = acc;
         }
     }
-
     __builtin_amdgcn_s_setprio(0);
-    int slot_i = 0, n_red = 0;
-    for (int ti = 0; ti < my_tiles; ++ti) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+
+    // Per tile and group of the wave: acc[g] = sum over stages of 4 s P and
+    // c[g] = sum over stages of s (4 + z), stage by stage as the units come.
+    int slot_i = 0, n_red = 0, st = 0, ti = 0;
+    f32x4 acc[GPW];
+    float cz[GPW];
 #pragma unroll
-        for (int g = 0; g < GPW; ++g) {
-            if (g >= gw) break;
-            // this item's loads have landed; the next D - 1 items' may not
-            wait_vm<(D - 1) * L::DMA>();
-            const char *slot = my_ring + slot_i * L::BYTES;
-            float c = 0.0f;
+    for (int g = 0; g < GPW; ++g) {
+        acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+        cz[g] = 0.0f;
+    }
+    for (int u = 0; u < n_units; u += UPB) {
+        // this wave's loads of the next UPB units have landed; then every
+        // wave's have, and every wave is done with the UPB units before
+        // (whose slots the refills below overwrite)
+        wait_vm<(D - UPB) * U::DMA>();
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __syncthreads();
 #pragma unroll
-            for (int st = 0; st < K; ++st) {
-                const u32x2 w = *reinterpret_cast<const u32x2 *>(
-                    slot + 1024 * (st >> 1) + 512 * (st & 1) + n * 32 + j * 8);
+        for (int h = 0; h < UPB; ++h) {
+            const char *unit = &ring[slot_i][0];
+            // every group slot, also past this wave's range (its activations
+            // are zero, the codes there other bytes of the unit): independent
+            // chains to interleave; only groups in range enter the tile's sum
+#pragma unroll
+            for (int g = 0; g < GPW; ++g) {
+                const u32x2 w = *reinterpret_cast<const u32x2 *>(unit + code_rd[g]);
                 u32x4 b[2][2];
                 code_operands_pair(w[0], w[1], mask, one, b);
                 f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int q = 0; q < 4; ++q) p = mfma(a[g][q], b[q >> 1][q & 1], p);
-                const uint32_t sw = *reinterpret_cast<const uint32_t *>(slot + L::SCALES + 4 * (16 * st + n));
-                const uint32_t zw = *reinterpret_cast<const uint32_t *>(slot + L::ZEROS + 4 * (16 * st + n));
+                const uint32_t sw = *reinterpret_cast<const uint32_t *>(unit + par_rd + 64 * g);
+                const uint32_t zw = *reinterpret_cast<const uint32_t *>(unit + U::PAR + par_rd + 64 * g);
                 float s, z;
                 if constexpr (DEF) {
                     s = __uint_as_float(sw);
@@ -277,27 +326,43 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel
                 }
                 const float s4 = 4.0f * s;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
-                c = __builtin_fmaf(s, 4.0f + z, c);
+                for (int i = 0; i < 4; ++i) acc[g][i] = __builtin_fmaf(s4, p[i], acc[g][i]);
+                cz[g] = __builtin_fmaf(s, 4.0f + z, cz[g]);
             }
+            if (++slot_i == NS) slot_i = 0;
+        }
+        // the slots of the units before are free: refill them, UPB units on
+#pragma unroll
+        for (int h = 0; h < UPB; ++h) issue_next();
+        st += UPB;
+        if (st < K) continue;
+        st = 0;
+
+        // end of the tile: per output, the wave's groups in order (each its
+        // stages' sum less c Sx), then the waves' partial sums in wave order.
+        // The buffer written here is next written two tiles later, after a
+        // barrier that the summing wave reaches only once it has read it.
+        f32x4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int g = 0; g < GPW; ++g) {
+            if (g >= gw) break;
             const f32x4 sxg = sx_lds[wave][g][j];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sxg[i], acc[i]);
-            // the slot is free: refill it with the item D ahead
-            issue_next();
-            if (++slot_i == D) slot_i = 0;
+            for (int i = 0; i < 4; ++i) {
+                const float t = __builtin_fmaf(-cz[g], sxg[i], acc[g][i]);
+                y[i] = g == 0 ? t : y[i] + t;
+            }
+            acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+            cz[g] = 0.0f;
         }
-        // end of the tile: the waves' partial sums in wave order. The buffer
-        // written here is next written two tiles later, after a barrier that
-        // the summing wave reaches only once it has read it.
-        red[n_red & 1][wave][lane] = acc;
+        red[n_red & 1][wave][lane] = y;
         __syncthreads();
         if (wave == 0) {
-            f32x4 y = red[n_red & 1][0][lane];
+            f32x4 yo = red[n_red & 1][0][lane];
 #pragma unroll
             for (int v = 1; v < kWaves; ++v) {
                 const f32x4 q = red[n_red & 1][v][lane];
-                y[0] += q[0]; y[1] += q[1]; y[2] += q[2]; y[3] += q[3];
+                yo[0] += q[0]; yo[1] += q[1]; yo[2] += q[2]; yo[3] += q[3];
             }
             // lane: tokens 4 j + i of output row 16 tile + n; 32-bit byte
             // offsets into Y (n_tokens rows < 2^26 x 16 x 4 bytes < 2^32)
@@ -307,11 +372,12 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(GPW)) void batch_kernel
                 for (int i = 0; i < 4; ++i)
                     if (4 * j + i < n_tokens)
                         __builtin_amdgcn_raw_buffer_store_b32(
-                            __float_as_uint(y[i]), yr, ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4,
+                            __float_as_uint(yo[i]), yr, ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4,
                             0, 0);
             }
         }
         ++n_red;
+        ++ti;
     }
     // no DMA load may still write this workgroup's LDS once it ends
     wait_vm<0>();
@@ -351,16 +417,16 @@ int64_t groups_per_wave(int64_t cols)
 
 bool linear_batch_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens)
 {
-    // The A operands of a wave's groups (16 tokens x at most 8 groups) fit its
-    // registers for cols up to 8 x 8 x 128. The form pays a fixed prologue per
+    // The A operands of a wave's groups (16 tokens x at most 4 groups) fit its
+    // registers for cols up to 8 x 4 x 128. The form pays a fixed prologue per
     // workgroup (every wave loads its activations before its first product), so
     // it only gains where each workgroup streams several row tiles: measured
     // ahead of the general kernel from 12288 rows at 4096 columns or fewer (2 to
     // 4 stages), and from 24576 rows for one stage; behind it below.
-    const int64_t per_wave = groups_per_wave(cols);
-    if (G != 128 || n_tokens < kBatchMinTokens || n_tokens > 16 || per_wave > kMaxGroupsPerWave)
+    if (G != 128 || n_tokens < kBatchMinTokens || n_tokens > 16 ||
+        groups_per_wave(cols) > kGroupsPerWave)
         return false;
-    return cols <= 4096 && (k >= 2 ? rows >= 12288 : rows >= 24576);
+    return k >= 2 ? rows >= 12288 : rows >= 24576;
 }
 
 hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const float *zeros,
@@ -368,22 +434,17 @@ hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const 
                                const uint16_t *X, int64_t n_tokens, float *Y, int cus,
                                hipStream_t stream)
 {
+    if (groups_per_wave(cols) > kGroupsPerWave || n_tokens > 16)
+        return hipErrorInvalidValue;
     const char *sc = static_cast<const char *>(scales);
     const int64_t tiles = (rows + 15) / 16;
-    const bool small = groups_per_wave(cols) <= 4;
-    const int64_t slots = (int64_t)cus * (small ? wgs_per_cu(4) : wgs_per_cu(8));
-    const int grid = (int)(tiles < slots ? tiles : slots);
+    const int grid = (int)(tiles < cus ? tiles : (int64_t)cus);
     const bool def = scale_type == kScaleF32 && zero_point != kZpSymmetric;
     const int nt = (int)n_tokens;
-    if (small)
-        return def ? launch_d<true, 4>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
-                                       nt, Y, grid, stream)
-                   : launch_d<false, 4>(codes, sc, zeros, rows, cols, k, zero_point, scale_type,
-                                        X, nt, Y, grid, stream);
-    return def ? launch_d<true, 8>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, nt,
-                                   Y, grid, stream)
-               : launch_d<false, 8>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
-                                    nt, Y, grid, stream);
+    return def ? launch_d<true, kGroupsPerWave>(codes, sc, zeros, rows, cols, k, zero_point,
+                                                scale_type, X, nt, Y, grid, stream)
+               : launch_d<false, kGroupsPerWave>(codes, sc, zeros, rows, cols, k, zero_point,
+                                                 scale_type, X, nt, Y, grid, stream);
 }
 
 }  // namespace rrq_detail

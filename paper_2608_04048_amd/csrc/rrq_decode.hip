@@ -187,7 +187,6 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
     const u32x4 ds = make_desc(scales, (uint32_t)K * (uint32_t)plane_groups * sbytes);
     const u32x4 dz = make_desc(sym ? nullptr : zeros,
                                sym ? 0u : (uint32_t)K * (uint32_t)plane_groups * 4);
-    const u32x4 dnone = make_desc(codes, 0u);
     const uint32_t set0 = (uint32_t)wave * SPW;
 
     // DMA lane offsets within an item. Codes: lane l fills bytes 16 l of a
