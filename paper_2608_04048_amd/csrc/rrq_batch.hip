@@ -128,9 +128,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
 {
     using U = Unit<GPW>;
     constexpr int NS = unit_slots<GPW>();
-    // Units per barrier: two where a tile has an even number of stages (half
-    // the barriers, twice the independent chains between them), else one.
-    constexpr int UPB = K % 2 == 0 ? 2 : 1;
+    // Two units per barrier (half the barriers, twice the independent chains
+    // between them); a loop step covers TPB whole tiles, two where a tile has
+    // an odd number of stages, so that every unit's tile is known at compile
+    // time.
+    constexpr int UPB = 2;
+    constexpr int TPB = K % 2 == 0 ? 1 : 2;
+    constexpr int PAIRS = TPB * K / UPB;
     // Units in flight: the refills after a barrier overwrite the slots of
     // the UPB units before it, which every wave is done with by then.
     constexpr int D = NS - UPB;
@@ -280,104 +284,118 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     }
     __builtin_amdgcn_s_setprio(0);
 
-    // Per tile and group of the wave: acc[g] = sum over stages of 4 s P and
-    // c[g] = sum over stages of s (4 + z), stage by stage as the units come.
-    int slot_i = 0, n_red = 0, st = 0, ti = 0;
-    f32x4 acc[GPW];
-    float cz[GPW];
+    // Per tile of the step and group of the wave: acc[t][g] = sum over
+    // stages of 4 s P and cz[t][g] = sum over stages of s (4 + z), stage by
+    // stage as the units come.
+    int slot_i = 0, n_red = 0;
+    f32x4 acc[TPB][GPW];
+    float cz[TPB][GPW];
 #pragma unroll
-    for (int g = 0; g < GPW; ++g) {
-        acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-        cz[g] = 0.0f;
-    }
-    for (int u = 0; u < n_units; u += UPB) {
-        // this wave's loads of the next UPB units have landed; then every
-        // wave's have, and every wave is done with the UPB units before
-        // (whose slots the refills below overwrite)
-        wait_vm<(D - UPB) * U::DMA>();
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        __syncthreads();
-#pragma unroll
-        for (int h = 0; h < UPB; ++h) {
-            const char *unit = &ring[slot_i][0];
-            // every group slot, also past this wave's range (its activations
-            // are zero, the codes there other bytes of the unit): independent
-            // chains to interleave; only groups in range enter the tile's sum
-#pragma unroll
-            for (int g = 0; g < GPW; ++g) {
-                const u32x2 w = *reinterpret_cast<const u32x2 *>(unit + code_rd[g]);
-                u32x4 b[2][2];
-                code_operands_pair(w[0], w[1], mask, one, b);
-                f32x4 p = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int q = 0; q < 4; ++q) p = mfma(a[g][q], b[q >> 1][q & 1], p);
-                const uint32_t sw = *reinterpret_cast<const uint32_t *>(unit + par_rd + 64 * g);
-                const uint32_t zw = *reinterpret_cast<const uint32_t *>(unit + U::PAR + par_rd + 64 * g);
-                float s, z;
-                if constexpr (DEF) {
-                    s = __uint_as_float(sw);
-                    z = __uint_as_float(zw);
-                } else {
-                    s = scale_type == kScaleF32 ? __uint_as_float(sw)
-                        : scale_type == kScaleF16
-                            ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
-                            : __uint_as_float(sw << 16);
-                    z = sym ? 2.0f : __uint_as_float(zw);
-                }
-                const float s4 = 4.0f * s;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) acc[g][i] = __builtin_fmaf(s4, p[i], acc[g][i]);
-                cz[g] = __builtin_fmaf(s, 4.0f + z, cz[g]);
-            }
-            if (++slot_i == NS) slot_i = 0;
-        }
-        // the slots of the units before are free: refill them, UPB units on
-#pragma unroll
-        for (int h = 0; h < UPB; ++h) issue_next();
-        st += UPB;
-        if (st < K) continue;
-        st = 0;
-
-        // end of the tile: per output, the wave's groups in order (each its
-        // stages' sum less c Sx), then the waves' partial sums in wave order.
-        // The buffer written here is next written two tiles later, after a
-        // barrier that the summing wave reaches only once it has read it.
-        f32x4 y = {0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < TPB; ++t)
 #pragma unroll
         for (int g = 0; g < GPW; ++g) {
-            if (g >= gw) break;
-            const f32x4 sxg = sx_lds[wave][g][j];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float t = __builtin_fmaf(-cz[g], sxg[i], acc[g][i]);
-                y[i] = g == 0 ? t : y[i] + t;
-            }
-            acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-            cz[g] = 0.0f;
+            acc[t][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+            cz[t][g] = 0.0f;
         }
-        red[n_red & 1][wave][lane] = y;
-        __syncthreads();
-        if (wave == 0) {
-            f32x4 yo = red[n_red & 1][0][lane];
+    // (a last step past this workgroup's tiles reads units through
+    // descriptors of size 0, whose sums are never stored)
+    for (int tb = 0; tb < my_tiles; tb += TPB) {
 #pragma unroll
-            for (int v = 1; v < kWaves; ++v) {
-                const f32x4 q = red[n_red & 1][v][lane];
-                yo[0] += q[0]; yo[1] += q[1]; yo[2] += q[2]; yo[3] += q[3];
-            }
-            // lane: tokens 4 j + i of output row 16 tile + n; 32-bit byte
-            // offsets into Y (n_tokens rows < 2^26 x 16 x 4 bytes < 2^32)
-            const uint32_t o = (uint32_t)((int)blockIdx.x + ti * (int)gridDim.x) * 16 + (uint32_t)n;
-            if (o < (uint32_t)rows) {
+        for (int pr = 0; pr < PAIRS; ++pr) {
+            // this wave's loads of the next UPB units have landed; then every
+            // wave's have, and every wave is done with the UPB units before
+            // (whose slots the refills below overwrite)
+            wait_vm<(D - UPB) * U::DMA>();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            __syncthreads();
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    if (4 * j + i < n_tokens)
-                        __builtin_amdgcn_raw_buffer_store_b32(
-                            __float_as_uint(yo[i]), yr, ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4,
-                            0, 0);
+            for (int h = 0; h < UPB; ++h) {
+                const int t = (UPB * pr + h) / K;      // tile of the step
+                const char *unit = &ring[slot_i][0];
+                // every group slot, also past this wave's range (its
+                // activations are zero, the codes there other bytes of the
+                // unit): independent chains to interleave; only groups in
+                // range enter the tile's sum
+#pragma unroll
+                for (int g = 0; g < GPW; ++g) {
+                    const u32x2 w = *reinterpret_cast<const u32x2 *>(unit + code_rd[g]);
+                    u32x4 b[2][2];
+                    code_operands_pair(w[0], w[1], mask, one, b);
+                    f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) p = mfma(a[g][q], b[q >> 1][q & 1], p);
+                    const uint32_t sw = *reinterpret_cast<const uint32_t *>(unit + par_rd + 64 * g);
+                    const uint32_t zw = *reinterpret_cast<const uint32_t *>(unit + U::PAR + par_rd + 64 * g);
+                    float s, z;
+                    if constexpr (DEF) {
+                        s = __uint_as_float(sw);
+                        z = __uint_as_float(zw);
+                    } else {
+                        s = scale_type == kScaleF32 ? __uint_as_float(sw)
+                            : scale_type == kScaleF16
+                                ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
+                                : __uint_as_float(sw << 16);
+                        z = sym ? 2.0f : __uint_as_float(zw);
+                    }
+                    const float s4 = 4.0f * s;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[t][g][i] = __builtin_fmaf(s4, p[i], acc[t][g][i]);
+                    cz[t][g] = __builtin_fmaf(s, 4.0f + z, cz[t][g]);
+                }
+                if (++slot_i == NS) slot_i = 0;
             }
+            // the slots of the units before are free: refill them, UPB units on
+#pragma unroll
+            for (int h = 0; h < UPB; ++h) issue_next();
         }
-        ++n_red;
-        ++ti;
+
+        // end of the step's tiles: per output, the wave's groups in order
+        // (each its stages' sum less c Sx), then the waves' partial sums in
+        // wave order. The buffer written here is next written two tiles
+        // later, after a barrier that the summing wave reaches only once it
+        // has read it.
+#pragma unroll
+        for (int t = 0; t < TPB; ++t) {
+            f32x4 y = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int g = 0; g < GPW; ++g) {
+                if (g >= gw) break;
+                const f32x4 sxg = sx_lds[wave][g][j];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float v = __builtin_fmaf(-cz[t][g], sxg[i], acc[t][g][i]);
+                    y[i] = g == 0 ? v : y[i] + v;
+                }
+            }
+#pragma unroll
+            for (int g = 0; g < GPW; ++g) {
+                acc[t][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+                cz[t][g] = 0.0f;
+            }
+            red[n_red & 1][wave][lane] = y;
+            __syncthreads();
+            const int ti = tb + t;
+            if (wave == 0 && ti < my_tiles) {
+                f32x4 yo = red[n_red & 1][0][lane];
+#pragma unroll
+                for (int v = 1; v < kWaves; ++v) {
+                    const f32x4 q = red[n_red & 1][v][lane];
+                    yo[0] += q[0]; yo[1] += q[1]; yo[2] += q[2]; yo[3] += q[3];
+                }
+                // lane: tokens 4 j + i of output row 16 tile + n; 32-bit byte
+                // offsets into Y (n_tokens rows < 2^26 x 16 x 4 bytes < 2^32)
+                const uint32_t o = (uint32_t)((int)blockIdx.x + ti * (int)gridDim.x) * 16 + (uint32_t)n;
+                if (o < (uint32_t)rows) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (4 * j + i < n_tokens)
+                            __builtin_amdgcn_raw_buffer_store_b32(
+                                __float_as_uint(yo[i]), yr,
+                                ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4, 0, 0);
+                }
+            }
+            ++n_red;
+        }
     }
     // no DMA load may still write this workgroup's LDS once it ends
     wait_vm<0>();
@@ -421,12 +439,13 @@ bool linear_batch_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_token
     // registers for cols up to 8 x 4 x 128. The form pays a fixed prologue per
     // workgroup (every wave loads its activations before its first product), so
     // it only gains where each workgroup streams several row tiles: measured
-    // ahead of the general kernel from 12288 rows at 4096 columns or fewer (2 to
-    // 4 stages), and from 24576 rows for one stage; behind it below.
+    // ahead of the general kernel (16 tokens, 4096 columns) from 6144 rows at 2
+    // to 4 stages and from 24576 rows at one stage; behind it at 4096 rows, and
+    // at one stage up to 12288.
     if (G != 128 || n_tokens < kBatchMinTokens || n_tokens > 16 ||
         groups_per_wave(cols) > kGroupsPerWave)
         return false;
-    return k >= 2 ? rows >= 12288 : rows >= 24576;
+    return k >= 2 ? rows >= 6144 : rows >= 24576;
 }
 
 hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const float *zeros,

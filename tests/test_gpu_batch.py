@@ -1,5 +1,5 @@
 """GPU parity of rrq_linear's batch form (groups of 128, 5 to 16 tokens, at most
-4096 cols; 2 to 4 stages from 12288 rows, one stage from 24576 rows), through
+4096 cols; 2 to 4 stages from 6144 rows, one stage from 24576 rows), through
 the C ABI, against the oracle's Eq. 20 product in float64:
 
 * exact: power-of-two scales, integer or dyadic zero-points and
@@ -56,6 +56,7 @@ def _exact(rows, cols, M, seed):
 
 @pytest.mark.parametrize("rows,cols,M,k", [
     (12288, 4096, 16, 4), (12288, 4096, 5, 2), (12290, 128, 5, 3), (12301, 384, 9, 4),
+    (6150, 4096, 13, 3), (7000, 2560, 16, 2),
     (16000, 1024, 12, 2), (12295, 2048, 7, 3), (24576, 4096, 16, 1), (24580, 256, 6, 1),
     (24583, 3072, 11, 4), (40000, 512, 16, 2),
 ])
