@@ -26,9 +26,10 @@
 // accumulator of the stages' 4 s P and a sum of the stages' s (4 + z). At
 // the end of a tile, per output, the wave adds its groups in order (each
 // its stage sum less c Sx) and the 8 waves' partial sums meet in LDS and are
-// summed in wave order. Each product term passes through at most k + 3 +
-// GPW roundings, fewer than in the general kernel's order, so the error
-// bound of include/rrq.h holds.
+// summed in wave order. After the matrix-core sum each product term passes
+// through at most k + 11 roundings (k in its group's stage sum, one with the
+// c Sx term, 3 across the wave's groups, 7 across the waves), within the
+// 2 n + 24 (n >= 2 k) of the error bound of include/rrq.h.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
