@@ -80,12 +80,18 @@ struct ItemSlot {
     static constexpr int DMA = CODE_DMA + 2;       // vector-memory loads per item
 };
 
-// Workgroups per CU: two where a wave needs at most 128 VGPRs (up to 2 sets
-// of 4 groups per wave: 16 waves per CU give the slow-issue integer work of
-// the code operands more waves to pair with), one otherwise. The rings share
-// the CU's 160 KiB of LDS with the reduction buffers accordingly.
-constexpr int wgs_per_cu(int spw) { return spw <= 2 ? 2 : 1; }
-constexpr int ring_bytes(int spw) { return wgs_per_cu(spw) == 2 ? 64 * 1024 : 120 * 1024; }
+// Workgroups per CU: three with one set of 4 groups per wave (at most 85
+// VGPRs: 24 waves per CU give the slow-issue integer work of the code
+// operands more waves to pair with; measured 2-6% faster than two on the
+// Qwen3-8B shapes at 2 to 4 stages, rings 2-3 items deep instead of 3-5),
+// two with 2 sets (at most 128 VGPRs), one otherwise (2 per CU with 3 sets
+// spilled at 4 stages, 25% slower). The rings share the CU's 160 KiB of LDS
+// with the reduction buffers accordingly.
+constexpr int wgs_per_cu(int spw) { return spw == 1 ? 3 : spw == 2 ? 2 : 1; }
+constexpr int ring_bytes(int spw)
+{
+    return wgs_per_cu(spw) == 3 ? 44 * 1024 : wgs_per_cu(spw) == 2 ? 64 * 1024 : 120 * 1024;
+}
 
 // Ring depth: as deep as the 6-bit vmcnt counter (all in-flight items'
 // loads) and the LDS for the 8 waves' rings allow, at most 16.
@@ -427,8 +433,8 @@ bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_toke
     // shape; with 1 stage an item is small and its per-item work costs more
     // than the general kernel's less efficient loads, except on small
     // matrices (latency-bound: this form fills the GPU with 4-row tiles) and
-    // on tall ones with up to 2 sets of 4 groups per wave (two workgroups per
-    // CU).
+    // on tall ones with up to 2 sets of 4 groups per wave (two or three
+    // workgroups per CU).
     if (k >= 2) return true;
     return rows <= 1024 || (rows >= 12288 && cols <= 8192);
 }
