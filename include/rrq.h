@@ -342,7 +342,7 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
  *   stream     HIP stream the work is enqueued on.
  *
- * Arithmetic: every product X * (1 + Q/4), X * 1 is exact in the matrix
+ * Arithmetic: every product X * (4 + Q), X * 1 is exact in the matrix
  * cores; fp32 rounding enters in the accumulations only, in an order fixed
  * by rows, cols, group_size, k_stages and n_tokens (results are
  * deterministic; the same token may round differently in calls with another

@@ -8,8 +8,8 @@
 // Matrix cores (v_mfma_f32_16x16x32_bf16, lane l: row / column n = l % 16,
 // k-slice j = l / 16), the general kernel's operand layouts: A = 16 tokens x
 // 32 inputs of X, B = 32 inputs x 16 output rows of codes (each the bfloat16
-// 1 + Q/4), so P = sum x (1 + Q/4) and Sx = sum x (the same MFMA with a ones
-// operand) give sum x Q = 4 P - 4 Sx; every output of an MFMA is used.
+// 4 + Q), so P = sum x (4 + Q) and Sx = sum x (the same MFMA with a ones
+// operand) give sum x Q = P - 4 Sx; every output of an MFMA is used.
 //
 // Work: the 8 waves of a workgroup split the groups of a row into contiguous
 // ranges of at most 8 (the general kernel's split for 8 waves), so a wave's A
@@ -23,7 +23,7 @@
 // the memory system serves far below its streaming rate). A wave waits for
 // its own share of the unit, one barrier per unit then makes every share
 // visible, and the wave works on its groups of the unit: per group, an
-// accumulator of the stages' 4 s P and a sum of the stages' s (4 + z). At
+// accumulator of the stages' s P and a sum of the stages' s (4 + z). At
 // the end of a tile, per output, the wave adds its groups in order (each
 // its stage sum less c Sx) and the 8 waves' partial sums meet in LDS and are
 // summed in wave order. After the matrix-core sum each product term passes
@@ -49,6 +49,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kWaves = 8;                      // waves per workgroup
 constexpr int kGroupsPerWave = 4;             // A operands held in registers (cols <= 4096)
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
+constexpr uint32_t kFourPair = 0x40804080u;    // two bfloat16 4.0: code operands 4 + Q
 constexpr uint32_t kCodeMask = 0x00600060u;    // top two mantissa bits of both halves
 constexpr int kZpSymmetric = 2;
 constexpr int kScaleF32 = 0, kScaleF16 = 1;
@@ -156,6 +157,8 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     uint32_t mask, one;
     asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
     asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
+    uint32_t four;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(four) : "n"(kFourPair));
 
     // This wave's groups: the general kernel's split for 8 waves (ranges of a
     // whole number of 2-group chunks).
@@ -286,7 +289,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     __builtin_amdgcn_s_setprio(0);
 
     // Per tile of the step and group of the wave: acc[t][g] = sum over
-    // stages of 4 s P and cz[t][g] = sum over stages of s (4 + z), stage by
+    // stages of s P and cz[t][g] = sum over stages of s (4 + z), stage by
     // stage as the units come.
     int slot_i = 0, n_red = 0;
     f32x4 acc[TPB][GPW];
@@ -321,7 +324,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
                 for (int g = 0; g < GPW; ++g) {
                     const u32x2 w = *reinterpret_cast<const u32x2 *>(unit + code_rd[g]);
                     u32x4 b[2][2];
-                    code_operands_pair(w[0], w[1], mask, one, b);
+                    code_operands_pair(w[0], w[1], mask, four, b);
                     f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int q = 0; q < 4; ++q) p = mfma(a[g][q], b[q >> 1][q & 1], p);
@@ -338,9 +341,8 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
                                 : __uint_as_float(sw << 16);
                         z = sym ? 2.0f : __uint_as_float(zw);
                     }
-                    const float s4 = 4.0f * s;
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[t][g][i] = __builtin_fmaf(s4, p[i], acc[t][g][i]);
+                    for (int i = 0; i < 4; ++i) acc[t][g][i] = __builtin_fmaf(s, p[i], acc[t][g][i]);
                     cz[t][g] = __builtin_fmaf(s, 4.0f + z, cz[t][g]);
                 }
                 if (++slot_i == NS) slot_i = 0;

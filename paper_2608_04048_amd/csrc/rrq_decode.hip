@@ -8,7 +8,7 @@
 // n = l % 16, k-slice j = l / 16):
 //   * B columns are 4 output rows x 4 consecutive groups (n = 4 r + g'); lane
 //     j owns inputs 32 j .. 32 j + 31 of its group, i.e. 8 contiguous bytes
-//     of codes per stage. Codes become the bfloat16 1 + Q/4 (one shift and
+//     of codes per stage. Codes become the bfloat16 4 + Q (one shift and
 //     one AND-OR per pair of codes, codes q and q + 8 of a word per register);
 //   * A rows are 4 tokens x the same 4 groups (m = 4 t + g), so C[m][n] is a
 //     group's dot product only on the diagonal g = g': lane l keeps all four
@@ -17,8 +17,9 @@
 //     A operands (the activations, in pairs (x[v], x[v + 8]) of every 16
 //     inputs) and the group sums Sx (from the same MFMA with a ones operand)
 //     are loaded and formed once and stay in registers.
-// Each lane accumulates sum over stages of (4 s) P - (sum over stages of
-// s (4 + z)) Sx for its token, row and group (P = sum x (1 + Q/4)); the four
+// Each lane accumulates sum over stages of s P - (sum over stages of
+// s (4 + z)) Sx for its token, row and group (P = sum x (4 + Q) = 4 Sx +
+// sum x Q); the four
 // groups of a set are summed across lanes and the waves' column ranges
 // through LDS, in a fixed order. Every matrix-core product is exact; fp32
 // rounding is in the accumulations only.
@@ -57,6 +58,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kWaves = 8;                      // waves per workgroup
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
+constexpr uint32_t kFourPair = 0x40804080u;    // two bfloat16 4.0: code operands 4 + Q
 constexpr uint32_t kCodeMask = 0x00600060u;    // top two mantissa bits of both halves
 constexpr int kZpSymmetric = 2;
 constexpr int kScaleF32 = 0, kScaleF16 = 1;
@@ -183,6 +185,8 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
     uint32_t mask, one;
     asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
     asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
+    uint32_t four;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(four) : "n"(kFourPair));
 
     // This lane as B column: row r of the tile, group gb of the set.
     const uint32_t r = n >> 2, gb = n & 3;
@@ -283,7 +287,7 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
     wait_runs<D * L::DMA>(run);
 
     u32x4 a[SPW][4];
-    f32x4 sx[SPW];
+    float sxd[SPW];
     {
         const u32x4 ones = {one, one, one, one};
 #pragma unroll
@@ -293,25 +297,27 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int b = 0; b < 4; ++b) acc = mfma(a[s][b], ones, acc);
-            sx[s] = acc;
+            // the lane's diagonal entry (token j, group gb) is the one used
+            sxd[s] = gb == 0 ? acc[0] : gb == 1 ? acc[1] : gb == 2 ? acc[2] : acc[3];
         }
     }
 
     int n_red = 0, slot_i = 0, tt = 0, bi = 0;
     for (int ti = 0; ti < my_tiles; ++ti) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        float c[SPW];
 #pragma unroll
         for (int set = 0; set < SPW; ++set) {
             // this item's loads have landed; the next D - 1 items' may not
             wait_vm<(D - 1) * L::DMA>();
             const char *slot = my_ring + slot_i * L::BYTES;
-            float c = 0.0f;
+            c[set] = 0.0f;
 #pragma unroll
             for (int st = 0; st < K; ++st) {
                 const u32x2 w = *reinterpret_cast<const u32x2 *>(
                     slot + 1024 * (st >> 1) + 512 * (st & 1) + r * 128 + gb * 32 + j * 8);
                 u32x4 b[2][2];
-                code_operands_pair(w[0], w[1], mask, one, b);
+                code_operands_pair(w[0], w[1], mask, four, b);
                 f32x4 p = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int q = 0; q < 4; ++q) p = mfma(a[set][q], b[q >> 1][q & 1], p);
@@ -328,21 +334,20 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
                             : __uint_as_float(sw << 16);
                     z = sym ? 2.0f : __uint_as_float(zw);
                 }
-                const float s4 = 4.0f * s;
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s4, p[i], acc[i]);
-                c = __builtin_fmaf(s, 4.0f + z, c);
+                for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s, p[i], acc[i]);
+                c[set] = __builtin_fmaf(s, 4.0f + z, c[set]);
             }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-c, sx[set][i], acc[i]);
             // the slot is free: refill it with the item D ahead
             issue_next();
             if (++slot_i == D) slot_i = 0;
         }
         // end of this wave's share of the tile: its diagonal entry (token j,
-        // row r, group gb) summed over the 4 groups of the lanes
-        // n = 4 r .. 4 r + 3, kept for the batch reduction
+        // row r, group gb) less the sets' c Sx terms, summed over the 4
+        // groups of the lanes n = 4 r .. 4 r + 3, kept for the batch reduction
         float y = gb == 0 ? acc[0] : gb == 1 ? acc[1] : gb == 2 ? acc[2] : acc[3];
+#pragma unroll
+        for (int set = 0; set < SPW; ++set) y = __builtin_fmaf(-c[set], sxd[set], y);
         // (quad permutations [1 0 3 2] and [2 3 0 1]: lanes n ^ 1, n ^ 2)
         y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0xB1, 0xF, 0xF, false));
         y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0x4E, 0xF, 0xF, false));

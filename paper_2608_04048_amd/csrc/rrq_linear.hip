@@ -8,14 +8,14 @@
 // and both inner sums run on v_mfma_f32_16x16x32_bf16 with fp32 accumulation:
 //   * A operand: 16 token rows x 32 inputs of X (bfloat16, exact);
 //   * B operand: 32 inputs x 16 output rows of codes, each code Q encoded as
-//     the bfloat16 1 + Q/4 (bits 0x3F80 | Q << 5: the code lands in the top
-//     two mantissa bits with one shift and one AND-OR per pair of codes), so
-//     the MFMA yields P_t = sum x (1 + Q/4) and sum x Q = 4 P_t - 4 Sx
+//     the bfloat16 4 + Q (bits 0x4080 | Q << 5: the code lands in the top
+//     two mantissa bits of 4 with one shift and one AND-OR per pair of
+//     codes), so the MFMA yields P_t = sum x (4 + Q) and sum x Q = P_t - 4 Sx
 //     exactly in real arithmetic;
 //   * Sx = sum x over the group comes from the same MFMA with a B operand of
 //     bfloat16 ones.
-// The group's contribution sum_t s_t (4 P_t - (4 + z_t) Sx) is added to the
-// lane's fp32 accumulators as sum_t (4 s_t) P_t (one fused multiply-add per
+// The group's contribution sum_t s_t (P_t - (4 + z_t) Sx) is added to the
+// lane's fp32 accumulators as sum_t s_t P_t (one fused multiply-add per
 // output and stage) minus c Sx with c = sum_t s_t (4 + z_t) (one per output
 // and group). Every product of the MFMAs is exact; fp32 rounding enters only
 // in the accumulations (error bound in the tests).
@@ -54,6 +54,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr uint32_t kOnePair = 0x3F803F80u;    // two bfloat16 1.0
+constexpr uint32_t kFourPair = 0x40804080u;    // two bfloat16 4.0: code operands 4 + Q
 constexpr uint32_t kCodeMask = 0x00600060u;   // top two mantissa bits of both halves
 
 // Package stage format (values of the C ABI's enums).
@@ -114,16 +115,16 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x
 }
 
 // B operand of one block: codes q = 0..3 of the (pre-shifted) word w sit at
-// bits 2q and 16 + 2q; register q gets codes q and q + 8 as 1 + code / 4.
-// mask and one hold kCodeMask and kOnePair in registers, so that each
+// bits 2q and 16 + 2q; register q gets codes q and q + 8 as 4 + code.
+// mask and four hold kCodeMask and kFourPair in registers, so that each
 // register costs a shift and one AND-OR.
-__device__ __forceinline__ u32x4 code_operand(uint32_t w, uint32_t mask, uint32_t one)
+__device__ __forceinline__ u32x4 code_operand(uint32_t w, uint32_t mask, uint32_t four)
 {
     u32x4 b;
-    b[0] = ((w << 5) & mask) | one;
-    b[1] = ((w << 3) & mask) | one;
-    b[2] = ((w << 1) & mask) | one;
-    b[3] = ((w >> 1) & mask) | one;
+    b[0] = ((w << 5) & mask) | four;
+    b[1] = ((w << 3) & mask) | four;
+    b[2] = ((w << 1) & mask) | four;
+    b[3] = ((w >> 1) & mask) | four;
     return b;
 }
 
@@ -223,13 +224,13 @@ __device__ __forceinline__ void load_chunk(uint32_t lds, const Sources &src, uin
 template <int G, int K, int TT, bool DEF>
 __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int r, int j, int tk,
                                               int scale_type, bool sym, uint32_t mask,
-                                              uint32_t one, f32x4 &acc)
+                                              uint32_t one, uint32_t four, f32x4 &acc)
 {
     using C = Chunk<G, K, TT>;
     constexpr int CG = C::CG;
     constexpr int NB = G / 32;
     const u32x4 ones = {one, one, one, one};
-    // 4 s_t and c = sum_t s_t (4 + z_t) per group of the lane's row
+    // s_t and c = sum_t s_t (4 + z_t) per group of the lane's row
     float s4[K][CG], c[CG];
 #pragma unroll
     for (int q = 0; q < CG; ++q) c[q] = 0.0f;
@@ -250,7 +251,7 @@ __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int
                         : __uint_as_float(sv[q] << 16);
                 z = sym ? 2.0f : __uint_as_float(zv[q]);
             }
-            s4[t][q] = 4.0f * s;
+            s4[t][q] = s;
             c[q] = __builtin_fmaf(s, 4.0f + z, c[q]);
         }
     }
@@ -304,18 +305,18 @@ __device__ __forceinline__ void compute_chunk(const char *lds, int n_groups, int
                 const u32x2 w = *reinterpret_cast<const u32x2 *>(
                     row + 16 * ((2 * q + (j >> 1)) ^ cs) + 8 * (j & 1));
                 u32x4 bop[2][2];
-                code_operands_pair(w[0], w[1], mask, one, bop);
+                code_operands_pair(w[0], w[1], mask, four, bop);
 #pragma unroll
                 for (int b = 0; b < NB; ++b) pq = mfma(a[b], bop[b >> 1][b & 1], pq);
             } else if constexpr (G == 64) {
                 const uint32_t word = *reinterpret_cast<const uint32_t *>(row + 16 * (q ^ cs) + 4 * j);
 #pragma unroll
                 for (int b = 0; b < NB; ++b)
-                    pq = mfma(a[b], code_operand(b ? word >> 8 : word, mask, one), pq);
+                    pq = mfma(a[b], code_operand(b ? word >> 8 : word, mask, four), pq);
             } else {
                 const uint32_t word = *reinterpret_cast<const uint32_t *>(
                     row + 16 * ((q >> 1) ^ cs) + 8 * (q & 1) + 4 * (j >> 1));
-                pq = mfma(a[0], code_operand((j & 1) ? word >> 8 : word, mask, one), pq);
+                pq = mfma(a[0], code_operand((j & 1) ? word >> 8 : word, mask, four), pq);
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s4[t][q], pq[i], acc[i]);
@@ -351,6 +352,8 @@ __global__ __launch_bounds__(64 * tile_waves(TT)) void linear_kernel(
     uint32_t mask, one;
     asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
     asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
+    uint32_t four;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(four) : "n"(kFourPair));
 
     const int64_t o0 = (int64_t)blockIdx.x * 16;
     const uint32_t rows_here = (uint32_t)(rows - o0 < 16 ? rows - o0 : 16);
@@ -398,13 +401,13 @@ __global__ __launch_bounds__(64 * tile_waves(TT)) void linear_kernel(
             const int na = (int)(g_end - ga < CG ? g_end - ga : CG);
             // chunk c is in buffer a; chunk c + 1, if any, may stay in flight
             if (c + 1 < n_chunks) wait_vm<C::DMA>(); else wait_vm<0>();
-            compute_chunk<G, K, TT, DEF>(la, na, r, j, tk, scale_type, sym, mask, one, acc);
+            compute_chunk<G, K, TT, DEF>(la, na, r, j, tk, scale_type, sym, mask, one, four, acc);
             if (c + 2 < n_chunks) load_chunk<G, K, TT>(lds_a, src, ga + 2 * CG, lane);
             if (c + 1 >= n_chunks) break;
             const uint32_t gb = ga + CG;
             const int nb = (int)(g_end - gb < CG ? g_end - gb : CG);
             if (c + 2 < n_chunks) wait_vm<C::DMA>(); else wait_vm<0>();
-            compute_chunk<G, K, TT, DEF>(lb, nb, r, j, tk, scale_type, sym, mask, one, acc);
+            compute_chunk<G, K, TT, DEF>(lb, nb, r, j, tk, scale_type, sym, mask, one, four, acc);
             if (c + 3 < n_chunks) load_chunk<G, K, TT>(lds_b, src, gb + 2 * CG, lane);
         }
 

@@ -6,10 +6,10 @@
 //
 // Per group and stage the inner sums run on v_mfma_f32_16x16x32_bf16 with the
 // general kernel's operand layouts: A = 16 tokens x 32 inputs of X, B = 32
-// inputs x 16 output rows of codes, each code the bfloat16 1 + Q/4, so that
-// P = sum x (1 + Q/4) and Sx = sum x (the same MFMA with a ones operand) give
-// sum x Q = 4 P - 4 Sx. Each output accumulates, per group, sum over stages of
-// (4 s) P then - (sum over stages of s (4 + z)) Sx.
+// inputs x 16 output rows of codes, each code the bfloat16 4 + Q, so that
+// P = sum x (4 + Q) and Sx = sum x (the same MFMA with a ones operand) give
+// sum x Q = P - 4 Sx. Each output accumulates, per group, sum over stages of
+// s P then - (sum over stages of s (4 + z)) Sx.
 //
 // Work: a workgroup of 4 waves owns a tile of 64 tokens x 64 output rows;
 // wave w owns rows 16 w .. 16 w + 15 of it for all 64 tokens, so a B operand
@@ -48,6 +48,7 @@ constexpr int kTokens = 64;                    // tokens per workgroup tile
 constexpr int kRows = 16 * kWaves;             // output rows per workgroup tile
 constexpr int kBuffers = 3;                    // group ring depth
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
+constexpr uint32_t kFourPair = 0x40804080u;    // two bfloat16 4.0: code operands 4 + Q
 constexpr uint32_t kCodeMask = 0x00600060u;    // top two mantissa bits of both halves
 constexpr int kZpSymmetric = 2;
 constexpr int kScaleF32 = 0, kScaleF16 = 1;
@@ -110,6 +111,8 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
     uint32_t mask, one;
     asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
     asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
+    uint32_t four;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(four) : "n"(kFourPair));
 
     // Tiles: consecutive workgroups share the token tile (its activations
     // stay in L2 while the row tiles stream their codes).
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
         const char *lb = &buf[g % kBuffers][0];
         const char *lw = lb + B::X_BYTES + wave * B::WAVE_BYTES;
 
-        // per-stage 4 s and c = sum over stages of s (4 + z) for the lane's row
+        // per-stage s and c = sum over stages of s (4 + z) for the lane's row
         float s4[K], c = 0.0f;
 #pragma unroll
         for (int t = 0; t < K; ++t) {
@@ -214,7 +217,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
                         : __uint_as_float(sw << 16);
                 z = sym ? 2.0f : __uint_as_float(zw);
             }
-            s4[t] = 4.0f * s;
+            s4[t] = s;
             c = __builtin_fmaf(s, 4.0f + z, c);
         }
         // A operands and group sums of the 4 token tiles
@@ -239,7 +242,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
             const u32x2 w = *reinterpret_cast<const u32x2 *>(
                 lw + 1024 * (t >> 1) + 512 * (t & 1) + n * 32 + 8 * j);
             u32x4 bop[2][2];
-            code_operands_pair(w[0], w[1], mask, one, bop);
+            code_operands_pair(w[0], w[1], mask, four, bop);
 #pragma unroll
             for (int tt = 0; tt < 4; ++tt) {
                 f32x4 p = {0.f, 0.f, 0.f, 0.f};
