@@ -12,7 +12,7 @@
 // operand) give sum x Q = P - 4 Sx; every output of an MFMA is used.
 //
 // Work: the 8 waves of a workgroup split the groups of a row into contiguous
-// ranges of at most 8 (the general kernel's split for 8 waves), so a wave's A
+// ranges of at most 4 (the general kernel's split for 8 waves), so a wave's A
 // operands and group sums (16 tokens x its groups) are loaded and formed once
 // and stay in registers. A workgroup takes 16-row tiles in turn and streams
 // each tile stage by stage: a unit (one stage of the tile's 16 rows, every
@@ -21,8 +21,8 @@
 // 64-element runs of scales and zero-points (a 16-row slice of one group
 // would be 16 runs of 32 bytes, and its parameters 64 single words, which
 // the memory system serves far below its streaming rate). A wave waits for
-// its own share of the unit, one barrier per unit then makes every share
-// visible, and the wave works on its groups of the unit: per group, an
+// its own shares of the next two units, one barrier then makes every share
+// visible, and the wave works on its groups of the units: per group, an
 // accumulator of the stages' s P and a sum of the stages' s (4 + z). At
 // the end of a tile, per output, the wave adds its groups in order (each
 // its stage sum less c Sx) and the 8 waves' partial sums meet in LDS and are
@@ -86,9 +86,9 @@ struct Unit {
 constexpr int kRedBytes = 2 * kWaves * 64 * 16;
 
 // Units resident: as many as the CU's 160 KiB of LDS holds beside the
-// reduction buffers and the group sums. The waves keep all but one in
-// flight: a unit's slot is refilled only once every wave has passed the next
-// unit's barrier, i.e. is done with it.
+// reduction buffers and the group sums. The waves keep all but the two being
+// worked on in flight: a unit's slot is refilled only once every wave has
+// passed the next barrier, i.e. is done with it.
 template <int GPW>
 constexpr int unit_slots()
 {
