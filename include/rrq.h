@@ -332,13 +332,13 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *   k_stages   1..n_stages (2 k_stages effective bits).
  *   X          device, bfloat16 bit patterns [n_tokens][cols], 16-byte
  *              aligned (read only).
- *   n_tokens   >= 1; up to 4 tokens are served by one pass over the
- *              package (single-token decode reads it once); 5 to 16 tokens
- *              also by one pass on tall packages (groups of 128, from 12288
- *              rows at up to 4096 cols), more tokens otherwise 16 per pass;
- *              from 128 tokens (groups of 128) 64-token tiles run as a
- *              matrix-core product with the 16-token tiles' accumulation
- *              order (the same results).
+ *   n_tokens   >= 1; the package is read once for up to 16 tokens (the
+ *              decode form streams it for up to 4 tokens, and for 5 to 8 on
+ *              rows of 4096 inputs; the batch form for 5 to 16 on packages
+ *              of at least 6144 rows of up to 4096 inputs), more tokens 16
+ *              per pass; from 128 tokens (groups of 128) 64-token tiles run
+ *              as a matrix-core product with the 16-token tiles'
+ *              accumulation order (the same results).
  *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
  *   stream     HIP stream the work is enqueued on.
  *

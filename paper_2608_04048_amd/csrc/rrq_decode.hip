@@ -1,5 +1,6 @@
-// Decode form of the stage-sum linear layer (Eq. 20) for up to 4 tokens and
-// groups of 128: Y[m][o] = sum over stages t < K and groups g of
+// Decode form of the stage-sum linear layer (Eq. 20) for up to 4 tokens (5
+// to 8 on rows of 4096 inputs) and groups of 128: Y[m][o] = sum over stages
+// t < K and groups g of
 // s_t,o,g (sum_i x_m,i Q_t,o,i - z_t,o,g sum_i x_m,i), the product
 // rrq_linear.hip computes for any shape, organised here for streaming the
 // package from HBM at full width when the activations are few.
@@ -17,6 +18,9 @@
 //     A operands (the activations, in pairs (x[v], x[v + 8]) of every 16
 //     inputs) and the group sums Sx (from the same MFMA with a ones operand)
 //     are loaded and formed once and stay in registers.
+// With 5 to 8 tokens (TQ = 2 quads of 4 tokens) each quad has its own A
+// operands and group sums, and a stage's B operands serve both quads' MFMAs:
+// the operand building, most of the instruction count, is shared.
 // Each lane accumulates sum over stages of s P - (sum over stages of
 // s (4 + z)) Sx for its token, row and group (P = sum x (4 + Q) = 4 Sx +
 // sum x Q); the four
@@ -89,19 +93,26 @@ struct ItemSlot {
 // two with 2 sets (at most 128 VGPRs), one otherwise (2 per CU with 3 sets
 // spilled at 4 stages, 25% slower). The rings share the CU's 160 KiB of LDS
 // with the reduction buffers accordingly.
-constexpr int wgs_per_cu(int spw) { return spw == 1 ? 3 : spw == 2 ? 2 : 1; }
-constexpr int ring_bytes(int spw)
+// With 5 to 8 tokens (two quads of tokens, one set per wave) the A operands
+// take 32 VGPRs: two workgroups per CU, with the larger reduction buffers.
+constexpr int wgs_per_cu(int spw, int tq = 1)
 {
-    return wgs_per_cu(spw) == 3 ? 44 * 1024 : wgs_per_cu(spw) == 2 ? 64 * 1024 : 120 * 1024;
+    return tq > 1 ? 2 : spw == 1 ? 3 : spw == 2 ? 2 : 1;
+}
+constexpr int ring_bytes(int spw, int tq = 1)
+{
+    return wgs_per_cu(spw, tq) == 3 ? 44 * 1024
+           : wgs_per_cu(spw, tq) == 2 ? 64 * 1024 - 8 * 1024 * (tq - 1)
+           : 120 * 1024;
 }
 
 // Ring depth: as deep as the 6-bit vmcnt counter (all in-flight items'
 // loads) and the LDS for the 8 waves' rings allow, at most 16.
-template <int K, int SPW>
+template <int K, int SPW, int TQ>
 constexpr int depth_for()
 {
     constexpr int by_count = 63 / ItemSlot<K>::DMA;
-    constexpr int by_lds = ring_bytes(SPW) / (kWaves * ItemSlot<K>::BYTES);
+    constexpr int by_lds = ring_bytes(SPW, TQ) / (kWaves * ItemSlot<K>::BYTES);
     constexpr int d = by_count < by_lds ? by_count : by_lds;
     return d < 16 ? d : 16;
 }
@@ -163,8 +174,8 @@ __device__ __forceinline__ void wait_runs(u32x4 (&run)[SPW][4])
 // is reduced across the waves through LDS. Batches go to workgroups in turn.
 constexpr int kBatch = 8;
 
-template <int K, int D, int SPW, bool DEF>
-__global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kernel(
+template <int K, int D, int SPW, int TQ, bool DEF>
+__global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW, TQ)) void decode_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int n_tokens, float *__restrict__ Y,
@@ -174,7 +185,7 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
     // the waves' item rings
     __shared__ __attribute__((aligned(16))) char ring[kWaves][D][L::BYTES];
     // partial row sums: [buffer][wave][tile of the batch][token][row]
-    __shared__ float red[2][kWaves][kBatch][16];
+    __shared__ float red[2][kWaves][kBatch][16 * TQ];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;
@@ -267,31 +278,35 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
         }
     };
 
-    // Activations first (the lane as A row: token ta, tokens past n_tokens
-    // repeating the last one, group ga of each of its sets), then the ring.
-    const uint32_t ta = (uint32_t)((n >> 2) < n_tokens ? (n >> 2) : n_tokens - 1);
+    // Activations first (the lane as A row of quad q: token 4 q + n / 4,
+    // tokens past n_tokens repeating the last one, group ga of each of its
+    // sets; operand set u = TQ set + q), then the ring.
     const uint32_t ga = n & 3;
-    u32x4 run[SPW][4];
+    u32x4 run[SPW * TQ][4];
     {
         const u32x4 xs = make_desc(X, (uint32_t)n_tokens * (uint32_t)cols * 2);
 #pragma unroll
-        for (int s = 0; s < SPW; ++s) {
-            const uint32_t gi = ((uint32_t)wave * SPW + s) * 4 + ga;
-            const uint32_t off = ta * (uint32_t)cols * 2 + gi * 256 + 64 * (uint32_t)j;
+        for (int s = 0; s < SPW; ++s)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) run[s][i] = load_run(xs, off + 16 * i);
-        }
+            for (int q = 0; q < TQ; ++q) {
+                const int t = 4 * q + (n >> 2);
+                const uint32_t ta = (uint32_t)(t < n_tokens ? t : n_tokens - 1);
+                const uint32_t gi = ((uint32_t)wave * SPW + s) * 4 + ga;
+                const uint32_t off = ta * (uint32_t)cols * 2 + gi * 256 + 64 * (uint32_t)j;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) run[TQ * s + q][i] = load_run(xs, off + 16 * i);
+            }
     }
 #pragma unroll
     for (int d = 0; d < D; ++d) issue_next();
     wait_runs<D * L::DMA>(run);
 
-    u32x4 a[SPW][4];
-    float sxd[SPW];
+    u32x4 a[SPW * TQ][4];
+    float sxd[SPW * TQ];
     {
         const u32x4 ones = {one, one, one, one};
 #pragma unroll
-        for (int s = 0; s < SPW; ++s) {
+        for (int s = 0; s < SPW * TQ; ++s) {
             act_operands(run[s], a[s]);
             // Sx: C rows 4 j + i = token j, group i of the set
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -304,7 +319,9 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
 
     int n_red = 0, slot_i = 0, tt = 0, bi = 0;
     for (int ti = 0; ti < my_tiles; ++ti) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        f32x4 acc[TQ];
+#pragma unroll
+        for (int q = 0; q < TQ; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
         float c[SPW];
 #pragma unroll
         for (int set = 0; set < SPW; ++set) {
@@ -318,9 +335,14 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
                     slot + 1024 * (st >> 1) + 512 * (st & 1) + r * 128 + gb * 32 + j * 8);
                 u32x4 b[2][2];
                 code_operands_pair(w[0], w[1], mask, four, b);
-                f32x4 p = {0.f, 0.f, 0.f, 0.f};
+                // the stage's B operands serve every quad of tokens
+                f32x4 p[TQ];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) p = mfma(a[set][q], b[q >> 1][q & 1], p);
+                for (int q = 0; q < TQ; ++q) {
+                    p[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) p[q] = mfma(a[TQ * set + q][v], b[v >> 1][v & 1], p[q]);
+                }
                 const uint32_t sw = *reinterpret_cast<const uint32_t *>(slot + L::SCALES + 4 * (16 * st + n));
                 const uint32_t zw = *reinterpret_cast<const uint32_t *>(slot + L::ZEROS + 4 * (16 * st + n));
                 float s, z;
@@ -335,7 +357,9 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
                     z = sym ? 2.0f : __uint_as_float(zw);
                 }
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s, p[i], acc[i]);
+                for (int q = 0; q < TQ; ++q)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[q][i] = __builtin_fmaf(s, p[q][i], acc[q][i]);
                 c[set] = __builtin_fmaf(s, 4.0f + z, c[set]);
             }
             // the slot is free: refill it with the item D ahead
@@ -345,13 +369,16 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
         // end of this wave's share of the tile: its diagonal entry (token j,
         // row r, group gb) less the sets' c Sx terms, summed over the 4
         // groups of the lanes n = 4 r .. 4 r + 3, kept for the batch reduction
-        float y = gb == 0 ? acc[0] : gb == 1 ? acc[1] : gb == 2 ? acc[2] : acc[3];
 #pragma unroll
-        for (int set = 0; set < SPW; ++set) y = __builtin_fmaf(-c[set], sxd[set], y);
-        // (quad permutations [1 0 3 2] and [2 3 0 1]: lanes n ^ 1, n ^ 2)
-        y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0xB1, 0xF, 0xF, false));
-        y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0x4E, 0xF, 0xF, false));
-        if (gb == 0) red[n_red & 1][wave][tt][4 * j + r] = y;
+        for (int q = 0; q < TQ; ++q) {
+            float y = gb == 0 ? acc[q][0] : gb == 1 ? acc[q][1] : gb == 2 ? acc[q][2] : acc[q][3];
+#pragma unroll
+            for (int set = 0; set < SPW; ++set) y = __builtin_fmaf(-c[set], sxd[TQ * set + q], y);
+            // (quad permutations [1 0 3 2] and [2 3 0 1]: lanes n ^ 1, n ^ 2)
+            y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0xB1, 0xF, 0xF, false));
+            y += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, y), 0x4E, 0xF, 0xF, false));
+            if (gb == 0) red[n_red & 1][wave][tt][16 * q + 4 * j + r] = y;
+        }
         if (tt == batch - 1) {
             // end of the batch: sum the waves' partial sums in wave order
             // and store. The buffer written here is next written two batches
@@ -359,8 +386,8 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW)) void decode_kerne
             // they have read it.
             __syncthreads();
             const int tid = threadIdx.x;
-            if (tid < batch * 16) {
-                const int tb = tid / 16, e = tid % 16;   // e = 4 token + row
+            if (tid < batch * 16 * TQ) {
+                const int tb = tid / (16 * TQ), e = tid % (16 * TQ);   // e = 4 token + row
                 float out = red[n_red & 1][0][tb][e];
 #pragma unroll
                 for (int w = 1; w < kWaves; ++w) out += red[n_red & 1][w][tb][e];
@@ -388,26 +415,27 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-template <int K, int SPW, bool DEF>
+template <int K, int SPW, int TQ, bool DEF>
 hipError_t launch_k(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int zp, int sdt, const uint16_t *X, int n_tokens, float *Y,
                     int grid, int batch, hipStream_t stream)
 {
-    constexpr int D = depth_for<K, SPW>();
-    return launch(decode_kernel<K, D, SPW, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros,
-                  rows, cols, rows * cols / 16, rows * cols / 128, X, n_tokens, Y, zp, sdt, batch);
+    constexpr int D = depth_for<K, SPW, TQ>();
+    return launch(decode_kernel<K, D, SPW, TQ, DEF>, grid, 64 * kWaves, stream, codes, scales,
+                  zeros, rows, cols, rows * cols / 16, rows * cols / 128, X, n_tokens, Y, zp, sdt,
+                  batch);
 }
 
-template <int SPW, bool DEF>
+template <int SPW, int TQ, bool DEF>
 hipError_t launch_s(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int n_tokens,
                     float *Y, int grid, int batch, hipStream_t stream)
 {
     switch (k) {
-    case 1: return launch_k<1, SPW, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 2: return launch_k<2, SPW, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 3: return launch_k<3, SPW, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 4: return launch_k<4, SPW, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 1: return launch_k<1, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 2: return launch_k<2, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 3: return launch_k<3, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 4: return launch_k<4, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -417,11 +445,15 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int n_tokens,
                     float *Y, int grid, int batch, hipStream_t stream)
 {
+    if (n_tokens > 4) {   // two quads of tokens, one set of 4 groups per wave
+        if (cols != 4096 || n_tokens > 8) return hipErrorInvalidValue;
+        return launch_s<1, 2, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    }
     switch (cols / 4096) {   // sets of 4 groups per wave
-    case 1: return launch_s<1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 2: return launch_s<2, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 3: return launch_s<3, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 4: return launch_s<4, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 1: return launch_s<1, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 2: return launch_s<2, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 3: return launch_s<3, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 4: return launch_s<4, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -430,9 +462,19 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
 
 bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens)
 {
-    if (G != 128 || n_tokens < 1 || n_tokens > 4 || cols % 4096 != 0 ||
+    if (G != 128 || n_tokens < 1 || n_tokens > 8 || cols % 4096 != 0 ||
         cols / 4096 > kDecodeMaxSetsPerWave)
         return false;
+    // 5 to 8 tokens (two quads, rows of 4096 inputs): measured against the
+    // batch form and the general kernel at 5 and 8 tokens, ahead up to 1024
+    // rows at every stage count (5.9 against 10.8 us at 4 stages, 8 tokens),
+    // up to 8192 rows from 3 stages and above 4096 rows at 2 (6144 x 4096, 8
+    // tokens, k = 4 / 2: 14.4 / 11.4 against 16.8 / 13.1 us), behind or even
+    // elsewhere.
+    if (n_tokens > 4) {
+        if (cols != 4096) return false;
+        return rows <= 1024 || (rows <= 8192 && (k >= 3 || (k == 2 && rows > 4096)));
+    }
     // Measured crossover against the general kernel (one token, packages
     // read from HBM): from 2 stages this form is as fast or faster on every
     // shape; with 1 stage an item is small and its per-item work costs more
@@ -449,10 +491,11 @@ hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const
                                 const uint16_t *X, int64_t n_tokens, float *Y, int cus,
                                 hipStream_t stream)
 {
+    if (n_tokens < 1 || n_tokens > 8 || (n_tokens > 4 && cols != 4096)) return hipErrorInvalidValue;
     const char *sc = static_cast<const char *>(scales);
     // Batches of up to 8 tiles, sized so that every resident workgroup
     // gets the same number of batches: R rounds of one batch per workgroup.
-    const int64_t slots = (int64_t)cus * wgs_per_cu((int)(cols / 4096));
+    const int64_t slots = (int64_t)cus * wgs_per_cu((int)(cols / 4096), (int)((n_tokens + 3) / 4));
     const int64_t tiles = (rows + 3) / 4;
     const int64_t rounds = (tiles + slots * kBatch - 1) / (slots * kBatch);
     const int64_t batch = (tiles + slots * rounds - 1) / (slots * rounds);

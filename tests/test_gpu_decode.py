@@ -1,6 +1,8 @@
 """GPU parity of rrq_linear's decode form (up to 4 tokens, groups of 128,
 cols a multiple of 4096 up to 16384; 2 to 4 stages at any row count, 1 stage
-up to 1024 rows or from 12288 rows with up to 8192 cols), through the C ABI,
+up to 1024 rows or from 12288 rows with up to 8192 cols; 5 to 8 tokens on
+rows of 4096 inputs, up to 1024 rows at any stage count and up to 8192 rows
+from 2 or 3 stages), through the C ABI,
 against the oracle's Eq. 20 product in float64 on sampled output rows.
 
 * exact: power-of-two scales, integer or dyadic zero-points and
@@ -64,6 +66,9 @@ def _run(gpu, codes, s, z, rows, cols, k, xb, zp=None, sd=None, s_raw=None):
     (4096, 4096, 1, 3), (4099, 8192, 2, 4), (1024, 16384, 1, 3),
     # one stage
     (1000, 4096, 2, 1), (12290, 8192, 1, 1), (13, 12288, 4, 1),
+    # 5 to 8 tokens: two quads of tokens (the second partly past the last)
+    (1024, 4096, 5, 1), (1021, 4096, 8, 2), (3, 4096, 6, 4), (6144, 4096, 8, 4),
+    (6150, 4096, 7, 3), (8192, 4096, 5, 2), (4099, 4096, 8, 3),
 ])
 def test_decode_form_exact(gpu, rows, cols, M, k):
     _log(f"decode exact rows={rows} cols={cols} M={M} k={k}")
@@ -88,8 +93,9 @@ def test_decode_form_exact(gpu, rows, cols, M, k):
 def test_decode_form_exact_formats(gpu, zp, sd):
     """Stage formats through the decode form: power-of-two scales stored as
     16-bit patterns where the format says so, dyadic real zero-points."""
-    rows, cols, M, k = 6148, 4096, 3, 4
-    _log(f"decode exact format {zp}/{sd}")
+    rows, cols, k = 6148, 4096, 4
+    M = 3 if zp == "int" and sd == "f32" else 7
+    _log(f"decode exact format {zp}/{sd} M={M}")
     rng = np.random.default_rng(77)
     S = 4
     codes = rng.integers(0, 2 ** 32, (S, rows * cols // 16), dtype=np.uint64).astype(np.uint32)
@@ -118,8 +124,9 @@ def test_decode_form_exact_formats(gpu, zp, sd):
 
 
 @pytest.mark.parametrize("zp,sd", [("int", "f32"), ("sym", "f16"), ("real", "f32")])
-def test_decode_form_realistic_within_bound(gpu, zp, sd):
-    rows, cols, M = 6144, 4096, 4
+@pytest.mark.parametrize("M", [4, 8])
+def test_decode_form_realistic_within_bound(gpu, zp, sd, M):
+    rows, cols = 6144, 4096
     rng = np.random.default_rng(9)
     w = (rng.standard_normal(rows * cols) * 0.02).astype(np.float32)
     w = np.where(rng.random(w.size) < 1e-3, w * 20, w).astype(np.float32)
