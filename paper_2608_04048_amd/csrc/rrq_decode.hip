@@ -28,9 +28,10 @@
 // through LDS, in a fixed order. Every matrix-core product is exact; fp32
 // rounding is in the accumulations only.
 //
-// Work: the 8 waves of a workgroup split every 4-row tile's columns, so at
-// any moment a workgroup reads whole rows and neighbouring workgroups read
-// neighbouring rows; a workgroup takes batches of consecutive tiles in turn.
+// Work: the waves of a workgroup (8; 12 and 16 on rows of 12288 and 16384
+// inputs) split every 4-row tile's columns, so at any moment a workgroup
+// reads whole rows and neighbouring workgroups read neighbouring rows; a
+// workgroup takes batches of consecutive tiles in turn.
 // Each wave walks its (tile, set) items as one sequence.
 //
 // Memory path: an item's codes (4 rows x 128 contiguous bytes per stage),
@@ -60,7 +61,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kWaves = 8;                      // waves per workgroup
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
 constexpr uint32_t kFourPair = 0x40804080u;    // two bfloat16 4.0: code operands 4 + Q
 constexpr uint32_t kCodeMask = 0x00600060u;    // top two mantissa bits of both halves
@@ -86,33 +86,48 @@ struct ItemSlot {
     static constexpr int DMA = CODE_DMA + 2;       // vector-memory loads per item
 };
 
-// Workgroups per CU: three with one set of 4 groups per wave (at most 85
+// Partial row sums of a batch of up to kBatch tiles, double-buffered.
+constexpr int kBatch = 8;
+constexpr int red_bytes(int wv, int tq) { return 2 * wv * kBatch * 16 * tq * 4; }
+
+// Waves per workgroup (WV) and sets of 4 groups per wave (SPW) by the sets
+// in a row (cols / 512; up to 4 tokens): 8 x 1 and 8 x 2 for rows of 4096
+// and 8192 inputs, 12 x 2 and 16 x 2 for 12288 and 16384. A set's A operands
+// take 16 VGPRs for the whole call, so at 3 sets per wave the 8-wave
+// workgroup fitted only once per CU (two waves per SIMD; twice it spilled at 4
+// stages); 12 or 16 waves of 2 sets keep 3 or 4 waves per SIMD busy
+// (measured 4096 x 12288 at 4 / 2 stages: 21.9 / 14.8 -> 19.3 / 13.9 us,
+// 4096 x 16384: 27.4 / 18.9 -> 25.7 / 16.6 us).
+constexpr int waves_for(int sets) { return sets <= 16 ? 8 : sets / 2; }
+constexpr int sets_per_wave(int sets) { return sets / waves_for(sets); }
+
+// Workgroups per CU: three with 8 waves of one set of 4 groups (at most 85
 // VGPRs: 24 waves per CU give the slow-issue integer work of the code
 // operands more waves to pair with; measured 2-6% faster than two on the
 // Qwen3-8B shapes at 2 to 4 stages, rings 2-3 items deep instead of 3-5),
-// two with 2 sets (at most 128 VGPRs), one otherwise (2 per CU with 3 sets
-// spilled at 4 stages, 25% slower). The rings share the CU's 160 KiB of LDS
-// with the reduction buffers accordingly.
-// With 5 to 8 tokens (two quads of tokens, one set per wave) the A operands
-// take 32 VGPRs: two workgroups per CU, with the larger reduction buffers.
-constexpr int wgs_per_cu(int spw, int tq = 1)
+// two with 8 waves of 2 sets (at most 128 VGPRs), one with 12 or 16 waves.
+// The rings share the CU's 160 KiB of LDS with the reduction buffers
+// accordingly. With 5 to 8 tokens (two quads of tokens, 8 waves of one set)
+// the A operands take 32 VGPRs: two workgroups per CU, with the larger
+// reduction buffers.
+constexpr int wgs_per_cu(int wv, int spw, int tq)
 {
-    return tq > 1 ? 2 : spw == 1 ? 3 : spw == 2 ? 2 : 1;
+    return wv > 8 ? 1 : tq > 1 ? 2 : spw == 1 ? 3 : 2;
 }
-constexpr int ring_bytes(int spw, int tq = 1)
+constexpr int ring_bytes(int wv, int spw, int tq)
 {
-    return wgs_per_cu(spw, tq) == 3 ? 44 * 1024
-           : wgs_per_cu(spw, tq) == 2 ? 64 * 1024 - 8 * 1024 * (tq - 1)
-           : 120 * 1024;
+    return wgs_per_cu(wv, spw, tq) == 3   ? 44 * 1024
+           : wgs_per_cu(wv, spw, tq) == 2 ? 64 * 1024 - 8 * 1024 * (tq - 1)
+                                          : 160 * 1024 - red_bytes(wv, tq);
 }
 
 // Ring depth: as deep as the 6-bit vmcnt counter (all in-flight items'
-// loads) and the LDS for the 8 waves' rings allow, at most 16.
-template <int K, int SPW, int TQ>
+// loads) and the LDS for the waves' rings allow, at most 16.
+template <int K, int WV, int SPW, int TQ>
 constexpr int depth_for()
 {
     constexpr int by_count = 63 / ItemSlot<K>::DMA;
-    constexpr int by_lds = ring_bytes(SPW, TQ) / (kWaves * ItemSlot<K>::BYTES);
+    constexpr int by_lds = ring_bytes(WV, SPW, TQ) / (WV * ItemSlot<K>::BYTES);
     constexpr int d = by_count < by_lds ? by_count : by_lds;
     return d < 16 ? d : 16;
 }
@@ -168,14 +183,12 @@ __device__ __forceinline__ void wait_runs(u32x4 (&run)[SPW][4])
     }
 }
 
-// Workgroup: 8 waves share each 4-row tile, wave w taking sets
-// w SPW .. w SPW + SPW - 1 of its 8 SPW sets of 4 groups (so the waves of a
+// Workgroup: WV waves share each 4-row tile, wave w taking sets
+// w SPW .. w SPW + SPW - 1 of its WV SPW sets of 4 groups (so the waves of a
 // workgroup read whole rows together); a batch of up to 8 consecutive tiles
 // is reduced across the waves through LDS. Batches go to workgroups in turn.
-constexpr int kBatch = 8;
-
-template <int K, int D, int SPW, int TQ, bool DEF>
-__global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW, TQ)) void decode_kernel(
+template <int K, int D, int WV, int SPW, int TQ, bool DEF>
+__global__ __launch_bounds__(64 * WV, WV * wgs_per_cu(WV, SPW, TQ) / 4) void decode_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int n_tokens, float *__restrict__ Y,
@@ -183,9 +196,9 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW, TQ)) void decode_k
 {
     using L = ItemSlot<K>;
     // the waves' item rings
-    __shared__ __attribute__((aligned(16))) char ring[kWaves][D][L::BYTES];
+    __shared__ __attribute__((aligned(16))) char ring[WV][D][L::BYTES];
     // partial row sums: [buffer][wave][tile of the batch][token][row]
-    __shared__ float red[2][kWaves][kBatch][16 * TQ];
+    __shared__ float red[2][WV][kBatch][16 * TQ];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;
@@ -390,7 +403,7 @@ __global__ __launch_bounds__(64 * kWaves, 2 * wgs_per_cu(SPW, TQ)) void decode_k
                 const int tb = tid / (16 * TQ), e = tid % (16 * TQ);   // e = 4 token + row
                 float out = red[n_red & 1][0][tb][e];
 #pragma unroll
-                for (int w = 1; w < kWaves; ++w) out += red[n_red & 1][w][tb][e];
+                for (int w = 1; w < WV; ++w) out += red[n_red & 1][w][tb][e];
                 const int64_t tile = ((int64_t)blockIdx.x + (int64_t)bi * gridDim.x) * batch + tb;
                 const int64_t o = tile * 4 + (e & 3);
                 const int tok = e >> 2;
@@ -415,27 +428,29 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-template <int K, int SPW, int TQ, bool DEF>
+template <int K, int WV, int SPW, int TQ, bool DEF>
 hipError_t launch_k(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int zp, int sdt, const uint16_t *X, int n_tokens, float *Y,
                     int grid, int batch, hipStream_t stream)
 {
-    constexpr int D = depth_for<K, SPW, TQ>();
-    return launch(decode_kernel<K, D, SPW, TQ, DEF>, grid, 64 * kWaves, stream, codes, scales,
+    static_assert(wgs_per_cu(WV, SPW, TQ) * (ring_bytes(WV, SPW, TQ) + red_bytes(WV, TQ)) <=
+                      160 * 1024, "the workgroups of a CU share its 160 KiB of LDS");
+    constexpr int D = depth_for<K, WV, SPW, TQ>();
+    return launch(decode_kernel<K, D, WV, SPW, TQ, DEF>, grid, 64 * WV, stream, codes, scales,
                   zeros, rows, cols, rows * cols / 16, rows * cols / 128, X, n_tokens, Y, zp, sdt,
                   batch);
 }
 
-template <int SPW, int TQ, bool DEF>
+template <int WV, int SPW, int TQ, bool DEF>
 hipError_t launch_s(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int n_tokens,
                     float *Y, int grid, int batch, hipStream_t stream)
 {
     switch (k) {
-    case 1: return launch_k<1, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 2: return launch_k<2, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 3: return launch_k<3, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 4: return launch_k<4, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 1: return launch_k<1, WV, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 2: return launch_k<2, WV, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 3: return launch_k<3, WV, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 4: return launch_k<4, WV, SPW, TQ, DEF>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, grid, batch, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -447,13 +462,13 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
 {
     if (n_tokens > 4) {   // two quads of tokens, one set of 4 groups per wave
         if (cols != 4096 || n_tokens > 8) return hipErrorInvalidValue;
-        return launch_s<1, 2, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+        return launch_s<8, 1, 2, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
     }
-    switch (cols / 4096) {   // sets of 4 groups per wave
-    case 1: return launch_s<1, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 2: return launch_s<2, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 3: return launch_s<3, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
-    case 4: return launch_s<4, 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    switch (cols / 4096) {   // sets of 4 groups per row / 8
+    case 1: return launch_s<waves_for(8), sets_per_wave(8), 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 2: return launch_s<waves_for(16), sets_per_wave(16), 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 3: return launch_s<waves_for(24), sets_per_wave(24), 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    case 4: return launch_s<waves_for(32), sets_per_wave(32), 1, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
     default: return hipErrorInvalidValue;
     }
 }
@@ -463,7 +478,7 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
 bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens)
 {
     if (G != 128 || n_tokens < 1 || n_tokens > 8 || cols % 4096 != 0 ||
-        cols / 4096 > kDecodeMaxSetsPerWave)
+        cols > kDecodeMaxCols)
         return false;
     // 5 to 8 tokens (two quads, rows of 4096 inputs): measured against the
     // batch form and the general kernel at 5 and 8 tokens, ahead up to 1024
@@ -495,7 +510,9 @@ hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const
     const char *sc = static_cast<const char *>(scales);
     // Batches of up to 8 tiles, sized so that every resident workgroup
     // gets the same number of batches: R rounds of one batch per workgroup.
-    const int64_t slots = (int64_t)cus * wgs_per_cu((int)(cols / 4096), (int)((n_tokens + 3) / 4));
+    const int sets = (int)(cols / 512), tq = (int)((n_tokens + 3) / 4);
+    const int64_t slots = (int64_t)cus * (tq > 1 ? wgs_per_cu(8, 1, tq)
+                                                 : wgs_per_cu(waves_for(sets), sets_per_wave(sets), 1));
     const int64_t tiles = (rows + 3) / 4;
     const int64_t rounds = (tiles + slots * kBatch - 1) / (slots * kBatch);
     const int64_t batch = (tiles + slots * rounds - 1) / (slots * rounds);

@@ -58,11 +58,11 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
                          hipStream_t stream);
 
 // The decode form of the linear layer (up to 4 tokens, groups of 128, cols
-// a multiple of 4096 up to 4096 kDecodeMaxSetsPerWave, or 5 to 8 tokens on
-// rows of 4096 inputs; and the stage counts and row counts where it is the
-// faster one: linear_decode_fits);
+// a multiple of 4096 up to kDecodeMaxCols, or 5 to 8 tokens on rows of 4096
+// inputs; and the stage counts and row counts where it is the faster one:
+// linear_decode_fits);
 // launch_linear covers every other case.
-constexpr int kDecodeMaxSetsPerWave = 4;
+constexpr int kDecodeMaxCols = 16384;
 // The batch form (groups of 128, kBatchMinTokens to 16 tokens, at most 4096
 // cols: the A operands of a wave's groups stay in its registers; and the row
 // and stage counts where it is the faster one: linear_batch_fits).

@@ -66,6 +66,8 @@ def _run(gpu, codes, s, z, rows, cols, k, xb, zp=None, sd=None, s_raw=None):
     (4096, 4096, 1, 3), (4099, 8192, 2, 4), (1024, 16384, 1, 3),
     # one stage
     (1000, 4096, 2, 1), (12290, 8192, 1, 1), (13, 12288, 4, 1),
+    # rows of 12288 and 16384 inputs: 12 and 16 waves of 2 sets per workgroup
+    (4096, 12288, 1, 4), (4099, 12288, 3, 3), (2050, 16384, 4, 4), (30, 16384, 2, 2),
     # 5 to 8 tokens: two quads of tokens (the second partly past the last)
     (1024, 4096, 5, 1), (1021, 4096, 8, 2), (3, 4096, 6, 4), (6144, 4096, 8, 4),
     (6150, 4096, 7, 3), (8192, 4096, 5, 2), (4099, 4096, 8, 3),
