@@ -11,25 +11,33 @@
 // 4 + Q), so P = sum x (4 + Q) and Sx = sum x (the same MFMA with a ones
 // operand) give sum x Q = P - 4 Sx; every output of an MFMA is used.
 //
-// Work: the 8 waves of a workgroup split the groups of a row into contiguous
-// ranges of at most 4 (the general kernel's split for 8 waves), so a wave's A
-// operands and group sums (16 tokens x its groups) are loaded and formed once
-// and stay in registers. A workgroup takes 16-row tiles in turn and streams
-// each tile stage by stage: a unit (one stage of the tile's 16 rows, every
-// group) goes from HBM into a ring of LDS slots shared by the 8 waves by
-// LDS-DMA loads, each wave issuing a fixed share of whole-row code runs and
-// 64-element runs of scales and zero-points (a 16-row slice of one group
-// would be 16 runs of 32 bytes, and its parameters 64 single words, which
-// the memory system serves far below its streaming rate). A wave waits for
-// its own shares of the next two units, one barrier then makes every share
-// visible, and the wave works on its groups of the units: per group, an
-// accumulator of the stages' s P and a sum of the stages' s (4 + z). At
-// the end of a tile, per output, the wave adds its groups in order (each
-// its stage sum less c Sx) and the 8 waves' partial sums meet in LDS and are
-// summed in wave order. After the matrix-core sum each product term passes
-// through at most k + 11 roundings (k in its group's stage sum, one with the
-// c Sx term, 3 across the wave's groups, 7 across the waves), within the
-// 2 n + 24 (n >= 2 k) of the error bound of include/rrq.h.
+// Work: wave w of a workgroup's 8 owns the set of groups 4 w .. 4 w + 3 of
+// every row (rows of up to 4096 inputs), so its A operands (16 tokens x 4
+// groups) are loaded and formed once and stay in registers. A workgroup
+// takes 16-row tiles in turn; each wave walks its (tile, stage) items as one
+// sequence, accumulating per output (lane: tokens 4 j .. 4 j + 3 of row n)
+// the stages' and groups' s P, and per group the stages' s (4 + z). At the
+// end of a tile the wave subtracts each group's c Sx and the 8 waves' sums
+// meet in LDS, summed in wave order: one barrier per tile.
+//
+// Memory path (the decode form's): an item's codes (16 rows x the set's 128
+// contiguous bytes, one stage), scales and zero-points (16 rows x 4 groups)
+// go from HBM straight into a ring of D LDS slots per wave by LDS-DMA loads,
+// a fixed count per item; the wave keeps the next D - 1 items in flight and
+// waits for exactly the item it is about to read. Code pieces sit in the
+// slot XOR-swizzled by row so that an MFMA's 16 rows read distinct banks.
+// One accumulator per output takes every group and stage (one per group was
+// slower: the compiler then holds more MFMA results), so after the
+// matrix-core sum each product term passes through at most 4 k + 11
+// roundings (4 k in the wave's sum over stages and groups, 4 with the groups'
+// c Sx terms, 7 across the waves), within the 2 n + 24 (n >= 2 k) of the
+// error bound of include/rrq.h.
+//
+// The form's first version streamed each unit (one stage of a tile, every
+// group) through a ring shared by the 8 waves, with a barrier per two units;
+// per-wave rings with one barrier per tile are 4-15% faster on the Qwen3-8B
+// shapes at 2 to 4 stages (24576 x 4096, 16 tokens, 4 / 2 stages: 39.5 /
+// 27.7 -> 37.8 / 26.5 us; 6144 x 4096: 18.6 / 14.5 -> 17.3 / 12.4 us).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -60,39 +68,29 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-// A unit: one stage of a 16-row tile, every group of the rows, as the
-// workgroup's 8 waves share it in LDS: the 16 rows' codes (row r at r RB
-// bytes, RB = cols / 4, its 16-byte pieces XOR-swizzled within aligned runs
-// of 16 so that an MFMA's 16 rows read distinct banks), then the scales and
-// the zero-points of the 16 rows (one 32-bit word per element, group-major:
-// row r group g at 16 g + r, so that an MFMA's 16 rows read consecutive
-// words; a 16-bit scale in the low half). The waves fetch a unit together,
-// each a fixed share of 1 KiB code loads (whole rows) and 64-element
-// parameter loads (4 groups of the 16 rows); loads past the unit's end read
-// nothing, so every wave issues the same loads per unit.
-template <int GPW>
-struct Unit {
-    static constexpr int CODE = 16 * GPW * kWaves * 32;      // 16 rows of at most GPW x 8 groups
-    static constexpr int PAR = 16 * GPW * kWaves * 4;        // 16 rows x groups, one word each
-    static constexpr int BYTES = CODE + 2 * PAR;
-    static constexpr int CI = CODE / 1024 / kWaves;          // code loads per wave
-    static constexpr int PI = PAR / 256 / kWaves;            // loads per wave per parameter buffer
-    static constexpr int DMA = CI + 2 * PI;                  // loads per wave per unit
+// One item's LDS slot (a 16-row tile, the wave's set of 4 groups, one
+// stage): the codes, row r's 16-byte piece p at 128 r + 16 (p ^ (r & 7)) (an
+// MFMA's 16 rows then fall on distinct banks but for rows 8 apart); then the
+// scales and the zero-points as 32-bit words, row r group g at 4 (4 r + g)
+// of their block (a 16-bit scale in the low half).
+struct ItemSlot {
+    static constexpr int SCALES = 2048;
+    static constexpr int ZEROS = SCALES + 256;
+    static constexpr int BYTES = ZEROS + 256;
+    static constexpr int DMA = 4;               // two 1 KiB code loads, scales, zero-points
 };
 
-// Groups per wave GPW: the A operands of a wave's groups stay in its
-// registers (16 tokens x GPW groups, 16 GPW VGPRs); GPW = 4 serves rows of up
-// to 4096 inputs. One workgroup per CU.
+// One workgroup per CU (up to 256 VGPRs a lane: the A operands of 4 groups
+// take 64; two per CU, at 128, spilled from 2 stages and were up to 40%
+// slower) and the ring depth its 160 KiB of LDS allows beside the reduction
+// buffers and group sums, within the 6-bit vmcnt with the activations' loads.
 constexpr int kRedBytes = 2 * kWaves * 64 * 16;
-
-// Units resident: as many as the CU's 160 KiB of LDS holds beside the
-// reduction buffers and the group sums. The waves keep all but the two being
-// worked on in flight: a unit's slot is refilled only once every wave has
-// passed the next barrier, i.e. is done with it.
-template <int GPW>
-constexpr int unit_slots()
+constexpr int kSxBytes = kWaves * kGroupsPerWave * 64;
+constexpr int depth_for()
 {
-    return (160 * 1024 - kRedBytes - kWaves * GPW * 64) / Unit<GPW>::BYTES;
+    constexpr int by_lds = (160 * 1024 - kRedBytes - kSxBytes) / (kWaves * ItemSlot::BYTES);
+    constexpr int by_count = (63 - 4 * kGroupsPerWave) / ItemSlot::DMA;
+    return by_lds < by_count ? by_lds : by_count;
 }
 
 // A operands of one group for the lane (token n, k-slice j) from its inputs
@@ -121,31 +119,19 @@ __device__ __forceinline__ u32x4 load_run(const u32x4 &desc, uint32_t voff)
     return v;
 }
 
-template <int K, bool DEF, int GPW>
+template <int K, int D, bool DEF>
 __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int n_tokens, float *__restrict__ Y,
     int zero_point, int scale_type)
 {
-    using U = Unit<GPW>;
-    constexpr int NS = unit_slots<GPW>();
-    // Two units per barrier (half the barriers, twice the independent chains
-    // between them); a loop step covers TPB whole tiles, two where a tile has
-    // an odd number of stages, so that every unit's tile is known at compile
-    // time.
-    constexpr int UPB = 2;
-    constexpr int TPB = K % 2 == 0 ? 1 : 2;
-    constexpr int PAIRS = TPB * K / UPB;
-    // Units in flight: the refills after a barrier overwrite the slots of
-    // the UPB units before it, which every wave is done with by then.
-    constexpr int D = NS - UPB;
-    static_assert(D >= 2 * UPB && D * U::DMA + 4 * GPW <= 63, "unit ring");
-    __shared__ __attribute__((aligned(16))) char ring[NS][U::BYTES];
+    using L = ItemSlot;
+    constexpr int GPW = kGroupsPerWave;
+    __shared__ __attribute__((aligned(16))) char ring[kWaves][D][L::BYTES];
     __shared__ f32x4 red[2][kWaves][64];
-    // group sums of the wave's groups: Sx depends on the token only, so a
-    // wave keeps its 16 tokens x GPW groups here rather than in registers
-    // (lane k-slice j reads tokens 4 j .. 4 j + 3 as one 16-byte broadcast)
+    // group sums of the wave's groups: Sx depends on the token only (lane
+    // k-slice j reads tokens 4 j .. 4 j + 3 as one 16-byte broadcast)
     __shared__ f32x4 sx_lds[kWaves][GPW][4];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -153,19 +139,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     const int j = lane >> 4;
     const bool sym = zero_point == kZpSymmetric;
     const int gpr = (int)(cols / 128);                  // groups per row
-    const int cpr = (int)(cols / 64);                   // 16-byte code pieces per row
+    const int g_begin = GPW * wave;                     // this wave's set
+    const int gw = gpr - g_begin < GPW ? (gpr - g_begin > 0 ? gpr - g_begin : 0) : GPW;
     uint32_t mask, one;
     asm volatile("s_mov_b32 %0, %1" : "=s"(mask) : "n"(kCodeMask));
     asm volatile("v_mov_b32 %0, %1" : "=v"(one) : "n"(kOnePair));
     uint32_t four;
     asm volatile("v_mov_b32 %0, %1" : "=v"(four) : "n"(kFourPair));
-
-    // This wave's groups: the general kernel's split for 8 waves (ranges of a
-    // whole number of 2-group chunks).
-    const int per_wave = ((gpr + kWaves - 1) / kWaves + 1) / 2 * 2;
-    const int g_begin = per_wave * wave < gpr ? per_wave * wave : gpr;
-    const int g_end = g_begin + per_wave < gpr ? g_begin + per_wave : gpr;
-    const int gw = g_end - g_begin;                     // 0 .. GPW
 
     const uint32_t row_bytes = (uint32_t)(cols / 4);
     const uint32_t plane_bytes = (uint32_t)plane_words * 4;
@@ -173,91 +153,75 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
     const u32x4 dc = make_desc(codes, (uint32_t)K * plane_bytes);
     const u32x4 ds = make_desc(scales, (uint32_t)K * (uint32_t)plane_groups * sbytes);
     const u32x4 dz = make_desc(sym ? nullptr : zeros, sym ? 0u : (uint32_t)K * (uint32_t)plane_groups * 4);
-    u32x4 dc0 = dc, ds0 = ds, dz0 = dz;                 // size 0: no access
-    dc0[2] = ds0[2] = dz0[2] = 0u;
 
-    // Code pieces within a row are swizzled by XOR with the row's low bits,
-    // over the largest run of 16 or fewer pieces that divides the row.
-    const int swz = (cpr & -cpr) < 16 ? (cpr & -cpr) - 1 : 15;
-    // This lane's loads of a unit (offsets from the unit's first row of the
-    // plane): code piece q = 64 (wave CI + i) + lane is row q / cpr, LDS piece
-    // q % cpr holding the row's piece (q % cpr) ^ (row & swz); parameter word
-    // e = 64 (wave PI + i) + lane holds row e % 16, group e / 16.
-    uint32_t v_code[U::CI], v_scale[U::PI], v_zero[U::PI];
+    // DMA lane offsets within an item (from the tile's first row of the
+    // stage plane, the set's first byte). Codes: load i, lane l -> slot
+    // bytes 1024 i + 16 l = row r = 8 i + l / 8, slot piece l % 8, holding
+    // the row's piece (l % 8) ^ (r & 7) (8 runs of 128 bytes per load);
+    // pieces of groups past the row read nothing. Scales and zero-points:
+    // lane l -> row l / 4, group l % 4.
+    uint32_t dma_code[2];
 #pragma unroll
-    for (int i = 0; i < U::CI; ++i) {
-        const int q = 64 * (wave * U::CI + i) + lane;
-        const int r = q / cpr, c = q - r * cpr;
-        v_code[i] = q < 16 * cpr ? (uint32_t)r * row_bytes + (uint32_t)(c ^ (r & swz)) * 16 : kSkip;
+    for (int i = 0; i < 2; ++i) {
+        const int r = 8 * i + (lane >> 3);
+        const int p = (lane & 7) ^ (r & 7);
+        dma_code[i] = p < 2 * gw ? (uint32_t)r * row_bytes + 16u * (uint32_t)p : kSkip;
     }
-#pragma unroll
-    for (int i = 0; i < U::PI; ++i) {
-        const int e = 64 * (wave * U::PI + i) + lane;
-        const uint32_t el = (uint32_t)((e & 15) * gpr + (e >> 4));
-        v_scale[i] = e < 16 * gpr ? el * sbytes : kSkip;
-        v_zero[i] = e < 16 * gpr ? el * 4 : kSkip;
-    }
-    // This lane's reads (B column: row n, k-slice j): the 8 code bytes of
-    // group g_begin + g at code_rd[g] within a unit, its parameters at
-    // par_rd + 64 g.
+    const int pg = lane & 3;
+    const uint32_t pel = (uint32_t)(lane >> 2) * (uint32_t)gpr + (uint32_t)pg;
+    const uint32_t dma_scale = pg < gw ? pel * sbytes : kSkip;
+    const uint32_t dma_zero = pg < gw ? pel * 4 : kSkip;
+    // This lane's reads (B column: row n, k-slice j): group g's 8 code bytes
+    // at code_rd[g], its scale and zero-point at par_rd + 4 g.
     uint32_t code_rd[GPW];
 #pragma unroll
-    for (int g = 0; g < GPW; ++g) {
-        const int c = 2 * (g_begin + g) + (j >> 1);
-        code_rd[g] = (uint32_t)n * row_bytes + (uint32_t)(c ^ (n & swz)) * 16 + (uint32_t)(j & 1) * 8;
-    }
-    const uint32_t par_rd = U::CODE + 4 * (uint32_t)(16 * g_begin + n);
+    for (int g = 0; g < GPW; ++g)
+        code_rd[g] = 128u * (uint32_t)n + 16u * (uint32_t)((2 * g + (j >> 1)) ^ (n & 7)) +
+                     8u * (uint32_t)(j & 1);
+    const uint32_t par_rd = 16u * (uint32_t)n;
 
-    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
-        Y, (short)0, (int)((uint32_t)n_tokens * (uint32_t)rows * 4u), (int)kRsrcWord3);
-    const uint32_t lds_ring = lds_address(&ring[0][0]);
+    const uint32_t lds_ring = lds_address(&ring[wave][0][0]);
+    const char *my_ring = &ring[wave][0][0];
 
-    // Row tiles of this workgroup: blockIdx, blockIdx + grid, ...; units in
-    // order: tile t, stage st = unit t K + st.
+    // Row tiles of this workgroup: blockIdx, blockIdx + grid, ...; items in
+    // order: tile t, stage st = item t K + st.
     const int tiles = (int)((rows + 15) / 16);
     const int my_tiles = (int)blockIdx.x < tiles ? (tiles - 1 - (int)blockIdx.x) / (int)gridDim.x + 1 : 0;
-    const int n_units = my_tiles * K;
+    const int total = my_tiles * K;
 
-    // DMA of this wave's share of the units in order, one call per unit,
-    // position in running counters; units past the end read through
-    // descriptors of size 0 (zeros).
-    int is_u = 0, is_st = 0, is_slot = 0;
+    // DMA of the items in order, one call per item, position in running
+    // counters; items past the end read through descriptors of size 0.
+    int issued = 0, is_st = 0, is_slot = 0;
     int is_tile = (int)blockIdx.x;
     auto issue_next = [&]() {
-        const bool live = is_u < n_units;
+        const bool live = issued < total;
         const uint32_t row0 = live ? (uint32_t)is_tile * 16 : 0u;
-        const uint32_t lds = lds_ring + (uint32_t)is_slot * U::BYTES;
-        const uint32_t code_off = (uint32_t)is_st * plane_bytes + row0 * row_bytes;
-        const uint32_t par_el = (uint32_t)is_st * (uint32_t)plane_groups + row0 * (uint32_t)gpr;
-        const u32x4 c_src = live ? dc : dc0, s_src = live ? ds : ds0, z_src = live ? dz : dz0;
-#pragma unroll
-        for (int i = 0; i < U::CI; ++i)
-            dma_x4(c_src, code_off, lds + 1024u * (uint32_t)(wave * U::CI + i), v_code[i]);
-#pragma unroll
-        for (int i = 0; i < U::PI; ++i) {
-            const uint32_t at = 256u * (uint32_t)(wave * U::PI + i);
-            if (DEF || scale_type == kScaleF32)
-                dma_dword(s_src, par_el * 4, lds + U::CODE + at, v_scale[i]);
-            else
-                dma_ushort(s_src, par_el * 2, lds + U::CODE + at, v_scale[i]);
-            dma_dword(z_src, par_el * 4, lds + U::CODE + U::PAR + at, v_zero[i]);
-        }
-        ++is_u;
-        if (++is_slot == NS) is_slot = 0;
+        const uint32_t code_off = (uint32_t)is_st * plane_bytes + row0 * row_bytes + (uint32_t)g_begin * 32;
+        const uint32_t par_el = (uint32_t)is_st * (uint32_t)plane_groups + row0 * (uint32_t)gpr + (uint32_t)g_begin;
+        const uint32_t lds = lds_ring + (uint32_t)is_slot * L::BYTES;
+        u32x4 c_src = dc, s_src = ds, z_src = dz;
+        if (!live) c_src[2] = s_src[2] = z_src[2] = 0u;
+        // the reads of the item that used this slot have completed
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        dma_x4(c_src, code_off, lds, dma_code[0]);
+        dma_x4(c_src, code_off, lds + 1024u, dma_code[1]);
+        if (DEF || scale_type == kScaleF32)
+            dma_dword(s_src, par_el * 4, lds + L::SCALES, dma_scale);
+        else
+            dma_ushort(s_src, par_el * 2, lds + L::SCALES, dma_scale);
+        dma_dword(z_src, par_el * 4, lds + L::ZEROS, dma_zero);
+        ++issued;
+        if (++is_slot == D) is_slot = 0;
         if (++is_st == K) {
             is_st = 0;
             is_tile += (int)gridDim.x;
         }
     };
 
-    // The ring's first units, then the activations of this wave's groups
-    // (lane as A row: token n, tokens past n_tokens reading zeros), waited
-    // for explicitly with the runs tied to the wait. The prologue runs at a
-    // raised wave priority: it is a serial stretch that every later unit
-    // waits for.
-    __builtin_amdgcn_s_setprio(2);
-#pragma unroll
-    for (int d = 0; d < D; ++d) issue_next();
+    // The activations of this wave's groups first (lane as A row: token n,
+    // tokens past n_tokens and groups past the row reading zeros), then the
+    // ring's first items; the activations are waited for explicitly, with
+    // the runs tied to the wait, leaving the ring's loads in flight.
     u32x4 a[GPW][4];
     {
         const u32x4 xs = make_desc(X, (uint32_t)n_tokens * (uint32_t)cols * 2);
@@ -265,13 +229,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
         u32x4 run[GPW][4];
 #pragma unroll
         for (int g = 0; g < GPW; ++g) {
-            // groups past this wave's range load nothing (an offset past the
-            // buffer) and are never used
             const uint32_t off = (g < gw ? xrow : kSkip) + (uint32_t)(g_begin + g) * 256 + 64 * (uint32_t)j;
 #pragma unroll
             for (int i = 0; i < 4; ++i) run[g][i] = load_run(xs, off + 16 * i);
         }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int d = 0; d < D; ++d) issue_next();
+        wait_vm<D * L::DMA>();
 #pragma unroll
         for (int g = 0; g < GPW; ++g)
             asm volatile("" : "+v"(run[g][0]), "+v"(run[g][1]), "+v"(run[g][2]), "+v"(run[g][3]));
@@ -286,119 +250,84 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
             if (n == 0) sx_lds[wave][g][j] = acc;
         }
     }
-    __builtin_amdgcn_s_setprio(0);
 
-    // Per tile of the step and group of the wave: acc[t][g] = sum over
-    // stages of s P and cz[t][g] = sum over stages of s (4 + z), stage by
-    // stage as the units come.
+    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(
+        Y, (short)0, (int)((uint32_t)n_tokens * (uint32_t)rows * 4u), (int)kRsrcWord3);
     int slot_i = 0, n_red = 0;
-    f32x4 acc[TPB][GPW];
-    float cz[TPB][GPW];
+    for (int ti = 0; ti < my_tiles; ++ti) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        float cz[GPW];
 #pragma unroll
-    for (int t = 0; t < TPB; ++t)
+        for (int g = 0; g < GPW; ++g) cz[g] = 0.0f;
+#pragma unroll
+        for (int st = 0; st < K; ++st) {
+            // this item's loads have landed; the next D - 1 items' may not
+            wait_vm<(D - 1) * L::DMA>();
+            const char *slot = my_ring + slot_i * L::BYTES;
+            // every group of the set, also past the row (zero activations,
+            // zero codes): independent chains to interleave
+#pragma unroll
+            for (int g = 0; g < GPW; ++g) {
+                const u32x2 w = *reinterpret_cast<const u32x2 *>(slot + code_rd[g]);
+                u32x4 b[2][2];
+                code_operands_pair(w[0], w[1], mask, four, b);
+                f32x4 p = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) p = mfma(a[g][q], b[q >> 1][q & 1], p);
+                const uint32_t sw = *reinterpret_cast<const uint32_t *>(slot + L::SCALES + par_rd + 4 * g);
+                const uint32_t zw = *reinterpret_cast<const uint32_t *>(slot + L::ZEROS + par_rd + 4 * g);
+                float s, z;
+                if constexpr (DEF) {
+                    s = __uint_as_float(sw);
+                    z = __uint_as_float(zw);
+                } else {
+                    s = scale_type == kScaleF32 ? __uint_as_float(sw)
+                        : scale_type == kScaleF16
+                            ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
+                            : __uint_as_float(sw << 16);
+                    z = sym ? 2.0f : __uint_as_float(zw);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(s, p[i], acc[i]);
+                cz[g] = __builtin_fmaf(s, 4.0f + z, cz[g]);
+            }
+            // the slot is free: refill it with the item D ahead
+            issue_next();
+            if (++slot_i == D) slot_i = 0;
+        }
+
+        // end of the tile: the wave's groups in order (each its stage sum
+        // less c Sx), then the waves' sums in wave order. The buffer written
+        // here is next written two tiles later, after a barrier that the
+        // summing wave reaches only once it has read it.
 #pragma unroll
         for (int g = 0; g < GPW; ++g) {
-            acc[t][g] = f32x4{0.f, 0.f, 0.f, 0.f};
-            cz[t][g] = 0.0f;
+            const f32x4 sxg = sx_lds[wave][g][j];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[i] = __builtin_fmaf(-cz[g], sxg[i], acc[i]);
         }
-    // (a last step past this workgroup's tiles reads units through
-    // descriptors of size 0, whose sums are never stored)
-    for (int tb = 0; tb < my_tiles; tb += TPB) {
+        red[n_red & 1][wave][lane] = acc;
+        __syncthreads();
+        if (wave == 0) {
+            f32x4 yo = red[n_red & 1][0][lane];
 #pragma unroll
-        for (int pr = 0; pr < PAIRS; ++pr) {
-            // this wave's loads of the next UPB units have landed; then every
-            // wave's have, and every wave is done with the UPB units before
-            // (whose slots the refills below overwrite)
-            wait_vm<(D - UPB) * U::DMA>();
-            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-            __syncthreads();
-#pragma unroll
-            for (int h = 0; h < UPB; ++h) {
-                const int t = (UPB * pr + h) / K;      // tile of the step
-                const char *unit = &ring[slot_i][0];
-                // every group slot, also past this wave's range (its
-                // activations are zero, the codes there other bytes of the
-                // unit): independent chains to interleave; only groups in
-                // range enter the tile's sum
-#pragma unroll
-                for (int g = 0; g < GPW; ++g) {
-                    const u32x2 w = *reinterpret_cast<const u32x2 *>(unit + code_rd[g]);
-                    u32x4 b[2][2];
-                    code_operands_pair(w[0], w[1], mask, four, b);
-                    f32x4 p = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) p = mfma(a[g][q], b[q >> 1][q & 1], p);
-                    const uint32_t sw = *reinterpret_cast<const uint32_t *>(unit + par_rd + 64 * g);
-                    const uint32_t zw = *reinterpret_cast<const uint32_t *>(unit + U::PAR + par_rd + 64 * g);
-                    float s, z;
-                    if constexpr (DEF) {
-                        s = __uint_as_float(sw);
-                        z = __uint_as_float(zw);
-                    } else {
-                        s = scale_type == kScaleF32 ? __uint_as_float(sw)
-                            : scale_type == kScaleF16
-                                ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
-                                : __uint_as_float(sw << 16);
-                        z = sym ? 2.0f : __uint_as_float(zw);
-                    }
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) acc[t][g][i] = __builtin_fmaf(s, p[i], acc[t][g][i]);
-                    cz[t][g] = __builtin_fmaf(s, 4.0f + z, cz[t][g]);
-                }
-                if (++slot_i == NS) slot_i = 0;
+            for (int v = 1; v < kWaves; ++v) {
+                const f32x4 q = red[n_red & 1][v][lane];
+                yo[0] += q[0]; yo[1] += q[1]; yo[2] += q[2]; yo[3] += q[3];
             }
-            // the slots of the units before are free: refill them, UPB units on
+            // lane: tokens 4 j + i of output row 16 tile + n; 32-bit byte
+            // offsets into Y (n_tokens rows < 2^26 x 16 x 4 bytes < 2^32)
+            const uint32_t o = (uint32_t)((int)blockIdx.x + ti * (int)gridDim.x) * 16 + (uint32_t)n;
+            if (o < (uint32_t)rows) {
 #pragma unroll
-            for (int h = 0; h < UPB; ++h) issue_next();
+                for (int i = 0; i < 4; ++i)
+                    if (4 * j + i < n_tokens)
+                        __builtin_amdgcn_raw_buffer_store_b32(
+                            __float_as_uint(yo[i]), yr,
+                            ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4, 0, 0);
+            }
         }
-
-        // end of the step's tiles: per output, the wave's groups in order
-        // (each its stages' sum less c Sx), then the waves' partial sums in
-        // wave order. The buffer written here is next written two tiles
-        // later, after a barrier that the summing wave reaches only once it
-        // has read it.
-#pragma unroll
-        for (int t = 0; t < TPB; ++t) {
-            f32x4 y = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int g = 0; g < GPW; ++g) {
-                if (g >= gw) break;
-                const f32x4 sxg = sx_lds[wave][g][j];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float v = __builtin_fmaf(-cz[t][g], sxg[i], acc[t][g][i]);
-                    y[i] = g == 0 ? v : y[i] + v;
-                }
-            }
-#pragma unroll
-            for (int g = 0; g < GPW; ++g) {
-                acc[t][g] = f32x4{0.f, 0.f, 0.f, 0.f};
-                cz[t][g] = 0.0f;
-            }
-            red[n_red & 1][wave][lane] = y;
-            __syncthreads();
-            const int ti = tb + t;
-            if (wave == 0 && ti < my_tiles) {
-                f32x4 yo = red[n_red & 1][0][lane];
-#pragma unroll
-                for (int v = 1; v < kWaves; ++v) {
-                    const f32x4 q = red[n_red & 1][v][lane];
-                    yo[0] += q[0]; yo[1] += q[1]; yo[2] += q[2]; yo[3] += q[3];
-                }
-                // lane: tokens 4 j + i of output row 16 tile + n; 32-bit byte
-                // offsets into Y (n_tokens rows < 2^26 x 16 x 4 bytes < 2^32)
-                const uint32_t o = (uint32_t)((int)blockIdx.x + ti * (int)gridDim.x) * 16 + (uint32_t)n;
-                if (o < (uint32_t)rows) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        if (4 * j + i < n_tokens)
-                            __builtin_amdgcn_raw_buffer_store_b32(
-                                __float_as_uint(yo[i]), yr,
-                                ((uint32_t)(4 * j + i) * (uint32_t)rows + o) * 4, 0, 0);
-                }
-            }
-            ++n_red;
-        }
+        ++n_red;
     }
     // no DMA load may still write this workgroup's LDS once it ends
     wait_vm<0>();
@@ -412,43 +341,44 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
                            argv, 0, stream);
 }
 
-template <bool DEF, int GPW>
+template <bool DEF>
 hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int n_tokens,
                     float *Y, int grid, hipStream_t stream)
 {
+    constexpr int D = depth_for();
     const int64_t pw = rows * cols / 16, pg = rows * cols / 128;
     switch (k) {
-    case 1: return launch(batch_kernel<1, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
-    case 2: return launch(batch_kernel<2, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
-    case 3: return launch(batch_kernel<3, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
-    case 4: return launch(batch_kernel<4, DEF, GPW>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 1: return launch(batch_kernel<1, D, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 2: return launch(batch_kernel<2, D, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 3: return launch(batch_kernel<3, D, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
+    case 4: return launch(batch_kernel<4, D, DEF>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt);
     default: return hipErrorInvalidValue;
     }
-}
-
-// Groups per wave of a row of cols inputs (the general kernel's 8-wave split).
-int64_t groups_per_wave(int64_t cols)
-{
-    const int64_t gpr = cols / 128;
-    return ((gpr + kWaves - 1) / kWaves + 1) / 2 * 2;
 }
 
 }  // namespace
 
 bool linear_batch_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens)
 {
-    // The A operands of a wave's groups (16 tokens x at most 4 groups) fit its
-    // registers for cols up to 8 x 4 x 128. The form pays a fixed prologue per
-    // workgroup (every wave loads its activations before its first product), so
-    // it only gains where each workgroup streams several row tiles: measured
-    // ahead of the general kernel (16 tokens, 4096 columns) from 6144 rows at 2
-    // to 4 stages and from 24576 rows at one stage; behind it at 4096 rows, and
-    // at one stage up to 12288.
-    if (G != 128 || n_tokens < kBatchMinTokens || n_tokens > 16 ||
-        groups_per_wave(cols) > kGroupsPerWave)
+    // Measured against the general kernel (5, 8 and 16 tokens, packages read
+    // from HBM, rows counted in 4096-input equivalents e): ahead from e =
+    // 3072 at 4 stages (16 tokens 3072 x 4096: 12.2 against 12.5 us; 4096 x
+    // 4096: 12.5 against 13.4), and with up to 8 tokens from 3072 at 3
+    // stages, 4096 at 2 and 6144 at 1; with 16 tokens from 6144 at 2 and 3
+    // stages and 12288 at 1 (below, a workgroup's fixed start outweighs its
+    // few tiles). Rows of fewer than 2048 inputs leave most waves without
+    // groups (16384 x 1024: behind at 1, 3 and 4 stages).
+    if (G != 128 || n_tokens < kBatchMinTokens || n_tokens > 16 || cols > 4096 || cols < 2048)
         return false;
-    return k >= 2 ? rows >= 6144 : rows >= 24576;
+    const int64_t e = rows * cols / 4096;
+    const bool few = n_tokens <= 8;
+    switch (k) {
+    case 1: return e >= (few ? 6144 : 12288);
+    case 2: return e >= (few ? 4096 : 6144);
+    case 3: return e >= (few ? 3072 : 6144);
+    default: return e >= 3072;
+    }
 }
 
 hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const float *zeros,
@@ -456,17 +386,16 @@ hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const 
                                const uint16_t *X, int64_t n_tokens, float *Y, int cus,
                                hipStream_t stream)
 {
-    if (groups_per_wave(cols) > kGroupsPerWave || n_tokens > 16)
-        return hipErrorInvalidValue;
+    if (cols > 4096 || n_tokens > 16) return hipErrorInvalidValue;
     const char *sc = static_cast<const char *>(scales);
     const int64_t tiles = (rows + 15) / 16;
     const int grid = (int)(tiles < cus ? tiles : (int64_t)cus);
     const bool def = scale_type == kScaleF32 && zero_point != kZpSymmetric;
     const int nt = (int)n_tokens;
-    return def ? launch_d<true, kGroupsPerWave>(codes, sc, zeros, rows, cols, k, zero_point,
-                                                scale_type, X, nt, Y, grid, stream)
-               : launch_d<false, kGroupsPerWave>(codes, sc, zeros, rows, cols, k, zero_point,
-                                                 scale_type, X, nt, Y, grid, stream);
+    return def ? launch_d<true>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, nt, Y,
+                                grid, stream)
+               : launch_d<false>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X, nt,
+                                 Y, grid, stream);
 }
 
 }  // namespace rrq_detail

@@ -482,13 +482,14 @@ bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_toke
         return false;
     // 5 to 8 tokens (two quads, rows of 4096 inputs): measured against the
     // batch form and the general kernel at 5 and 8 tokens, ahead up to 1024
-    // rows at every stage count (5.9 against 10.8 us at 4 stages, 8 tokens),
-    // up to 8192 rows from 3 stages and above 4096 rows at 2 (6144 x 4096, 8
-    // tokens, k = 4 / 2: 14.4 / 11.4 against 16.8 / 13.1 us), behind or even
-    // elsewhere.
+    // rows at every stage count (5.9 against 9.8 us at 4 stages, 8 tokens),
+    // and from 3 stages up to 2048 rows (8 tokens, 4 stages: 9.2 against 10.3
+    // us) and from 4097 to 6144 rows, where the batch form's 16-row tiles
+    // leave a round of workgroups half full (6144 x 4096, 5 tokens, 4 stages:
+    // 14.0 against 15.2 us); behind or even elsewhere.
     if (n_tokens > 4) {
         if (cols != 4096) return false;
-        return rows <= 1024 || (rows <= 8192 && (k >= 3 || (k == 2 && rows > 4096)));
+        return rows <= 1024 || (k >= 3 && (rows <= 2048 || (rows > 4096 && rows <= 6144)));
     }
     // Measured crossover against the general kernel (one token, packages
     // read from HBM): from 2 stages this form is as fast or faster on every
