@@ -64,8 +64,9 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
 // launch_linear covers every other case.
 constexpr int kDecodeMaxCols = 16384;
 // The batch form (groups of 128, kBatchMinTokens to 16 tokens, at most 4096
-// cols: the A operands of a wave's groups stay in its registers; and the row
-// and stage counts where it is the faster one: linear_batch_fits).
+// cols: the A operands of a wave's groups stay in its registers; and the
+// row, column, stage and token counts where it is the faster one:
+// linear_batch_fits).
 constexpr int kBatchMinTokens = 5;
 bool linear_batch_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens);
 hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const float *zeros,
