@@ -63,9 +63,9 @@ def counters(directory: str, match):
 KERNEL_SOURCE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "rrq_kernels.hip")
 
 
-def kernel_source_sha256() -> str:
+def kernel_source_sha256(path: str = KERNEL_SOURCE) -> str:
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as fh:
+    with open(path, "rb") as fh:
         return hashlib.sha256(fh.read()).hexdigest()
 
 
@@ -165,12 +165,15 @@ def main(argv=None):
     t.add_argument("--copy-write", required=True)
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--kernel", required=True)
+    t.add_argument("--source", default=KERNEL_SOURCE,
+                   help="the kernel's source file, whose hash the summary records")
     args = ap.parse_args(argv)
     if args.cmd == "traffic":
         r = traffic(args.fetch, args.write, args.copy_fetch, args.copy_write, args.kernel,
                     args.copy_bytes)
         print(f"kernel: `{args.kernel}`")
-        print(f"kernel_source_sha256: `{kernel_source_sha256()}`")
+        print(f"kernel_source: `{os.path.relpath(args.source, os.path.dirname(os.path.dirname(KERNEL_SOURCE)))}`")
+        print(f"kernel_source_sha256: `{kernel_source_sha256(args.source)}`")
         print(f"traffic_bytes_per_launch: `{r['traffic_bytes']:.6e}`")
         print()
         print("| quantity | value |")
