@@ -497,12 +497,17 @@ def stream_probe(src_bytes, flush_buf=None, launches=10):
                        "frac": round(serial_gbs / HBM_PEAK_GBS, 4)}}
 
 
-def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5):
+def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5, n_streams=4):
     """Each weight tensor into its own package (laid out back to back in the
     package buffers), the way a checkpoint stored tensor by tensor is
-    quantized: one rrq_construct call per tensor, and every tensor in one
-    rrq_construct_many call; mean time of one pass over every tensor, HIP
-    events on the launch stream."""
+    quantized: one rrq_construct call per tensor issued from Python on one
+    stream; the same calls spread round-robin over n_streams streams and
+    captured once in a HIP graph (the tensors are independent, so one
+    call's last waves overlap the next calls' first ones, and the host's
+    per-call launch cost leaves the timed pass); and every tensor in one
+    rrq_construct_many call. Mean time of one pass over every tensor, HIP
+    events on the launch stream; the graph's packages are checked equal to
+    the eager calls'."""
     import torch
 
     import paper_2608_04048_amd as rrq
@@ -523,6 +528,33 @@ def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5):
     def many():
         rrq.rrq_construct_many(calls, G, S, stream)
 
+    def package_sum():
+        return (int(codes.sum(dtype=torch.int64)), float(scales.sum(dtype=torch.float64)),
+                float(zeros.sum(dtype=torch.float64)))
+
+    # the per-tensor calls on n_streams streams, captured once (default
+    # priority streams; the capture stream forks to them and joins back)
+    cap = torch.cuda.Stream()
+    side = [torch.cuda.Stream() for _ in range(n_streams)]
+    one_pass()
+    torch.cuda.synchronize()
+    eager_sum = package_sum()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=cap):
+        fork = torch.cuda.Event()
+        fork.record(cap)
+        for sd in side:
+            sd.wait_event(fork)
+        for i, (Wc, r_, c_, cc, sc, zz) in enumerate(calls):
+            rrq.rrq_construct(Wc, r_, c_, G, S, cc, sc, zz, side[i % n_streams])
+        for sd in side:
+            join = torch.cuda.Event()
+            join.record(sd)
+            cap.wait_event(join)
+
+    def graphed():
+        graph.replay()
+
     def timed(fn):
         fn()
         torch.cuda.synchronize()
@@ -541,14 +573,23 @@ def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5):
 
     cb = construct_bytes(n, G, S)
     out = {}
-    for key, fn, ncalls in (("calls", one_pass, len(calls)), ("one_call", many, 1)):
+    for key, fn, ncalls in (("calls", one_pass, len(calls)), ("calls_graph", graphed, len(calls)),
+                            ("one_call", many, 1)):
         t = timed(fn)
-        out[key] = {"api": "rrq_construct" if key == "calls" else "rrq_construct_many",
+        if key == "calls_graph":
+            torch.cuda.synchronize()
+            if package_sum() != eager_sum:
+                raise RuntimeError("bench: the graph-replayed per-tensor packages differ "
+                                   "from the eager calls'")
+        out[key] = {"api": "rrq_construct_many" if key == "one_call" else "rrq_construct",
                     "calls": ncalls, "construct_ms": round(t, 4),
                     "gbs_bf16_weights": round(2 * n / (t * 1e-3) / 1e9, 1),
                     "hbm_gbs": round(cb / (t * 1e-3) / 1e9, 1),
                     "hbm_frac": round(cb / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    out["calls_graph"]["streams"] = n_streams
+    out["calls_graph"]["launch"] = "one HIP graph per pass, calls round-robin over the streams"
     out["tensors"] = len(calls)
+    del graph
     return out
 
 
