@@ -333,8 +333,8 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *   X          device, bfloat16 bit patterns [n_tokens][cols], 16-byte
  *              aligned (read only).
  *   n_tokens   >= 1; the package is read once for up to 16 tokens (the
- *              decode form streams it for up to 4 tokens, and for 5 to 8 on
- *              small packages of rows of 4096 inputs; the batch form for 5
+ *              decode form streams it for up to 4 tokens, and for 5 to 16
+ *              on small packages of rows of 4096 inputs; the batch form for 5
  *              to 16 on packages of 3072 to 12288 rows or more of 2048 to
  *              4096 inputs, by stage and token count), more tokens 16
  *              per pass; from 128 tokens (groups of 128) 64-token tiles run

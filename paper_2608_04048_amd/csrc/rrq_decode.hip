@@ -1,5 +1,5 @@
 // Decode form of the stage-sum linear layer (Eq. 20) for up to 4 tokens (5
-// to 8 on rows of 4096 inputs) and groups of 128: Y[m][o] = sum over stages
+// to 16 on rows of 4096 inputs) and groups of 128: Y[m][o] = sum over stages
 // t < K and groups g of
 // s_t,o,g (sum_i x_m,i Q_t,o,i - z_t,o,g sum_i x_m,i), the product
 // rrq_linear.hip computes for any shape, organised here for streaming the
@@ -18,9 +18,10 @@
 //     A operands (the activations, in pairs (x[v], x[v + 8]) of every 16
 //     inputs) and the group sums Sx (from the same MFMA with a ones operand)
 //     are loaded and formed once and stay in registers.
-// With 5 to 8 tokens (TQ = 2 quads of 4 tokens) each quad has its own A
-// operands and group sums, and a stage's B operands serve both quads' MFMAs:
-// the operand building, most of the instruction count, is shared.
+// With 5 to 8 (9 to 16) tokens, TQ = 2 (4) quads of 4 tokens, each quad has
+// its own A operands and group sums, and a stage's B operands serve every
+// quad's MFMAs: the operand building, most of the instruction count, is
+// shared.
 // Each lane accumulates sum over stages of s P - (sum over stages of
 // s (4 + z)) Sx for its token, row and group (P = sum x (4 + Q) = 4 Sx +
 // sum x Q); the four
@@ -109,10 +110,10 @@ constexpr int sets_per_wave(int sets) { return sets / waves_for(sets); }
 // The rings share the CU's 160 KiB of LDS with the reduction buffers
 // accordingly. With 5 to 8 tokens (two quads of tokens, 8 waves of one set)
 // the A operands take 32 VGPRs: two workgroups per CU, with the larger
-// reduction buffers.
+// reduction buffers; with 9 to 16 (four quads) 64: one.
 constexpr int wgs_per_cu(int wv, int spw, int tq)
 {
-    return wv > 8 ? 1 : tq > 1 ? 2 : spw == 1 ? 3 : 2;
+    return wv > 8 || tq > 2 ? 1 : tq > 1 ? 2 : spw == 1 ? 3 : 2;
 }
 constexpr int ring_bytes(int wv, int spw, int tq)
 {
@@ -460,6 +461,10 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int n_tokens,
                     float *Y, int grid, int batch, hipStream_t stream)
 {
+    if (n_tokens > 8) {   // four quads of tokens, one set of 4 groups per wave
+        if (cols != 4096 || n_tokens > 16) return hipErrorInvalidValue;
+        return launch_s<8, 1, 4, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
+    }
     if (n_tokens > 4) {   // two quads of tokens, one set of 4 groups per wave
         if (cols != 4096 || n_tokens > 8) return hipErrorInvalidValue;
         return launch_s<8, 1, 2, DEF>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, grid, batch, stream);
@@ -477,7 +482,7 @@ hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zero
 
 bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens)
 {
-    if (G != 128 || n_tokens < 1 || n_tokens > 8 || cols % 4096 != 0 ||
+    if (G != 128 || n_tokens < 1 || n_tokens > 16 || cols % 4096 != 0 ||
         cols > kDecodeMaxCols)
         return false;
     // 5 to 8 tokens (two quads, rows of 4096 inputs): measured against the
@@ -487,6 +492,13 @@ bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_toke
     // us) and from 4097 to 6144 rows, where the batch form's 16-row tiles
     // leave a round of workgroups half full (6144 x 4096, 5 tokens, 4 stages:
     // 14.0 against 15.2 us); behind or even elsewhere.
+    // 9 to 16 tokens (four quads, rows of 4096 inputs, one workgroup per CU):
+    // ahead of the general kernel, whose 16-row tiles leave most CUs idle on
+    // so few rows, from 3 stages up to 1024 rows (1024 x 4096, 16 tokens, 4 /
+    // 3 stages: 9.0 / 8.7 against 10.8 / 9.3 us; 256 rows, 4 stages: 8.2
+    // against 9.5); behind at 1 and 2 stages (8.1 against 7.3 us at 2) and
+    // even from 2048 rows.
+    if (n_tokens > 8) return cols == 4096 && rows <= 1024 && k >= 3;
     if (n_tokens > 4) {
         if (cols != 4096) return false;
         return rows <= 1024 || (k >= 3 && (rows <= 2048 || (rows > 4096 && rows <= 6144)));
@@ -507,11 +519,11 @@ hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const
                                 const uint16_t *X, int64_t n_tokens, float *Y, int cus,
                                 hipStream_t stream)
 {
-    if (n_tokens < 1 || n_tokens > 8 || (n_tokens > 4 && cols != 4096)) return hipErrorInvalidValue;
+    if (n_tokens < 1 || n_tokens > 16 || (n_tokens > 4 && cols != 4096)) return hipErrorInvalidValue;
     const char *sc = static_cast<const char *>(scales);
     // Batches of up to 8 tiles, sized so that every resident workgroup
     // gets the same number of batches: R rounds of one batch per workgroup.
-    const int sets = (int)(cols / 512), tq = (int)((n_tokens + 3) / 4);
+    const int sets = (int)(cols / 512), tq = n_tokens > 8 ? 4 : n_tokens > 4 ? 2 : 1;
     const int64_t slots = (int64_t)cus * (tq > 1 ? wgs_per_cu(8, 1, tq)
                                                  : wgs_per_cu(waves_for(sets), sets_per_wave(sets), 1));
     const int64_t tiles = (rows + 3) / 4;

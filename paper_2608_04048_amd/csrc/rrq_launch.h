@@ -58,8 +58,8 @@ hipError_t launch_linear(const uint32_t *codes, const void *scales, const float 
                          hipStream_t stream);
 
 // The decode form of the linear layer (up to 4 tokens, groups of 128, cols
-// a multiple of 4096 up to kDecodeMaxCols, or 5 to 8 tokens on rows of 4096
-// inputs; and the stage counts and row counts where it is the faster one:
+// a multiple of 4096 up to kDecodeMaxCols, or 5 to 16 tokens on rows of 4096
+// inputs; and the stage, row and token counts where it is the faster one:
 // linear_decode_fits);
 // launch_linear covers every other case.
 constexpr int kDecodeMaxCols = 16384;

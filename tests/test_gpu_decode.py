@@ -2,7 +2,8 @@
 cols a multiple of 4096 up to 16384; 2 to 4 stages at any row count, 1 stage
 up to 1024 rows or from 12288 rows with up to 8192 cols; 5 to 8 tokens on
 rows of 4096 inputs, up to 1024 rows at any stage count and from 3 stages up
-to 2048 rows and from 4097 to 6144 rows), through the C ABI,
+to 2048 rows and from 4097 to 6144 rows; 9 to 16 tokens up to 1024 rows from
+3 stages), through the C ABI,
 against the oracle's Eq. 20 product in float64 on sampled output rows.
 
 * exact: power-of-two scales, integer or dyadic zero-points and
@@ -71,6 +72,8 @@ def _run(gpu, codes, s, z, rows, cols, k, xb, zp=None, sd=None, s_raw=None):
     # 5 to 8 tokens: two quads of tokens (the second partly past the last)
     (1024, 4096, 5, 1), (1021, 4096, 8, 2), (3, 4096, 6, 4), (6144, 4096, 8, 4),
     (6000, 4096, 7, 3), (2048, 4096, 5, 3), (4099, 4096, 8, 3), (1999, 4096, 6, 4),
+    # 9 to 16 tokens: four quads (the last partly past the last token)
+    (1024, 4096, 16, 4), (1000, 4096, 12, 3), (3, 4096, 9, 4), (513, 4096, 13, 3),
 ])
 def test_decode_form_exact(gpu, rows, cols, M, k):
     _log(f"decode exact rows={rows} cols={cols} M={M} k={k}")
