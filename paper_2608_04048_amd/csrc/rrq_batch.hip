@@ -296,10 +296,10 @@ __global__ __launch_bounds__(64 * kWaves, 2) void batch_kernel(
             if (++slot_i == D) slot_i = 0;
         }
 
-        // end of the tile: the wave's groups in order (each its stage sum
-        // less c Sx), then the waves' sums in wave order. The buffer written
-        // here is next written two tiles later, after a barrier that the
-        // summing wave reaches only once it has read it.
+        // end of the tile: less each group's c Sx in group order, then the
+        // waves' sums in wave order. The buffer written here is next written
+        // two tiles later, after a barrier that the summing wave reaches only
+        // once it has read it.
 #pragma unroll
         for (int g = 0; g < GPW; ++g) {
             const f32x4 sxg = sx_lds[wave][g][j];
