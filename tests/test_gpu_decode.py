@@ -128,6 +128,35 @@ def test_decode_form_exact_formats(gpu, zp, sd):
     assert np.array_equal(got, ref), np.max(np.abs(got - ref))
 
 
+@pytest.mark.parametrize("zp,sd", [("sym", "f16"), ("real", "f32"), ("int", "bf16")])
+def test_decode_form_exact_formats_four_quads(gpu, zp, sd):
+    """Stage formats through the decode form's four quads of tokens (16
+    tokens on 1000 rows of 4096 inputs, 4 and 3 stages)."""
+    rows, cols, M = 1000, 4096, 16
+    _log(f"decode exact format four quads {zp}/{sd}")
+    rng = np.random.default_rng(78)
+    S = 4
+    codes = rng.integers(0, 2 ** 32, (S, rows * cols // 16), dtype=np.uint64).astype(np.uint32)
+    s = (2.0 ** rng.integers(-4, -1, (S, rows * cols // G))).astype(np.float32)
+    if zp == "sym":
+        z, zv = None, np.full_like(s, 2.0)
+    elif zp == "real":
+        z = (rng.integers(0, 13, s.shape) * 0.25).astype(np.float32)
+        zv = z
+    else:
+        z = rng.integers(0, 4, s.shape).astype(np.float32)
+        zv = z
+    s_raw = (s.astype(np.float16).view(np.uint16) if sd == "f16"
+             else (s.view(np.uint32) >> 16).astype(np.uint16) if sd == "bf16" else s)
+    xb = npo.f32_to_bf16_bits(rng.integers(-4, 5, (M, cols)).astype(np.float32))
+    for k in (4, 3):
+        y = _run(gpu, codes, s, z, rows, cols, k, xb, zp=zp, sd=sd, s_raw=s_raw)
+        idx = _sample_rows(rows, 7)
+        ref = npo.linear(codes, s, zv, rows, cols, G, k, xb, row_index=idx)
+        got = y[:, idx].astype(np.float64)
+        assert np.array_equal(got, ref), (k, np.max(np.abs(got - ref)))
+
+
 @pytest.mark.parametrize("zp,sd", [("int", "f32"), ("sym", "f16"), ("real", "f32")])
 @pytest.mark.parametrize("M", [4, 8])
 def test_decode_form_realistic_within_bound(gpu, zp, sd, M):
