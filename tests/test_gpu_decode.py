@@ -184,3 +184,31 @@ def test_decode_form_realistic_within_bound(gpu, zp, sd, M):
         err = np.abs(y[:, idx].astype(np.float64) - ref)
         assert np.all(err <= tol), f"k={k}: {np.max(err / tol)}"
         _log(f"decode realistic {zp}/{sd} k={k}: max err / bound = {np.max(err / tol):.3g}")
+
+
+@pytest.mark.parametrize("zp,sd", [("int", "f32"), ("sym", "f16")])
+def test_decode_form_four_quads_realistic_within_bound(gpu, zp, sd):
+    """Realistic packages through the four quads of tokens (16 tokens on 1000
+    rows of 4096 inputs, 3 and 4 stages) stay within the stated bound."""
+    rows, cols, M = 1000, 4096, 16
+    rng = np.random.default_rng(19)
+    w = (rng.standard_normal(rows * cols) * 0.02).astype(np.float32)
+    w = np.where(rng.random(w.size) < 1e-3, w * 20, w).astype(np.float32)
+    oc, os_, oz = oracle.c_construct_format(npo.f32_to_bf16_bits(w), G, 4, zp, sd)
+    sv = npo.load_scales(os_, sd)
+    zv = np.full_like(sv, 2.0) if zp == "sym" else oz
+    xb = npo.f32_to_bf16_bits(rng.standard_normal((M, cols)).astype(np.float32))
+    xa = np.abs(npo.bf16_bits_to_f32(xb).reshape(M, cols).astype(np.float64))
+    T = xa.reshape(M, cols // G, G).sum(axis=2)
+    for k in (3, 4):
+        y = _run(gpu, oc, sv, None if zp == "sym" else oz, rows, cols, k, xb, zp=zp, sd=sd,
+                 s_raw=os_)
+        ref = npo.linear(oc, sv, zv, rows, cols, G, k, xb)
+        A = sum(T @ (np.abs(sv[t].astype(np.float64)) * (11 + np.abs(zv[t].astype(np.float64))))
+                .reshape(rows, cols // G).T for t in range(k))
+        p = cols // G
+        n = k * (min(p, 4 * math.ceil(p / 16)) + 1)
+        tol = 1.05 * U * A * (G + 2 * n + 24) + 1e-300
+        err = np.abs(y.astype(np.float64) - ref)
+        assert np.all(err <= tol), f"k={k}: {np.max(err / tol)}"
+        _log(f"decode four quads realistic {zp}/{sd} k={k}: max err / bound = {np.max(err / tol):.3g}")
