@@ -160,7 +160,8 @@ int linear_common(const uint32_t *codes, const void *scales, const float *zeros,
                                             scale_type, X, n_tokens, Y, cus, stream);
     else if (rrq_detail::linear_prefill_fits(rows, cols, group_size, n_tokens))
         e = rrq_detail::launch_linear_prefill(codes, scales, zeros, rows, cols, k_stages,
-                                              zero_point, scale_type, X, n_tokens, Y, stream);
+                                              zero_point, scale_type, X, n_tokens, Y, cus,
+                                              stream);
     else
         e = rrq_detail::launch_linear(codes, scales, zeros, rows, cols, group_size, n_stages,
                                       k_stages, zero_point, scale_type, X, n_tokens, Y, stream);

@@ -73,16 +73,17 @@ hipError_t launch_linear_batch(const uint32_t *codes, const void *scales, const 
                                int64_t rows, int64_t cols, int k, int zero_point, int scale_type,
                                const uint16_t *X, int64_t n_tokens, float *Y, int cus,
                                hipStream_t stream);
-// The prefill form (groups of 128, at least kPrefillMinTokens tokens, 64-token
-// x 64-row tiles). Measured against the general kernel on the Qwen3-8B
-// shapes: from 128 tokens it is faster on all of them (2-3x from 256); below
-// that a matrix of a few thousand rows gives too few tiles to fill the GPU.
+// The prefill form (groups of 128, at least kPrefillMinTokens tokens;
+// 128-token x 128-row tiles when they still give every compute unit one,
+// else 64 x 64). Measured against the general kernel on the Qwen3-8B shapes:
+// from 128 tokens it is faster on all of them (2-3x from 256); below that a
+// matrix of a few thousand rows gives too few tiles to fill the GPU.
 constexpr int kPrefillMinTokens = 128;
 bool linear_prefill_fits(int64_t rows, int64_t cols, int G, int64_t n_tokens);
 hipError_t launch_linear_prefill(const uint32_t *codes, const void *scales, const float *zeros,
                                  int64_t rows, int64_t cols, int k, int zero_point,
                                  int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
-                                 hipStream_t stream);
+                                 int cus, hipStream_t stream);
 bool linear_decode_fits(int64_t rows, int64_t cols, int G, int k, int64_t n_tokens);
 hipError_t launch_linear_decode(const uint32_t *codes, const void *scales, const float *zeros,
                                 int64_t rows, int64_t cols, int k, int zero_point, int scale_type,

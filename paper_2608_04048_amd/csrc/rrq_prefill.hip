@@ -11,22 +11,31 @@
 // sum x Q = P - 4 Sx. Each output accumulates, per group, sum over stages of
 // s P then - (sum over stages of s (4 + z)) Sx.
 //
-// Work: a workgroup of 4 waves owns a tile of 64 tokens x 64 output rows;
-// wave w owns rows 16 w .. 16 w + 15 of it for all 64 tokens, so a B operand
-// (one stage of one group of its 16 rows) feeds 4 MFMAs, and the A operands
-// of a group (its 64 tokens) are built once and serve every stage. The
-// waves walk the groups of a row together: a group's activations (64 tokens
-// x 256 bytes) are staged once in LDS for all 4 waves, each wave stages its
-// own rows' codes, scales and zero-points, all by LDS-DMA loads into a ring
-// of 3 buffers (2 groups in flight while one is computed), with one barrier
-// per group.
+// Work: a workgroup of WV waves owns a tile of 16 T tokens x 16 WV output
+// rows (8 waves and 128 x 128 when that still fills the GPU, else 4 waves
+// and 64 x 64); wave w owns rows 16 w .. 16 w + 15 of it for all 16 T
+// tokens, so a B operand (one stage of one group of its 16 rows) feeds T
+// MFMAs. The waves walk the groups of a row together. A group's
+// activations (16 T tokens x 256 bytes) are staged once in LDS for all the
+// waves, each wave staging its share of T / WV 16-token tiles, and its own
+// rows' codes, scales and zero-points, all by LDS-DMA loads into a ring of
+// 3 buffers (2 groups in flight while one is computed), with one barrier
+// per group. Once its loads of a group have landed, a wave prepares its
+// share of the activations for every wave: it rewrites its tiles in place
+// as A operands (the order the code operands need) and stores their sums Sx
+// in LDS, so that each operand is built and each sum is taken once per
+// workgroup instead of once per wave. A wave prepares group g + 1 when it
+// is done computing group g, and the barrier that opens group g + 1
+// publishes it.
 //
 // Accumulation order: each output is accumulated over 4 contiguous quarters
 // of the groups (quarter length: the groups per wave of the general kernel's
 // 16-token tile, 4 waves, 2-group chunks), starting from 0 each, and the
-// quarters are summed in order, ((Q0 + Q1) + Q2) + Q3: the same operations in
-// the same order as the general kernel, so the results are identical to its
-// and the error bound in rrq.h holds unchanged.
+// quarters are summed in order, ((Q0 + Q1) + Q2) + Q3 (taken as
+// (((+0 + Q0) + Q1) + Q2) + Q3, the same value: a quarter sum is never -0):
+// the same operations in the same order as the general kernel, so the
+// results are identical to its and the error bound in rrq.h holds
+// unchanged.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -34,6 +43,7 @@
 #include "rrq_code_operands.h"
 #include "rrq_dma.h"
 #include "rrq_launch.h"
+
 
 namespace rrq_detail {
 namespace {
@@ -43,9 +53,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kWaves = 4;                      // waves per workgroup, 16 rows each
-constexpr int kTokens = 64;                    // tokens per workgroup tile
-constexpr int kRows = 16 * kWaves;             // output rows per workgroup tile
 constexpr int kBuffers = 3;                    // group ring depth
 constexpr uint32_t kOnePair = 0x3F803F80u;     // two bfloat16 1.0
 constexpr uint32_t kFourPair = 0x40804080u;    // two bfloat16 4.0: code operands 4 + Q
@@ -59,21 +66,27 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, const f32x
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-// One ring buffer (one group): the activations of the tile's 64 tokens (16
-// slots of 16 bytes per token, slot p of token m holding piece p ^ (m % 16)
-// of its 256 bytes, so that the 16 tokens an MFMA reads hit different LDS
-// banks), then per wave its 16 rows' codes (stage t at 1024 (t / 2) +
-// 512 (t % 2), row-major 16 x 32 bytes), scales and zero-points (32-bit
-// words, stage t of row r at 4 (16 t + r)).
-template <int K>
+// One ring buffer (one group) of a tile of 16 T tokens and WV waves: the
+// activations (16 slots of 16 bytes per token, slot p of token m holding
+// piece p ^ (m % 16) of its 256 bytes, so that the 16 tokens an MFMA reads
+// hit different LDS banks; once prepared, the same slots hold the token's A
+// operands), the tokens' sums Sx (one float each), then per wave its 16
+// rows' codes (stage t at 1024 (t / 2) + 512 (t % 2), row-major 16 x 32
+// bytes), scales and zero-points (32-bit words, stage t of row r at
+// 4 (16 t + r)).
+template <int K, int WV, int T>
 struct GroupBuf {
-    static constexpr int X_BYTES = kTokens * 256;
-    static constexpr int X_DMA = X_BYTES / 1024 / kWaves;   // 1 KiB loads per wave
+    static_assert(T % WV == 0, "every wave prepares the same number of token tiles");
+    static constexpr int PT = T / WV;                       // token tiles a wave prepares
+    static constexpr int X_BYTES = 16 * T * 256;
+    static constexpr int SX = X_BYTES;
+    static constexpr int WAVES = SX + 16 * T * 4;
+    static constexpr int X_DMA = 4 * PT;                    // 1 KiB loads per wave
     static constexpr int CODE_DMA = (K + 1) / 2;            // two stages per load
     static constexpr int SCALES = CODE_DMA * 1024;          // within a wave's part
     static constexpr int ZEROS = SCALES + 256;
     static constexpr int WAVE_BYTES = ZEROS + 256;
-    static constexpr int BYTES = X_BYTES + kWaves * WAVE_BYTES;
+    static constexpr int BYTES = WAVES + WV * WAVE_BYTES;
     static constexpr int DMA = X_DMA + CODE_DMA + 2;        // loads per wave per group
 };
 
@@ -93,14 +106,14 @@ __device__ __forceinline__ void act_operands(const u32x4 (&run)[4], u32x4 (&a)[4
     }
 }
 
-template <int K, bool DEF, bool MFMA_PRIO>
-__global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
+template <int K, bool DEF, int WV, int T, bool MFMA_PRIO>
+__global__ __launch_bounds__(64 * WV) void prefill_kernel(
     const uint32_t *__restrict__ codes, const char *__restrict__ scales,
     const float *__restrict__ zeros, int64_t rows, int64_t cols, int64_t plane_words,
     int64_t plane_groups, const uint16_t *__restrict__ X, int64_t n_tokens,
     float *__restrict__ Y, int zero_point, int scale_type, int row_tiles)
 {
-    using B = GroupBuf<K>;
+    using B = GroupBuf<K, WV, T>;
     __shared__ __attribute__((aligned(16))) char buf[kBuffers][B::BYTES];
 
     const int lane = threadIdx.x & 63;
@@ -116,9 +129,9 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 
     // Tiles: consecutive workgroups share the token tile (its activations
     // stay in L2 while the row tiles stream their codes).
-    const int64_t m0 = (int64_t)(blockIdx.x / row_tiles) * kTokens;
-    const int64_t o0 = (int64_t)(blockIdx.x % row_tiles) * kRows + 16 * wave;
-    const uint32_t tokens_here = (uint32_t)(n_tokens - m0 < kTokens ? n_tokens - m0 : kTokens);
+    const int64_t m0 = (int64_t)(blockIdx.x / row_tiles) * (16 * T);
+    const int64_t o0 = (int64_t)(blockIdx.x % row_tiles) * (16 * WV) + 16 * wave;
+    const uint32_t tokens_here = (uint32_t)(n_tokens - m0 < 16 * T ? n_tokens - m0 : 16 * T);
     const int64_t rem = rows - o0;
     const uint32_t rows_here = rem <= 0 ? 0u : (uint32_t)(rem < 16 ? rem : 16);
     const uint32_t gpr = (uint32_t)(cols / 128);        // groups per row
@@ -138,7 +151,8 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
                                sym || !rows_here ? 0u : (K - 1) * zero_plane + rows_here * gpr * 4);
 
     // DMA lane offsets. Activations: this wave's X_DMA loads fill slots
-    // 64 (X_DMA wave + i) + lane, slot s -> token s / 16, piece
+    // 64 (X_DMA wave + i) + lane (the tokens of its token tiles
+    // PT wave .. PT wave + PT - 1), slot s -> token s / 16, piece
     // (s % 16) ^ (token % 16); tokens past the tile read nothing.
     uint32_t dma_x[B::X_DMA];
 #pragma unroll
@@ -164,7 +178,7 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
 #pragma unroll
         for (int i = 0; i < B::X_DMA; ++i)
             dma_x4(dx, g * 256, lds + (uint32_t)(B::X_DMA * wave + i) * 1024, dma_x[i]);
-        const uint32_t lw = lds + B::X_BYTES + (uint32_t)wave * B::WAVE_BYTES;
+        const uint32_t lw = lds + B::WAVES + (uint32_t)wave * B::WAVE_BYTES;
 #pragma unroll
         for (int i = 0; i < B::CODE_DMA; ++i)
             dma_x4(dc, g * 32 + 2u * i * code_plane, lw + 1024u * i, dma_code);
@@ -175,118 +189,174 @@ __global__ __launch_bounds__(64 * kWaves) void prefill_kernel(
         dma_dword(dz, g * 4, lw + B::ZEROS, dma_zero);
     };
 
-    // Quarter length as in the general kernel (4 waves, 2-group chunks).
-    const uint32_t per_q = (((gpr + 3) / 4 + 1) / 2) * 2;
     const u32x4 ones = {one, one, one, one};
-    // MFMA_PRIO (2 to 4 stages, long token runs): the stage products of a
-    // group (its MFMA stretch) are issued at a raised wave priority, so that
-    // the matrix core keeps being fed while the other wave of the SIMD builds
-    // operands (measured 4-9% faster from 1024 tokens; not for short runs).
+    auto token_tile = [&](int q) { return q; };
 
-    f32x4 run[4], cur[4];
+    // This wave's token tiles of buffer b, once its loads have landed: each
+    // lane reads its 64 bytes (token n, inputs 32 j .. 32 j + 31), rewrites
+    // them in place as its four A operands (slot (4 j + i) ^ n then holds
+    // block i) and the tile's sums (the MFMA with a ones operand, lane (n,
+    // j) holding tokens 4 j .. 4 j + 3) go to the group's Sx, from n = 0.
+    // The operands and sums stay in ao, so for the wave's own tiles.
+    auto prepare = [&](int b, u32x4 (&ao)[B::PT][4], f32x4 (&so)[B::PT]) {
+        char *lb = &buf[b][0];
 #pragma unroll
-    for (int tt = 0; tt < 4; ++tt) cur[tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    int quarter = 0;
-
-    issue(0, 0);
-    if (gpr > 1) issue(1, 1);
-    for (uint32_t g = 0; g < gpr; ++g) {
-        // this wave's loads of group g have landed (group g + 1's may not),
-        // and after the barrier every wave's have: the buffer of group
-        // g - 1 is free again
-        if (g + 1 < gpr) wait_vm<B::DMA>(); else wait_vm<0>();
-        __syncthreads();
-        if (g + 2 < gpr) issue(g + 2, (int)((g + 2) % kBuffers));
-        const char *lb = &buf[g % kBuffers][0];
-        const char *lw = lb + B::X_BYTES + wave * B::WAVE_BYTES;
-
-        // per-stage s and c = sum over stages of s (4 + z) for the lane's row
-        float s4[K], c = 0.0f;
-#pragma unroll
-        for (int t = 0; t < K; ++t) {
-            const uint32_t sw = *reinterpret_cast<const uint32_t *>(lw + B::SCALES + 4 * (16 * t + n));
-            const uint32_t zw = *reinterpret_cast<const uint32_t *>(lw + B::ZEROS + 4 * (16 * t + n));
-            float s, z;
-            if constexpr (DEF) {
-                s = __uint_as_float(sw);
-                z = __uint_as_float(zw);
-            } else {
-                s = scale_type == kScaleF32 ? __uint_as_float(sw)
-                    : scale_type == kScaleF16
-                        ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
-                        : __uint_as_float(sw << 16);
-                z = sym ? 2.0f : __uint_as_float(zw);
-            }
-            s4[t] = s;
-            c = __builtin_fmaf(s, 4.0f + z, c);
-        }
-        // A operands and group sums of the 4 token tiles
-        u32x4 a[4][4];
-        f32x4 sx[4];
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-            const char *xt = lb + (16 * tt + n) * 256;
+        for (int q = 0; q < B::PT; ++q) {
+            const int tt = B::PT * wave + q;
+            char *xt = lb + (16 * tt + n) * 256;
             u32x4 runs[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
                 runs[i] = *reinterpret_cast<const u32x4 *>(xt + 16 * ((4 * j + i) ^ n));
-            act_operands(runs, a[tt]);
+            act_operands(runs, ao[q]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                *reinterpret_cast<u32x4 *>(xt + 16 * ((4 * j + i) ^ n)) = ao[q][i];
             f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int b = 0; b < 4; ++b) acc = mfma(a[tt][b], ones, acc);
-            sx[tt] = acc;
+            for (int i = 0; i < 4; ++i) acc = mfma(ao[q][i], ones, acc);
+            so[q] = acc;
+            if (n == 0) *reinterpret_cast<f32x4 *>(lb + B::SX + 4 * (16 * tt + 4 * j)) = acc;
         }
-        if constexpr (MFMA_PRIO) __builtin_amdgcn_s_setprio(1);
+    };
+
+    // A operands and sums of another wave's tile, from LDS.
+    auto read_tile = [&](const char *lb, int tt, u32x4 (&a)[4], f32x4 &sx) {
+        const char *xt = lb + (16 * tt + n) * 256;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            a[i] = *reinterpret_cast<const u32x4 *>(xt + 16 * ((4 * j + i) ^ n));
+        sx = *reinterpret_cast<const f32x4 *>(lb + B::SX + 4 * (16 * tt + 4 * j));
+    };
+
+    // Per-stage s and c = sum over stages of s (4 + z) for the lane's row,
+    // and the code operands of every stage, from this wave's part of a
+    // buffer (its own loads: no barrier needed).
+    float s4[K], c;
+    u32x4 bop[K][2][2];
+    auto params = [&](int b) {
+        const char *lw = &buf[b][0] + B::WAVES + wave * B::WAVE_BYTES;
+        c = 0.0f;
+#pragma unroll
+        for (int t = 0; t < K; ++t) {
+            const uint32_t sw = *reinterpret_cast<const uint32_t *>(lw + B::SCALES + 4 * (16 * t + n));
+            const uint32_t zw = *reinterpret_cast<const uint32_t *>(lw + B::ZEROS + 4 * (16 * t + n));
+            float sc, z;
+            if constexpr (DEF) {
+                sc = __uint_as_float(sw);
+                z = __uint_as_float(zw);
+            } else {
+                sc = scale_type == kScaleF32 ? __uint_as_float(sw)
+                     : scale_type == kScaleF16
+                         ? (float)__builtin_bit_cast(_Float16, (uint16_t)(sw & 0xFFFFu))
+                         : __uint_as_float(sw << 16);
+                z = sym ? 2.0f : __uint_as_float(zw);
+            }
+            s4[t] = sc;
+            c = __builtin_fmaf(sc, 4.0f + z, c);
+        }
 #pragma unroll
         for (int t = 0; t < K; ++t) {
             const u32x2 w = *reinterpret_cast<const u32x2 *>(
                 lw + 1024 * (t >> 1) + 512 * (t & 1) + n * 32 + 8 * j);
-            u32x4 bop[2][2];
-            code_operands_pair(w[0], w[1], mask, four, bop);
+            code_operands_pair(w[0], w[1], mask, four, bop[t]);
+        }
+    };
+
+    f32x4 run[T], cur[T];
 #pragma unroll
-            for (int tt = 0; tt < 4; ++tt) {
-                f32x4 p = {0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < T; ++q) {
+        cur[q] = (f32x4){0.f, 0.f, 0.f, 0.f};
+        run[q] = cur[q];
+    }
+    // One group's stage products for local tile q: per stage s P, then
+    // - c Sx.
+    auto tile = [&](int q, const u32x4 (&a)[4], const f32x4 &sx) {
 #pragma unroll
-                for (int b = 0; b < 4; ++b) p = mfma(a[tt][b], bop[b >> 1][b & 1], p);
+        for (int t = 0; t < K; ++t) {
+            f32x4 pr = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int i = 0; i < 4; ++i) cur[tt][i] = __builtin_fmaf(s4[t], p[i], cur[tt][i]);
-            }
+            for (int b = 0; b < 4; ++b) pr = mfma(a[b], bop[t][b >> 1][b & 1], pr);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) cur[q][i] = __builtin_fmaf(s4[t], pr[i], cur[q][i]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cur[q][i] = __builtin_fmaf(-c, sx[i], cur[q][i]);
+    };
+
+    // Quarter length as in the general kernel (4 waves, 2-group chunks).
+    const uint32_t per_q = (((gpr + 3) / 4 + 1) / 2) * 2;
+    // MFMA_PRIO (2 to 4 stages, long token runs): a group's stage products
+    // (its MFMA stretch) are issued at a raised wave priority, so that the
+    // matrix core keeps being fed while the other waves of the SIMD build
+    // operands.
+    int quarter = 0;
+    u32x4 ao[B::PT][4];
+    f32x4 so[B::PT];
+
+    issue(0, 0);
+    if (gpr > 1) {
+        issue(1, 1);
+        wait_vm<B::DMA>();
+    } else {
+        wait_vm<0>();
+    }
+    prepare(0, ao, so);
+    for (uint32_t g = 0; g < gpr; ++g) {
+        // every wave has prepared group g, and every wave is done with the
+        // buffer of group g - 1: it is free again
+        __syncthreads();
+        if (g + 2 < gpr) issue(g + 2, (int)((g + 2) % kBuffers));
+        const char *lb = &buf[g % kBuffers][0];
+        params((int)(g % kBuffers));
+        u32x4 a_next[4];
+        f32x4 sx_next;
+        read_tile(lb, token_tile(0), a_next, sx_next);
+        if constexpr (MFMA_PRIO) __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int q = 0; q < T; ++q) {
+            u32x4 a[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) a[i] = a_next[i];
+            const f32x4 sx = sx_next;
+            if (q + 1 < T) read_tile(lb, token_tile(q + 1), a_next, sx_next);
+            tile(q, a, sx);
         }
         if constexpr (MFMA_PRIO) __builtin_amdgcn_s_setprio(0);
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) cur[tt][i] = __builtin_fmaf(-c, sx[tt][i], cur[tt][i]);
-        // end of a quarter: fold it into the running sum
+        // end of a quarter: fold it into the running sum (which starts at
+        // +0: a quarter sum is never -0, as it starts at +0 and rounds to
+        // nearest, so +0 + Q0 is Q0 bit for bit)
         if ((g + 1) % per_q == 0 || g + 1 == gpr) {
 #pragma unroll
-            for (int tt = 0; tt < 4; ++tt) {
-                if (quarter == 0) {
-                    run[tt] = cur[tt];
-                } else {
+            for (int q = 0; q < T; ++q) {
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) run[tt][i] = run[tt][i] + cur[tt][i];
-                }
-                cur[tt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+                for (int i = 0; i < 4; ++i) run[q][i] = run[q][i] + cur[q][i];
+                cur[q] = (f32x4){0.f, 0.f, 0.f, 0.f};
             }
             ++quarter;
+        }
+        // this wave's loads of group g + 1 have landed (group g + 2's may
+        // not): prepare its share of them
+        if (g + 1 < gpr) {
+            if (g + 2 < gpr) wait_vm<B::DMA>(); else wait_vm<0>();
+            prepare((int)((g + 1) % kBuffers), ao, so);
         }
     }
     // quarters with no groups add zeros, as the general kernel's idle waves do
     for (; quarter < 4; ++quarter)
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt)
+        for (int q = 0; q < T; ++q)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) run[tt][i] = run[tt][i] + 0.0f;
+            for (int i = 0; i < 4; ++i) run[q][i] = run[q][i] + 0.0f;
 
-    // lane: tokens m0 + 16 tt + 4 j + i of output row o0 + n
+    // lane: tokens m0 + 16 token_tile(q) + 4 j + i of output row o0 + n
     if ((uint32_t)n < rows_here) {
 #pragma unroll
-        for (int tt = 0; tt < 4; ++tt)
+        for (int q = 0; q < T; ++q)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const uint32_t tk = (uint32_t)(16 * tt + 4 * j + i);
-                if (tk < tokens_here) Y[(m0 + tk) * rows + o0 + n] = run[tt][i];
+                const uint32_t tk = (uint32_t)(16 * token_tile(q) + 4 * j + i);
+                if (tk < tokens_here) Y[(m0 + tk) * rows + o0 + n] = run[q][i];
             }
     }
 }
@@ -300,52 +370,80 @@ hipError_t launch(void (*kernel)(Args...), int grid, int block, hipStream_t stre
 }
 
 // From this many tokens the 2-4 stage kernels issue their MFMA stretches at
-// a raised wave priority (A/B: faster from 1024 tokens, slower at 256).
+// a raised wave priority.
 constexpr int64_t kPrefillPrioTokens = 1024;
+
+template <int K, bool DEF, int WV, int T>
+hipError_t launch_t(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
+                    int64_t cols, int zp, int sdt, const uint16_t *X, int64_t n_tokens, float *Y,
+                    hipStream_t stream)
+{
+    const int row_tiles = (int)((rows + 16 * WV - 1) / (16 * WV));
+    const int grid = (int)((int64_t)row_tiles * ((n_tokens + 16 * T - 1) / (16 * T)));
+    const int64_t pw = rows * cols / 16, pg = rows * cols / 128;
+    const bool prio = K > 1 && n_tokens >= kPrefillPrioTokens;
+    return prio ? launch(prefill_kernel<K, DEF, WV, T, true>, grid, 64 * WV, stream, codes, scales,
+                         zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
+                : launch(prefill_kernel<K, DEF, WV, T, false>, grid, 64 * WV, stream, codes, scales,
+                         zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
+}
+
+template <bool DEF, int WV, int T>
+hipError_t launch_k(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
+                    int64_t cols, int k, int zp, int sdt, const uint16_t *X, int64_t n_tokens,
+                    float *Y, hipStream_t stream)
+{
+    switch (k) {
+    case 1: return launch_t<1, DEF, WV, T>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, stream);
+    case 2: return launch_t<2, DEF, WV, T>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, stream);
+    case 3: return launch_t<3, DEF, WV, T>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, stream);
+    case 4: return launch_t<4, DEF, WV, T>(codes, scales, zeros, rows, cols, zp, sdt, X, n_tokens, Y, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+// Tile shape: the large tile (8 waves, 128 rows x 128 tokens: every code
+// operand serves 8 token tiles) when it gives at least 3/4 of the compute
+// units a workgroup, else the small one (4 waves, 64 rows x 64 tokens).
+// Measured on 4096 x 4096, 12288 x 4096 and 4096 x 12288 from 256 to 2048
+// tokens, the large tile is the faster one exactly there.
+bool large_tiles(int64_t rows, int64_t n_tokens, int cus)
+{
+    return 4 * ((rows + 127) / 128) * ((n_tokens + 127) / 128) >= 3 * (int64_t)cus;
+}
 
 template <bool DEF>
 hipError_t launch_d(const uint32_t *codes, const char *scales, const float *zeros, int64_t rows,
                     int64_t cols, int k, int zp, int sdt, const uint16_t *X, int64_t n_tokens,
-                    float *Y, hipStream_t stream)
+                    float *Y, int cus, hipStream_t stream)
 {
-    const int row_tiles = (int)((rows + kRows - 1) / kRows);
-    const int64_t tiles = (int64_t)row_tiles * ((n_tokens + kTokens - 1) / kTokens);
-    const int grid = (int)tiles;
-    const int64_t pw = rows * cols / 16, pg = rows * cols / 128;
-    const bool prio = n_tokens >= kPrefillPrioTokens;
-    switch (k) {
-    case 1: return launch(prefill_kernel<1, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    case 2: return prio ? launch(prefill_kernel<2, DEF, true>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
-                        : launch(prefill_kernel<2, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    case 3: return prio ? launch(prefill_kernel<3, DEF, true>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
-                        : launch(prefill_kernel<3, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    case 4: return prio ? launch(prefill_kernel<4, DEF, true>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles)
-                        : launch(prefill_kernel<4, DEF, false>, grid, 64 * kWaves, stream, codes, scales, zeros, rows, cols, pw, pg, X, n_tokens, Y, zp, sdt, row_tiles);
-    default: return hipErrorInvalidValue;
-    }
+    return large_tiles(rows, n_tokens, cus)
+        ? launch_k<DEF, 8, 8>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream)
+        : launch_k<DEF, 4, 4>(codes, scales, zeros, rows, cols, k, zp, sdt, X, n_tokens, Y, stream);
 }
 
 }  // namespace
 
 bool linear_prefill_fits(int64_t rows, int64_t cols, int G, int64_t n_tokens)
 {
-    // 64-token tiles: the activation descriptor spans 64 rows of X (under
-    // 2^31 bytes), and the grid (row tiles x token tiles) fits an int.
-    const int64_t tiles = ((rows + kRows - 1) / kRows) * ((n_tokens + kTokens - 1) / kTokens);
+    // The activation descriptor spans at most 128 rows of X (under 2^31
+    // bytes), and the grid (row tiles x token tiles, at most 64 x 64 each)
+    // fits an int.
+    const int64_t tiles = ((rows + 63) / 64) * ((n_tokens + 63) / 64);
     return G == 128 && n_tokens >= kPrefillMinTokens && cols <= 65536 && tiles < (1ll << 31);
 }
 
 hipError_t launch_linear_prefill(const uint32_t *codes, const void *scales, const float *zeros,
                                  int64_t rows, int64_t cols, int k, int zero_point,
                                  int scale_type, const uint16_t *X, int64_t n_tokens, float *Y,
-                                 hipStream_t stream)
+                                 int cus, hipStream_t stream)
 {
     const char *sc = static_cast<const char *>(scales);
     const bool def = scale_type == kScaleF32 && zero_point != kZpSymmetric;
     return def ? launch_d<true>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
-                                n_tokens, Y, stream)
+                                n_tokens, Y, cus, stream)
                : launch_d<false>(codes, sc, zeros, rows, cols, k, zero_point, scale_type, X,
-                                 n_tokens, Y, stream);
+                                 n_tokens, Y, cus, stream);
 }
 
 }  // namespace rrq_detail
