@@ -337,9 +337,9 @@ int rrq_reconstruct_format(const uint32_t *codes, const void *scales, const floa
  *              on small packages of rows of 4096 inputs; the batch form for 5
  *              to 16 on packages of 3072 to 12288 rows or more of 2048 to
  *              4096 inputs, by stage and token count), more tokens 16
- *              per pass; from 128 tokens (groups of 128) 64-token tiles run
- *              as a matrix-core product with the 16-token tiles'
- *              accumulation order (the same results).
+ *              per pass; from 128 tokens (groups of 128) tiles of 64 or
+ *              128 tokens run as a matrix-core product with the 16-token
+ *              tiles' accumulation order (the same results).
  *   Y          device, float [n_tokens][rows], 4-byte aligned (written).
  *   stream     HIP stream the work is enqueued on.
  *
