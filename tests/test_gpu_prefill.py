@@ -73,11 +73,38 @@ def test_prefill_exact(gpu, rows, cols, M, k):
     assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
 
 
-@pytest.mark.parametrize("M", [148, 1030])
+def _large_tiles(rows, M):
+    """Whether rrq_linear takes the 128-row x 128-token tiles for this call:
+    when they give at least 3/4 of the compute units a workgroup."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    return 4 * -(-rows // 128) * -(-M // 128) >= 3 * cus
+
+
+# 128 x 128 tiles with ragged edges: 1990 rows leave the last row tile 70 rows
+# (waves 0-3 full, wave 4 six rows, waves 5-7 none), 1500 tokens leave the
+# last token tile 92 (its tiles 6 and 7 without tokens)
+LARGE = [(1990, 1024, 1500), (2048, 1152, 1409)]
+
+
+@pytest.mark.parametrize("rows,cols,M", LARGE)
+@pytest.mark.parametrize("k", [1, 2, 3, 4])
+def test_prefill_exact_large_tiles(gpu, rows, cols, M, k):
+    assert _large_tiles(rows, M)
+    _log(f"prefill exact, large tiles rows={rows} cols={cols} M={M} k={k}")
+    codes, s, z, xb = _exact(rows, cols, M, rows + cols + M + k)
+    y = _run(gpu, codes, s, z, rows, cols, k, xb)
+    ref = npo.linear(codes, s, z, rows, cols, G, k, xb)
+    assert np.all(np.abs(ref) < 2.0 ** 20)
+    bad = np.argwhere(y.astype(np.float64) != ref)
+    assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
+
+
+@pytest.mark.parametrize("rows,M", [(70, 148), (70, 1030), (1990, 1500)])
 @pytest.mark.parametrize("zp,sd", [("sym", "f16"), ("real", "f32"), ("int", "bf16")])
-def test_prefill_exact_formats(gpu, zp, sd, M):
-    rows, cols, k = 70, 2048, 3
-    _log(f"prefill exact format {zp}/{sd} M={M}")
+def test_prefill_exact_formats(gpu, zp, sd, rows, M):
+    cols, k = 2048, 3
+    _log(f"prefill exact format {zp}/{sd} rows={rows} M={M}")
     codes, s, z, xb = _exact(rows, cols, M, 99)
     if zp == "sym":
         zz, zv = None, np.full_like(s, 2.0)
@@ -102,7 +129,8 @@ def _realistic(rows, cols, seed, zp="int", sd="f32"):
 
 
 @pytest.mark.parametrize("rows,cols,M,k", [(300, 4096, 160, 4), (64, 12288, 152, 2),
-                                           (129, 1024, 250, 1), (100, 2048, 1056, 3)])
+                                           (129, 1024, 250, 1), (100, 2048, 1056, 3),
+                                           (1990, 1024, 1504, 4), (1990, 1024, 1504, 2)])
 def test_prefill_equals_16_token_calls(gpu, rows, cols, M, k):
     """The prefill form and the general kernel's 16-token tiles accumulate
     every output in the same order: identical bits on a realistic package.
