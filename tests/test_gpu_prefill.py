@@ -100,6 +100,41 @@ def test_prefill_exact_large_tiles(gpu, rows, cols, M, k):
     assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
 
 
+def _wide_tiles(rows, M):
+    """Whether rrq_linear takes waves of 32 rows at one stage (256 rows x
+    128 tokens per workgroup): when they give every compute unit one."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    return -(-rows // 256) * -(-M // 128) >= cus
+
+
+# one stage, 32-row waves with ragged edges: 3000 rows leave the last row tile
+# 184 rows (waves 0-4 full, wave 5 24 rows: 8 in its second row tile, waves
+# 6 and 7 none), 2700 tokens leave the last token tile 12
+WIDE = (3000, 384, 2700)
+
+
+@pytest.mark.parametrize("zp,sd", [("int", "f32"), ("sym", "f16"), ("real", "f32"), ("int", "bf16")])
+def test_prefill_exact_wide_tiles(gpu, zp, sd):
+    rows, cols, M = WIDE
+    assert _wide_tiles(rows, M)
+    _log(f"prefill exact, 32-row waves {zp}/{sd} rows={rows} cols={cols} M={M}")
+    codes, s, z, xb = _exact(rows, cols, M, 31)
+    if zp == "sym":
+        zz, zv = None, np.full_like(s, 2.0)
+    elif zp == "real":
+        zz = (np.random.default_rng(6).integers(0, 13, s.shape) * 0.25).astype(np.float32)
+        zv = zz
+    else:
+        zz = zv = z
+    s_raw = (s.astype(np.float16).view(np.uint16) if sd == "f16"
+             else (s.view(np.uint32) >> 16).astype(np.uint16) if sd == "bf16" else s)
+    y = _run(gpu, codes, s_raw, zz, rows, cols, 1, xb, zp, sd)
+    ref = npo.linear(codes, s, zv, rows, cols, G, 1, xb)
+    bad = np.argwhere(y.astype(np.float64) != ref)
+    assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
+
+
 @pytest.mark.parametrize("rows,M", [(70, 148), (70, 1030), (1990, 1500)])
 @pytest.mark.parametrize("zp,sd", [("sym", "f16"), ("real", "f32"), ("int", "bf16")])
 def test_prefill_exact_formats(gpu, zp, sd, rows, M):
@@ -130,7 +165,8 @@ def _realistic(rows, cols, seed, zp="int", sd="f32"):
 
 @pytest.mark.parametrize("rows,cols,M,k", [(300, 4096, 160, 4), (64, 12288, 152, 2),
                                            (129, 1024, 250, 1), (100, 2048, 1056, 3),
-                                           (1990, 1024, 1504, 4), (1990, 1024, 1504, 2)])
+                                           (1990, 1024, 1504, 4), (1990, 1024, 1504, 2),
+                                           (3000, 384, 2720, 1)])
 def test_prefill_equals_16_token_calls(gpu, rows, cols, M, k):
     """The prefill form and the general kernel's 16-token tiles accumulate
     every output in the same order: identical bits on a realistic package.
