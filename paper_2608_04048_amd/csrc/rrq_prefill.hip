@@ -16,7 +16,8 @@
 // waves and 64 x 64; at one stage 8 waves of 32 rows, 256 x 128); wave w
 // owns rows 16 NR w .. 16 NR (w + 1) - 1 of it for all 16 T tokens, so a B
 // operand (one stage of one group of 16 rows) feeds T MFMAs and an A
-// operand NR K of them. The waves walk the groups of a row together. A group's
+// operand (16 tokens of a group) NR K of them, one per row tile and stage.
+// The waves walk the groups of a row together. A group's
 // activations (16 T tokens x 256 bytes) are staged once in LDS for all the
 // waves, each wave staging its share of T / WV 16-token tiles, and its own
 // rows' codes, scales and zero-points, all by LDS-DMA loads into a ring of
@@ -44,7 +45,6 @@
 #include "rrq_code_operands.h"
 #include "rrq_dma.h"
 #include "rrq_launch.h"
-
 
 namespace rrq_detail {
 namespace {
