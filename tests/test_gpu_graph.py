@@ -86,7 +86,9 @@ def test_construct_calls_on_streams_in_a_graph(gpu):
     (4096, 12288, 1, 2),     # decode form, 12 waves of two sets
     (24576, 4096, 16, 3),    # batch form
     (4096, 12288, 16, 4),    # general kernel
-    (4096, 4096, 256, 2),    # prefill form
+    (4096, 4096, 256, 2),    # prefill form, 64 x 64 tiles
+    (4096, 4096, 2048, 4),   # prefill form, 128 x 128 tiles
+    (4096, 4096, 2048, 1),   # prefill form, waves of 32 rows
 ])
 def test_linear_calls_in_a_graph(gpu, rows, cols, M, k):
     """rrq_linear on 3 packages captured in one graph: after each of 3
