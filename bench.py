@@ -497,6 +497,48 @@ def stream_probe(src_bytes, flush_buf=None, launches=10):
                        "frac": round(serial_gbs / HBM_PEAK_GBS, 4)}}
 
 
+def machine_probe(iters_issue=20000, iters_lds=4000):
+    """The machine terms the linear-layer kernels are built from, from the
+    probes of libhbm_probe.so (hbm_probe_issue, hbm_probe_lds): s_memtime
+    ticks per wave of a loop of v_mfma_f32_16x16x32_bf16 (16 per iteration,
+    4 chains), of binary32 FMAs (64, 8 chains) and of both interleaved, at 1,
+    2 and 4 waves per SIMD; and of 16-byte LDS reads at 4 and 8 waves per
+    compute unit. Second of two launches each."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    res = {"issue": {}, "lds": {}}
+    for wps in (1, 2, 4):
+        out = torch.empty(cus * wps * 256, dtype=torch.float32, device="cuda")
+        ticks = torch.empty(cus * wps * 4, dtype=torch.int64, device="cuda")
+        per = {}
+        for mode, name in ((0, "mfma16"), (1, "fma64"), (2, "mfma16_fma64")):
+            for _ in range(2):
+                probe.hbm_probe_issue(mode, wps, iters_issue, out, ticks)
+            torch.cuda.synchronize()
+            per[name] = ticks.double().mean().item() / iters_issue
+        res["issue"][str(wps)] = {
+            "ticks_per_iter_per_wave": {k: round(v, 1) for k, v in per.items()},
+            "ticks_per_mfma_per_simd": round(per["mfma16"] / 16 / wps, 2),
+            "ticks_per_fma_per_simd": round(per["fma64"] / 64 / wps, 2),
+            "both_over_mfma": round(per["mfma16_fma64"] / per["mfma16"], 3),
+            "both_over_sum": round(per["mfma16_fma64"] / (per["mfma16"] + per["fma64"]), 3),
+        }
+    for wpc in (4, 8):
+        out = torch.empty(cus * wpc * 64, dtype=torch.int32, device="cuda")
+        ticks = torch.empty(cus * wpc, dtype=torch.int64, device="cuda")
+        for _ in range(2):
+            probe.hbm_probe_lds(wpc, iters_lds, out, ticks)
+        torch.cuda.synchronize()
+        t = ticks.double().mean().item()
+        reads = iters_lds * 16 * wpc                      # per compute unit
+        res["lds"][str(wpc)] = {"ticks_per_read_per_cu": round(t / reads, 2),
+                                "bytes_per_tick_per_cu": round(reads * 1024 / t, 1)}
+    return res
+
+
 def time_per_tensor(w, W_flat, codes, scales, zeros, stream, passes=5, n_streams=4):
     """Each weight tensor into its own package (laid out back to back in the
     package buffers), the way a checkpoint stored tensor by tensor is
@@ -697,6 +739,8 @@ def main():
                     help="prefix stage counts for --linear-shape")
     ap.add_argument("--linear-tokens", default="1", metavar="M,...",
                     help="token counts for --linear-shape")
+    ap.add_argument("--machine-probe", action="store_true",
+                    help="print the instruction-issue and LDS-read probes' figures and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of the benchmark, run a plain device-to-device copy of MIB "
                          "MiB three times (calibrates profiler byte counters)")
@@ -713,6 +757,9 @@ def main():
     from paper_2608_04048_amd import workloads as wl
 
     torch.cuda.set_device(0)
+    if args.machine_probe:
+        print(json.dumps({"machine_probe": machine_probe()}), flush=True)
+        return
     if args.copy_probe:
         src = torch.ones(args.copy_probe << 18, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)

@@ -6,8 +6,9 @@
  * mixed probe reads B bytes and writes 5B/8 bytes with the same kind of wide,
  * coalesced accesses, and no arithmetic; the read-only and write-only probes
  * give each direction's own ceiling, and the construct-pattern and
- * reconstruct-pattern probes replay those kernels' own loads and stores. Measurement aids only: they compute
- * nothing of the method.
+ * reconstruct-pattern probes replay those kernels' own loads and stores; two
+ * machine probes time instruction issue (matrix-core and vector) and LDS
+ * reads. Measurement aids only: they compute nothing of the method.
  */
 #ifndef HBM_PROBE_H
 #define HBM_PROBE_H
@@ -118,6 +119,38 @@ int hbm_probe_construct(const void *W, int64_t n_groups, int32_t group_size, int
 int hbm_probe_reconstruct(const uint32_t *codes, const uint32_t *scales, const uint32_t *zeros,
                           int64_t n_groups, int32_t group_size, int32_t k_stages, uint32_t *out,
                           int32_t blocks_per_cu, hipStream_t stream);
+
+/*
+ * hbm_probe_issue - machine probe of instruction issue: one 4-wave workgroup
+ * per compute unit and waves_per_simd (one wave per SIMD each); every wave
+ * runs iters iterations of, by mode, 0: 16 v_mfma_f32_16x16x32_bf16 on 4
+ * accumulator chains; 1: 64 binary32 FMAs on 8 chains; 2: both. Each wave
+ * writes the s_memtime ticks of its loop to ticks[wave] (global wave index),
+ * each thread a checksum to out (so that no work is folded away).
+ *
+ *   out        device, out_len floats, >= CUs x waves_per_simd x 256.
+ *   ticks      device, ticks_len int64, >= CUs x waves_per_simd x 4.
+ *   waves_per_simd  1 .. 4; iters >= 1.
+ *
+ * Returns 0, 1 (NULL), 3 (bad argument or size) with nothing enqueued, or 7.
+ */
+int hbm_probe_issue(int mode, int waves_per_simd, int iters, float *out, size_t out_len,
+                    long long *ticks, size_t ticks_len, hipStream_t stream);
+
+/*
+ * hbm_probe_lds - machine probe of LDS reads: one workgroup of
+ * waves_per_cu (4 or 8) waves per compute unit on a 96 KiB LDS array; every
+ * wave runs iters iterations of 16 reads of 16 bytes per lane (a wave's
+ * 64 slots distinct) and writes the s_memtime ticks of its loop to
+ * ticks[wave], each thread a checksum to out.
+ *
+ *   out        device, out_len uint32, >= CUs x waves_per_cu x 64.
+ *   ticks      device, ticks_len int64, >= CUs x waves_per_cu.
+ *
+ * Returns as hbm_probe_issue.
+ */
+int hbm_probe_lds(int waves_per_cu, int iters, uint32_t *out, size_t out_len, long long *ticks,
+                  size_t ticks_len, hipStream_t stream);
 
 #ifdef __cplusplus
 }

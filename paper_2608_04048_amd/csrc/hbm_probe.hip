@@ -6,6 +6,10 @@
 // (its tiles, loads, LDS transpose, prefetch and the 16 stores per tile over
 // 12 output planes) with no quantization arithmetic, and the
 // reconstruct-pattern probe does the same for reconstruction (bfloat16 out).
+// Two machine probes time the terms the linear-layer kernels are built from:
+// the issue of v_mfma_f32_16x16x32_bf16 and of binary32 FMAs, alone and
+// interleaved, and 16-byte LDS reads, each wave reporting the clock ticks
+// (s_memtime) of its loop.
 
 #include "hbm_probe.h"
 
@@ -266,6 +270,121 @@ int grid_limit(int per_cu, int64_t work, int per_block, int *grid)
 }
 
 }  // namespace
+
+namespace {
+
+// ---- machine probes ----
+
+typedef float f32x4p __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8p __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4p __attribute__((ext_vector_type(4)));
+
+// Per iteration: NM MFMAs over 4 accumulator chains (distinct operands per
+// chain and round, so that none is folded away) and NV FMAs over 8 chains.
+template <int NM, int NV>
+__global__ __launch_bounds__(256) void issue_probe_kernel(float *out, long long *ticks, int iters)
+{
+    const uint32_t t = threadIdx.x;
+    const u32x4p a0 = {0x3F803F80u ^ t, 0x3F803F81u, 0x3F803F82u, 0x3F803F83u};
+    const u32x4p b0 = {0x3F803F84u, 0x3F803F85u ^ t, 0x3F803F86u, 0x3F803F87u};
+    u32x4p b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) b[i] = b0 ^ (u32x4p){0u, (uint32_t)i << 1, 0u, 0u};
+    f32x4p acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = (f32x4p){0.f, 0.f, 0.f, 0.f};
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = (float)(t + i);
+    u32x4p a = a0;
+    const long long c0 = __builtin_amdgcn_s_memtime();
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+            acc[m & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8p, a), __builtin_bit_cast(bf16x8p, b[m & 3]), acc[m & 3], 0, 0, 0);
+#pragma unroll
+        for (int k = 0; k < NV; ++k) v[k & 7] = __builtin_fmaf(v[k & 7], 1.0001f, 0.5f);
+        a[2] += 1u;
+    }
+    const long long c1 = __builtin_amdgcn_s_memtime();
+    float r = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r += acc[i][0] + acc[i][1] + acc[i][2] + acc[i][3];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) r += v[i];
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + t;
+    out[idx] = r;
+    if ((t & 63) == 0) ticks[idx >> 6] = c1 - c0;
+}
+
+// Each lane reads 16 bytes per instruction from a 96 KiB LDS array (one
+// workgroup per compute unit), distinct 16-byte slots across the wave, 16
+// reads per iteration.
+constexpr int kLdsProbeWords = 24576;   // 96 KiB
+__global__ __launch_bounds__(512) void lds_probe_kernel(uint32_t *out, long long *ticks, int iters)
+{
+    __shared__ __attribute__((aligned(16))) uint32_t buf[kLdsProbeWords];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    for (int i = t; i < kLdsProbeWords; i += blockDim.x) buf[i] = (uint32_t)i * 2654435761u;
+    __syncthreads();
+    u32x4p acc = {0u, 0u, 0u, 0u};
+    const uint32_t base = (uint32_t)(wave * 1024 + lane * 16);
+    const long long c0 = __builtin_amdgcn_s_memtime();
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const uint32_t off = (base + (uint32_t)k * 8192u + (uint32_t)it * 16u) % (4u * kLdsProbeWords);
+            acc ^= *reinterpret_cast<const u32x4p *>(reinterpret_cast<const char *>(buf) + (off & ~15u));
+        }
+    }
+    const long long c1 = __builtin_amdgcn_s_memtime();
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + t;
+    out[idx] = acc[0] ^ acc[1] ^ acc[2] ^ acc[3];
+    if (lane == 0) ticks[idx >> 6] = c1 - c0;
+}
+
+int cu_count()
+{
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    return cus;
+}
+
+}  // namespace
+
+extern "C" int hbm_probe_issue(int mode, int waves_per_simd, int iters, float *out, size_t out_len,
+                               long long *ticks, size_t ticks_len, hipStream_t stream)
+{
+    if (!out || !ticks) return 1;
+    if (mode < 0 || mode > 2 || waves_per_simd < 1 || waves_per_simd > 4 || iters < 1) return 3;
+    const int cus = cu_count();
+    if (cus <= 0) return 7;
+    const int grid = cus * waves_per_simd;              // 4 waves per workgroup, one per SIMD
+    if (out_len < (size_t)grid * 256 || ticks_len < (size_t)grid * 4) return 3;
+    if (mode == 0)
+        hipLaunchKernelGGL((issue_probe_kernel<16, 0>), dim3(grid), dim3(256), 0, stream, out, ticks, iters);
+    else if (mode == 1)
+        hipLaunchKernelGGL((issue_probe_kernel<0, 64>), dim3(grid), dim3(256), 0, stream, out, ticks, iters);
+    else
+        hipLaunchKernelGGL((issue_probe_kernel<16, 64>), dim3(grid), dim3(256), 0, stream, out, ticks, iters);
+    return hipGetLastError() == hipSuccess ? 0 : 7;
+}
+
+extern "C" int hbm_probe_lds(int waves_per_cu, int iters, uint32_t *out, size_t out_len,
+                             long long *ticks, size_t ticks_len, hipStream_t stream)
+{
+    if (!out || !ticks) return 1;
+    if ((waves_per_cu != 4 && waves_per_cu != 8) || iters < 1) return 3;
+    const int cus = cu_count();
+    if (cus <= 0) return 7;
+    const int block = 64 * waves_per_cu;
+    if (out_len < (size_t)cus * block || ticks_len < (size_t)cus * waves_per_cu) return 3;
+    hipLaunchKernelGGL(lds_probe_kernel, dim3(cus), dim3(block), 0, stream, out, ticks, iters);
+    return hipGetLastError() == hipSuccess ? 0 : 7;
+}
 
 extern "C" int hbm_probe_read(const void *src, size_t src_bytes, uint32_t *out,
                               hipStream_t stream)

@@ -1,8 +1,9 @@
 """Binding of libhbm_probe.so (include/hbm_probe.h): streaming kernels used by
 the benchmark as practical HBM ceilings: one with package construction's
 read/write ratio (reads B bytes, writes 5B/8), a read-only and a write-only
-one, and two that replay package construction's and reconstruction's own
-loads and stores."""
+one, two that replay package construction's and reconstruction's own loads
+and stores, and two machine probes (matrix-core and vector instruction
+issue, LDS reads) that report clock ticks per wave."""
 
 from __future__ import annotations
 
@@ -41,6 +42,13 @@ def load_library() -> ctypes.CDLL:
                                               ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
         lib.hbm_probe_reconstruct.restype = ctypes.c_int
+        lib.hbm_probe_issue.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                        ctypes.c_size_t, ctypes.c_void_p, ctypes.c_size_t,
+                                        ctypes.c_void_p]
+        lib.hbm_probe_issue.restype = ctypes.c_int
+        lib.hbm_probe_lds.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
+                                      ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        lib.hbm_probe_lds.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -103,3 +111,22 @@ def hbm_probe_reconstruct(codes, scales, zeros, n_groups: int, group_size: int, 
                                               _ptr(out), int(blocks_per_cu), _sp(stream))
     if st != 0:
         raise RuntimeError(f"hbm_probe_reconstruct failed with status {st}")
+
+
+def hbm_probe_issue(mode: int, waves_per_simd: int, iters: int, out, ticks, stream=None) -> None:
+    """Enqueue the issue probe (mode 0: MFMAs, 1: FMAs, 2: both); out holds
+    CUs x waves_per_simd x 256 floats, ticks CUs x waves_per_simd x 4 int64."""
+    st = load_library().hbm_probe_issue(int(mode), int(waves_per_simd), int(iters), _ptr(out),
+                                        int(out.numel()), _ptr(ticks), int(ticks.numel()),
+                                        _sp(stream))
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_issue failed with status {st}")
+
+
+def hbm_probe_lds(waves_per_cu: int, iters: int, out, ticks, stream=None) -> None:
+    """Enqueue the LDS read probe; out holds CUs x waves_per_cu x 64 uint32,
+    ticks CUs x waves_per_cu int64."""
+    st = load_library().hbm_probe_lds(int(waves_per_cu), int(iters), _ptr(out), int(out.numel()),
+                                      _ptr(ticks), int(ticks.numel()), _sp(stream))
+    if st != 0:
+        raise RuntimeError(f"hbm_probe_lds failed with status {st}")

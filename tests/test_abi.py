@@ -229,8 +229,9 @@ def test_probe_library_exports_declared_function():
     from paper_2608_04048_amd import probe
     text = re.sub(r"/\*.*?\*/", "", open(PROBE_HEADER).read(), flags=re.S)
     names = sorted(set(re.findall(r"\b(hbm_probe_\w+)\s*\(", text)))
-    assert names == ["hbm_probe_construct", "hbm_probe_read", "hbm_probe_reconstruct",
-                     "hbm_probe_stream", "hbm_probe_write"]
+    assert names == ["hbm_probe_construct", "hbm_probe_issue", "hbm_probe_lds",
+                     "hbm_probe_read", "hbm_probe_reconstruct", "hbm_probe_stream",
+                     "hbm_probe_write"]
     lib = probe.load_library()
     out = os.popen(f"nm -D --defined-only {probe.LIB_PATH}").read()
     for name in names:
@@ -302,6 +303,30 @@ def test_reconstruct_probe_rejects(kw, status):
     assert probe.load_library().hbm_probe_reconstruct(
         a["codes"], a["scales"], a["zeros"], a["n_groups"], a["G"], a["k"], a["out"], a["bpc"],
         None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(out=None), 1), (dict(ticks=None), 1), (dict(mode=3), 3), (dict(mode=-1), 3),
+    (dict(wps=0), 3), (dict(wps=5), 3), (dict(iters=0), 3),
+])
+def test_issue_probe_rejects(kw, status):
+    from paper_2608_04048_amd import probe
+    a = dict(mode=0, wps=1, iters=1, out=FAKE, ticks=FAKE)
+    a.update(kw)
+    assert probe.load_library().hbm_probe_issue(a["mode"], a["wps"], a["iters"], a["out"], 1 << 30,
+                                                a["ticks"], 1 << 30, None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(out=None), 1), (dict(ticks=None), 1), (dict(wpc=6), 3), (dict(wpc=16), 3),
+    (dict(iters=0), 3),
+])
+def test_lds_probe_rejects(kw, status):
+    from paper_2608_04048_amd import probe
+    a = dict(wpc=8, iters=1, out=FAKE, ticks=FAKE)
+    a.update(kw)
+    assert probe.load_library().hbm_probe_lds(a["wpc"], a["iters"], a["out"], 1 << 30, a["ticks"],
+                                              1 << 30, None) == status
 
 
 def _linear_status(codes=FAKE, scales=FAKE, zeros=FAKE, rows=64, cols=128, G=128, S=4, k=4,

@@ -2,7 +2,8 @@
 probe packs the first 80 bytes of every 128 bytes of src into dst, the
 read-only probe XORs what it reads, the write-only probe fills, and the
 construct-pattern probe stores XORs of each group's words in rrq_construct's
-planes, and the reconstruct-pattern probe XORs of each chunk's loads."""
+planes, and the reconstruct-pattern probe XORs of each chunk's loads; the
+machine probes report clock ticks that behave as a timing must."""
 
 import numpy as np
 import pytest
@@ -123,3 +124,34 @@ def test_reconstruct_probe_output(gpu, G, n_groups, k, bpc):
     o = out.cpu().numpy().view(np.uint32)
     assert np.array_equal(o[:n // 2], want)
     assert np.all(o[n // 2:] == 0xFFFFFFFF)
+
+
+def test_machine_probes_report_ticks(gpu):
+    """The issue and LDS probes run in bounds and report positive ticks per
+    wave; a loop doing both the MFMAs and the FMAs takes at least as long as
+    either alone (within timing noise), and more waves per SIMD never make a
+    wave's own loop faster."""
+    import torch
+
+    from paper_2608_04048_amd import probe
+    print("machine probes", flush=True)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    per = {}
+    for wps in (1, 2):
+        out = torch.full((cus * wps * 256,), float("nan"), dtype=torch.float32, device="cuda")
+        ticks = torch.zeros(cus * wps * 4, dtype=torch.int64, device="cuda")
+        for mode in (0, 1, 2):
+            probe.hbm_probe_issue(mode, wps, 2000, out, ticks)
+            torch.cuda.synchronize()
+            t = ticks.cpu().numpy()
+            assert np.all(t > 0)
+            assert torch.isfinite(out).all()
+            per[(wps, mode)] = t.mean()
+        assert per[(wps, 2)] >= 0.9 * max(per[(wps, 0)], per[(wps, 1)])
+    assert per[(2, 0)] >= 0.9 * per[(1, 0)]
+    for wpc in (4, 8):
+        out = torch.zeros(cus * wpc * 64, dtype=torch.int32, device="cuda")
+        ticks = torch.zeros(cus * wpc, dtype=torch.int64, device="cuda")
+        probe.hbm_probe_lds(wpc, 400, out, ticks)
+        torch.cuda.synchronize()
+        assert np.all(ticks.cpu().numpy() > 0)
