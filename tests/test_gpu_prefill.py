@@ -114,6 +114,22 @@ def _wide_tiles(rows, M):
 WIDE = (3000, 384, 2700)
 
 
+@pytest.mark.parametrize("rows,M,k", [(2048, 1536, 1), (2048, 1536, 2), (2048, 1536, 4),
+                                      (4096, 2048, 1)])
+def test_prefill_exact_one_group_per_row(gpu, rows, M, k):
+    """Rows of a single group on the 128 x 128 tiles and, at one stage with
+    enough tiles, the 32-row waves: the group ring never holds a second
+    group."""
+    cols = 128
+    assert _large_tiles(rows, M)
+    _log(f"prefill exact, one group per row rows={rows} M={M} k={k}")
+    codes, s, z, xb = _exact(rows, cols, M, rows + M + k)
+    y = _run(gpu, codes, s, z, rows, cols, k, xb)
+    ref = npo.linear(codes, s, z, rows, cols, G, k, xb)
+    bad = np.argwhere(y.astype(np.float64) != ref)
+    assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
+
+
 @pytest.mark.parametrize("zp,sd", [("int", "f32"), ("sym", "f16"), ("real", "f32"), ("int", "bf16")])
 def test_prefill_exact_wide_tiles(gpu, zp, sd):
     rows, cols, M = WIDE
