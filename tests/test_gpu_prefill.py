@@ -223,10 +223,12 @@ def test_prefill_realistic_within_bound(gpu, zp, sd):
         _log(f"prefill realistic {zp}/{sd} k={k}: max err / bound = {np.max(err / tol):.3g}")
 
 
-@pytest.mark.parametrize("rows,cols,k", [(4096, 4096, 4), (12288, 4096, 1)])
+@pytest.mark.parametrize("rows,cols,k", [(4096, 4096, 4), (4096, 4096, 1), (12288, 4096, 4),
+                                          (12288, 4096, 1), (4096, 12288, 4), (4096, 12288, 1)])
 def test_prefill_full_size_sampled(gpu, rows, cols, k):
-    """The benchmark's prefill size (2048 tokens, Qwen3-8B layer shapes, the
-    launch configuration the bench times) on an exact package: sampled rows,
+    """The benchmark's prefill sizes (2048 tokens on the Qwen3-8B q/o,
+    gate/up and down shapes at 1 and 4 stages, the launch configurations the
+    bench times) on an exact package: sampled rows,
     every token, bit-exact."""
     M = 2048
     _log(f"prefill full size rows={rows} cols={cols} M={M} k={k}")
