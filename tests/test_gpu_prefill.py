@@ -242,3 +242,27 @@ def test_prefill_full_size_sampled(gpu, rows, cols, k):
     bad = np.argwhere(got != ref)
     assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
     assert not np.any(np.isnan(y)), "unwritten outputs"
+
+
+@pytest.mark.parametrize("rows,M,k", [(40, 130, 1), (40, 130, 4), (2048, 1536, 4)])
+def test_prefill_widest_rows(gpu, rows, M, k):
+    """Rows of 65536 inputs, the widest the prefill form takes (512 groups,
+    quarters of 128): the small tile with ragged rows and tokens compared in
+    full, and the large tile (16 x 12 tiles of 128) on sampled rows, every
+    token; exact packages, bit-exact."""
+    cols = 65536
+    _log(f"prefill widest rows rows={rows} cols={cols} M={M} k={k}")
+    codes, s, z, xb = _exact(rows, cols, M, rows + M + k)
+    y = _run(gpu, codes, s, z, rows, cols, k, xb)
+    if rows <= 64:
+        idx = np.arange(rows)
+    else:
+        rng = np.random.default_rng(k)
+        idx = np.unique(np.concatenate([np.arange(16), np.arange(rows - 16, rows),
+                                        rng.choice(rows, 16, replace=False)]))
+    ref = npo.linear(codes, s, z, rows, cols, G, k, xb, row_index=idx)
+    assert np.all(np.abs(ref) < 2.0 ** 20)
+    got = y[:, idx].astype(np.float64)
+    bad = np.argwhere(got != ref)
+    assert bad.size == 0, f"{len(bad)} outputs differ, first {bad[:3]}"
+    assert not np.any(np.isnan(y)), "unwritten outputs"
